@@ -1,0 +1,456 @@
+// Append and quantize-on-append kernels (prefill and decode).
+//
+// Every method first writes the new token's key and value into its cache (MetaKV Section 2.1):
+// plain fp16 rows (FP16, H2O, RocketKV), uniform 4-bit group codes, or KVQuant-style codes with
+// per-channel key thresholds calibrated on the prompt and fp16 outliers.  The quantizer steps are
+// written with explicit round-to-nearest float32 operations (__fmul_rn, __fsub_rn, __fdiv_rn)
+// so that codes are reproducible bit for bit.
+#include "kernels_common.h"
+
+namespace mkv {
+
+namespace {
+
+// ---- shared quantizer pieces -----------------------------------------------------------------
+
+MKV_DEV int code_from_mid(float xhat, const float *mid, int nmid) {
+  int c = 0;
+  for (int i = 0; i < nmid; ++i) c += (xhat > mid[i]) ? 1 : 0;
+  return c;
+}
+
+// Pack one code per thread (thread c = channel c, blockDim.x == D) into `row` with the layout
+// of `bits` (4: two per byte, low nibble first; 2: four per byte; 3: a 2-bit plane of D/4 bytes
+// followed by a 1-bit plane of D/8 bytes).  `s_code` is D bytes of LDS.
+template <int D>
+MKV_DEV void pack_row(int code, int bits, uint8_t *s_code, uint8_t *row) {
+  const int c = threadIdx.x;
+  s_code[c] = (uint8_t)code;
+  __syncthreads();
+  if (bits == 4) {
+    if (c < D / 2) row[c] = (uint8_t)(s_code[2 * c] | (s_code[2 * c + 1] << 4));
+  } else if (bits == 2) {
+    if (c < D / 4)
+      row[c] = (uint8_t)(s_code[4 * c] | (s_code[4 * c + 1] << 2) | (s_code[4 * c + 2] << 4) |
+                         (s_code[4 * c + 3] << 6));
+  } else {
+    if (c < D / 4)
+      row[c] = (uint8_t)((s_code[4 * c] & 3) | ((s_code[4 * c + 1] & 3) << 2) |
+                         ((s_code[4 * c + 2] & 3) << 4) | ((s_code[4 * c + 3] & 3) << 6));
+    if (c < D / 8) {
+      uint32_t b = 0;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) b |= (uint32_t)((s_code[8 * c + i] >> 2) & 1) << i;
+      row[D / 4 + c] = (uint8_t)b;
+    }
+  }
+  __syncthreads();
+}
+
+// Inclusive rank among flagged threads of the block (blockDim.x == D <= 128) and the total.
+template <int D>
+MKV_DEV int flag_rank(bool f, int *s_tmp, int *total) {
+  const uint64_t m = __ballot(f);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int before = __popcll(m & ((lane == 0) ? 0ull : (~0ull >> (64 - lane))));
+  if (lane == 0) s_tmp[w] = __popcll(m);
+  __syncthreads();
+  int base = 0, tot = 0;
+  for (int i = 0; i < D / 64; ++i) {
+    if (i < w) base += s_tmp[i];
+    tot += s_tmp[i];
+  }
+  __syncthreads();
+  *total = tot;
+  return base + before;
+}
+
+// KVQ value row of one token: per-token scale = n_ov-th largest |v| (0-based), codes, outliers.
+template <int D>
+MKV_DEV void kvq_value_token(const SeqDesc &sd, int h, int t, uint32_t vbits, const float *cbtab,
+                             float *s_abs, float *s_scale, uint8_t *s_code, int *s_tmp) {
+  const int c = threadIdx.x;
+  const float x = h2f(vbits);
+  const float ax = fabsf(x);
+  s_abs[c] = ax;
+  __syncthreads();
+  int gt = 0, ge = 0;
+  for (int j = 0; j < D; ++j) {
+    const float y = s_abs[j];
+    gt += (y > ax) ? 1 : 0;
+    ge += (y >= ax) ? 1 : 0;
+  }
+  const int nov = sd.bp > 0 ? sd.n_ov : 0;
+  if (gt <= nov && nov < ge) *s_scale = ax;
+  __syncthreads();
+  const float s = *s_scale;
+  const float inv = s > 0.f ? __fdiv_rn(1.0f, s) : 0.f;
+  const float xhat = __fmul_rn(x, inv);
+  const int nc = 1 << sd.bits;
+  const float *mid = cbtab + cb_offset(sd.bits) + 2 * nc + (nc - 1);
+  const int code = code_from_mid(xhat, mid, nc - 1);
+  const bool outl = sd.bp > 0 && ax > s;
+  uint8_t *row = reinterpret_cast<uint8_t *>(sd.vc) + h * stride_codes(sd) + (size_t)t * sd.rowbytes;
+  pack_row<D>(code, sd.bits, s_code, row);
+  int total;
+  const int r = flag_rank<D>(outl, s_tmp, &total);
+  uint32_t *vo = reinterpret_cast<uint32_t *>(sd.vout) + h * stride_vout(sd) + (size_t)t * sd.nov_slots;
+  if (outl && r < sd.nov_slots) vo[r] = ((vbits & 0xFFFFu) << 16) | (uint32_t)c;
+  if (c >= total && c < sd.nov_slots) vo[c] = kNoOutlier;
+  if (c == 0) (reinterpret_cast<float *>(sd.vmeta) + h * stride_slots(sd))[t] = s;
+}
+
+// KVQ key of one token: code under the frozen per-channel threshold, and the outlier flag.
+MKV_DEV int kvq_key_code(const SeqDesc &sd, int h, int c, uint32_t kbits, const float *cbtab, int D,
+                         bool *outl) {
+  const float2 ti = (reinterpret_cast<const float2 *>(sd.kmeta) + (size_t)h * D)[c];
+  const float x = h2f(kbits);
+  const float xhat = __fmul_rn(x, ti.y);
+  const int nc = 1 << sd.bits;
+  const float *mid = cbtab + cb_offset(sd.bits) + 2 * nc;
+  *outl = sd.bp > 0 && fabsf(x) > ti.x;
+  return code_from_mid(xhat, mid, nc - 1);
+}
+
+// UQ value row of one token: 64-channel groups, one wave per group.
+template <int D>
+MKV_DEV void uq_value_token(const SeqDesc &sd, int h, int t, uint32_t vbits) {
+  const int c = threadIdx.x;
+  const float x = h2f(vbits);
+  const float mn = wave_min(x), mx = wave_max(x);
+  const float r = __fsub_rn(mx, mn);
+  const float inv = r > 0.f ? __fdiv_rn(15.0f, r) : 0.f;
+  const float y = __fmul_rn(__fsub_rn(x, mn), inv);
+  const int code = (int)fminf(fmaxf(rintf(y), 0.f), 15.f);
+  const int partner = __shfl_down(code, 1);
+  uint8_t *row = reinterpret_cast<uint8_t *>(sd.vc) + h * stride_codes(sd) + (size_t)t * (D / 2);
+  if ((c & 1) == 0) row[c / 2] = (uint8_t)(code | (partner << 4));
+  if ((c & 63) == 0)
+    (reinterpret_cast<float2 *>(sd.vmeta) + h * stride_uq_vmeta(sd, D))[(size_t)t * (D / 64) + c / 64] =
+        make_float2(mn, __fdiv_rn(r, 15.0f));
+}
+
+// UQ key block: thread c quantizes channel c over 64 tokens read through `get(t)`.
+template <int D, typename Get>
+MKV_DEV void uq_key_block(const SeqDesc &sd, int h, int blk, Get get) {
+  const int c = threadIdx.x;
+  float mn = INFINITY, mx = -INFINITY;
+  for (int t = 0; t < 64; ++t) {
+    const float x = h2f(get(t));
+    mn = fminf(mn, x);
+    mx = fmaxf(mx, x);
+  }
+  const float r = __fsub_rn(mx, mn);
+  const float inv = r > 0.f ? __fdiv_rn(15.0f, r) : 0.f;
+  uint8_t *base = reinterpret_cast<uint8_t *>(sd.kc) + h * stride_codes(sd) + (size_t)blk * 64 * (D / 2);
+  for (int t = 0; t < 64; ++t) {
+    const float x = h2f(get(t));
+    const float y = __fmul_rn(__fsub_rn(x, mn), inv);
+    const int code = (int)fminf(fmaxf(rintf(y), 0.f), 15.f);
+    const int partner = __shfl_down(code, 1);
+    if ((c & 1) == 0) base[(size_t)t * (D / 2) + c / 2] = (uint8_t)(code | (partner << 4));
+  }
+  (reinterpret_cast<float2 *>(sd.kmeta) + h * stride_uq_kmeta(sd, D))[(size_t)blk * D + c] =
+      make_float2(mn, __fdiv_rn(r, 15.0f));
+}
+
+// ---- decode append: one workgroup of D threads per (sequence, kv head) -----------------------
+template <int D>
+__global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict__ seqs, int32_t *state,
+                                                      const uint16_t *__restrict__ k,
+                                                      const uint16_t *__restrict__ v,
+                                                      const float *__restrict__ cbtab, int Hkv) {
+  __shared__ float s_abs[D];
+  __shared__ float s_scale;
+  __shared__ uint8_t s_code[D];
+  __shared__ int s_tmp[4];
+  const int seq = blockIdx.x / Hkv, h = blockIdx.x % Hkv, c = threadIdx.x;
+  const SeqDesc &sd = seqs[seq];
+  int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
+  const int count = st[ST_COUNT], pos = st[ST_NEXT_POS];
+  const uint32_t kb = k[((size_t)seq * Hkv + h) * D + c];
+  const uint32_t vb = v[((size_t)seq * Hkv + h) * D + c];
+  __syncthreads();  // every thread has read the state before thread 0 updates it
+  switch (sd.method) {
+    case FP16: {
+      (reinterpret_cast<uint16_t *>(sd.k) + h * stride_rows(sd, D))[(size_t)count * D + c] = (uint16_t)kb;
+      (reinterpret_cast<uint16_t *>(sd.v) + h * stride_rows(sd, D))[(size_t)count * D + c] = (uint16_t)vb;
+      if (c == 0) st[ST_COUNT] = count + 1;
+      break;
+    }
+    case H2O: {
+      const int slot = st[ST_FREE_SLOT];
+      (reinterpret_cast<uint16_t *>(sd.k) + h * stride_rows(sd, D))[(size_t)slot * D + c] = (uint16_t)kb;
+      (reinterpret_cast<uint16_t *>(sd.v) + h * stride_rows(sd, D))[(size_t)slot * D + c] = (uint16_t)vb;
+      __syncthreads();
+      if (c == 0) {
+        (reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd))[slot] = pos;
+        (reinterpret_cast<float *>(sd.score) + h * stride_slots(sd))[slot] = 0.f;
+        st[ST_COUNT] = count + 1;
+        st[ST_FREE_SLOT] = count + 1;
+      }
+      break;
+    }
+    case ROCKET: {
+      (reinterpret_cast<uint16_t *>(sd.k) + h * stride_rows(sd, D))[(size_t)count * D + c] = (uint16_t)kb;
+      (reinterpret_cast<uint16_t *>(sd.v) + h * stride_rows(sd, D))[(size_t)count * D + c] = (uint16_t)vb;
+      (reinterpret_cast<uint16_t *>(sd.kcm) + h * stride_rows(sd, D))[(size_t)c * sd.cap + count] = (uint16_t)kb;
+      if (c == 0) {
+        (reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd))[count] = pos;
+        st[ST_COUNT] = count + 1;
+      }
+      break;
+    }
+    case UQ: {
+      uq_value_token<D>(sd, h, count, vb);
+      uint16_t *res = reinterpret_cast<uint16_t *>(sd.kres) + (size_t)h * 64 * D;
+      res[(size_t)(count & 63) * D + c] = (uint16_t)kb;
+      if ((count & 63) == 63) {
+        // the block is complete: thread c quantizes channel c of the 64 residual rows it wrote
+        __syncthreads();
+        uq_key_block<D>(sd, h, count >> 6, [&](int t) { return (uint32_t)res[(size_t)t * D + c]; });
+      }
+      if (c == 0) st[ST_COUNT] = count + 1;
+      break;
+    }
+    case KVQ: {
+      bool outl;
+      const int code = kvq_key_code(sd, h, c, kb, cbtab, D, &outl);
+      uint8_t *row = reinterpret_cast<uint8_t *>(sd.kc) + h * stride_codes(sd) + (size_t)count * sd.rowbytes;
+      pack_row<D>(code, sd.bits, s_code, row);
+      int total;
+      const int r = flag_rank<D>(outl, s_tmp, &total);
+      const int fill = st[ST_KOUT_FILL];
+      uint32_t *ko = reinterpret_cast<uint32_t *>(sd.kout) + h * stride_kout(sd);
+      if (outl) ko[fill + r] = ((kb & 0xFFFFu) << 16) | (uint32_t)c;
+      kvq_value_token<D>(sd, h, count, vb, cbtab, s_abs, &s_scale, s_code, s_tmp);
+      __syncthreads();
+      if (c == 0) {
+        (reinterpret_cast<uint32_t *>(sd.krow) + h * stride_krow(sd))[count + 1] = (uint32_t)(fill + total);
+        st[ST_KOUT_FILL] = fill + total;
+        st[ST_COUNT] = count + 1;
+      }
+      break;
+    }
+    default:
+      break;
+  }
+  if (c == 0) st[ST_NEXT_POS] = pos + 1;
+}
+
+// ---- prefill -----------------------------------------------------------------------------------
+
+// Copy prompt rows [n0][Hkv][D] (input layout) into per-head rows [Hkv][n0 or cap][D].
+template <int D>
+__global__ void k_prefill_copy(const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
+                               uint16_t *dk, uint16_t *dv, int64_t head_stride, int n0, int Hkv) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // one 16-byte chunk
+  const int64_t total = (int64_t)n0 * Hkv * (D / 8);
+  if (i >= total) return;
+  const int ch = (int)(i % (D / 8));
+  const int h = (int)((i / (D / 8)) % Hkv);
+  const int64_t t = i / ((D / 8) * Hkv);
+  const uint4 a = reinterpret_cast<const uint4 *>(k)[i];
+  const uint4 b = reinterpret_cast<const uint4 *>(v)[i];
+  *reinterpret_cast<uint4 *>(dk + h * head_stride + t * D + ch * 8) = a;
+  *reinterpret_cast<uint4 *>(dv + h * head_stride + t * D + ch * 8) = b;
+}
+
+template <int D>
+__global__ __launch_bounds__(128) void k_prefill_uq_values(const SeqDesc *__restrict__ seqs, int seq,
+                                                          const uint16_t *__restrict__ v, int Hkv) {
+  const SeqDesc &sd = seqs[seq];
+  const int t = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
+  uq_value_token<D>(sd, h, t, v[((size_t)t * Hkv + h) * D + c]);
+}
+
+template <int D>
+__global__ __launch_bounds__(128) void k_prefill_uq_keys(const SeqDesc *__restrict__ seqs, int seq,
+                                                        const uint16_t *__restrict__ k, int Hkv, int n0) {
+  const SeqDesc &sd = seqs[seq];
+  const int blk = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
+  const int nfull = n0 / 64;
+  if (blk < nfull) {
+    uq_key_block<D>(sd, h, blk, [&](int t) { return (uint32_t)k[((size_t)(blk * 64 + t) * Hkv + h) * D + c]; });
+  } else {
+    uint16_t *res = reinterpret_cast<uint16_t *>(sd.kres) + (size_t)h * 64 * D;
+    for (int t = nfull * 64; t < n0; ++t) res[(size_t)(t & 63) * D + c] = k[((size_t)t * Hkv + h) * D + c];
+  }
+}
+
+// KVQ key thresholds: thread c finds the n_o-th largest |k| (0-based) of channel c over the prompt
+// by a two-pass radix select on the 15-bit fp16 magnitude, with a private 256-bin histogram.
+template <int D>
+__global__ __launch_bounds__(128) void k_kvq_calibrate(const SeqDesc *__restrict__ seqs, int seq,
+                                                      const uint16_t *__restrict__ k, int Hkv, int n0) {
+  __shared__ uint16_t hist[D][256];
+  const SeqDesc &sd = seqs[seq];
+  const int h = blockIdx.x, c = threadIdx.x;
+  const int want = sd.bp > 0 ? sd.n_o : 0;   // 0-based rank from the top
+  float tau = 0.f;
+  if (want < n0) {
+    uint32_t hi_sel = 0;
+    int remaining = want + 1;   // 1-based rank
+    for (int pass = 0; pass < 2; ++pass) {
+      for (int b = 0; b < 256; ++b) hist[c][b] = 0;
+      for (int t = 0; t < n0; ++t) {
+        const uint32_t key = k[((size_t)t * Hkv + h) * D + c] & 0x7FFFu;
+        if (pass == 0) hist[c][key >> 8]++;
+        else if ((key >> 8) == hi_sel) hist[c][key & 255u]++;
+      }
+      int cum = 0, dg = 0;
+      for (int b = 255; b >= 0; --b) {
+        if (cum + hist[c][b] >= remaining) { dg = b; break; }
+        cum += hist[c][b];
+      }
+      remaining -= cum;
+      if (pass == 0) hi_sel = (uint32_t)dg;
+      else tau = h2f((hi_sel << 8) | (uint32_t)dg);
+    }
+  }
+  const float inv = tau > 0.f ? __fdiv_rn(1.0f, tau) : 0.f;
+  (reinterpret_cast<float2 *>(sd.kmeta) + (size_t)h * D)[c] = make_float2(tau, inv);
+}
+
+// KVQ prompt keys, pass 1 (write codes, count outliers per token into krow[t+1]) or pass 2
+// (write the outlier entries at their CSR offsets).
+template <int D>
+__global__ __launch_bounds__(128) void k_kvq_keys(const SeqDesc *__restrict__ seqs, int seq,
+                                                 const uint16_t *__restrict__ k, const float *__restrict__ cbtab,
+                                                 int Hkv, int pass) {
+  __shared__ uint8_t s_code[D];
+  __shared__ int s_tmp[4];
+  const SeqDesc &sd = seqs[seq];
+  const int t = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
+  const uint32_t kb = k[((size_t)t * Hkv + h) * D + c];
+  bool outl;
+  const int code = kvq_key_code(sd, h, c, kb, cbtab, D, &outl);
+  uint32_t *krow = reinterpret_cast<uint32_t *>(sd.krow) + h * stride_krow(sd);
+  if (pass == 0) {
+    uint8_t *row = reinterpret_cast<uint8_t *>(sd.kc) + h * stride_codes(sd) + (size_t)t * sd.rowbytes;
+    pack_row<D>(code, sd.bits, s_code, row);
+    int total;
+    flag_rank<D>(outl, s_tmp, &total);
+    if (c == 0) krow[t + 1] = (uint32_t)total;
+  } else {
+    int total;
+    const int r = flag_rank<D>(outl, s_tmp, &total);
+    if (outl) (reinterpret_cast<uint32_t *>(sd.kout) + h * stride_kout(sd))[krow[t] + r] =
+        ((kb & 0xFFFFu) << 16) | (uint32_t)c;
+  }
+}
+
+// In-place inclusive scan of krow[1..n0] (per-token outlier counts) per kv head.
+__global__ __launch_bounds__(256) void k_kvq_scan(const SeqDesc *__restrict__ seqs, int seq, int32_t *state,
+                                                  int Hkv, int n0) {
+  __shared__ int s_tmp[4];
+  const SeqDesc &sd = seqs[seq];
+  const int h = blockIdx.x;
+  uint32_t *krow = reinterpret_cast<uint32_t *>(sd.krow) + h * stride_krow(sd);
+  int run = 0;
+  for (int a = 0; a < n0; a += 256) {
+    const int i = a + (int)threadIdx.x;
+    const int x = (i < n0) ? (int)krow[i + 1] : 0;
+    int total;
+    const int ex = block_exclusive_scan<256>(x, s_tmp, &total);
+    if (i < n0) krow[i + 1] = (uint32_t)(run + ex + x);
+    run += total;
+  }
+  if (threadIdx.x == 0) {
+    krow[0] = 0;
+    state[((size_t)seq * Hkv + h) * ST_WORDS + ST_KOUT_FILL] = run;
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(128) void k_prefill_kvq_values(const SeqDesc *__restrict__ seqs, int seq,
+                                                           const uint16_t *__restrict__ v,
+                                                           const float *__restrict__ cbtab, int Hkv) {
+  __shared__ float s_abs[D];
+  __shared__ float s_scale;
+  __shared__ uint8_t s_code[D];
+  __shared__ int s_tmp[4];
+  const SeqDesc &sd = seqs[seq];
+  const int t = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
+  kvq_value_token<D>(sd, h, t, v[((size_t)t * Hkv + h) * D + c], cbtab, s_abs, &s_scale, s_code, s_tmp);
+}
+
+__global__ void k_prefill_state(const SeqDesc *__restrict__ seqs, int seq, int32_t *state, int Hkv) {
+  const SeqDesc &sd = seqs[seq];
+  const int h = threadIdx.x;
+  if (h >= Hkv) return;
+  int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
+  const bool staged = sd.method == H2O || sd.method == ROCKET;
+  st[ST_COUNT] = staged ? 0 : sd.n0;
+  st[ST_NEXT_POS] = sd.n0;
+  st[ST_FREE_SLOT] = 0;
+  st[ST_KEPT] = sd.n0;
+}
+
+__global__ void k_init_state(int32_t *state, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) state[i] = 0;
+}
+
+template <int D>
+hipError_t append_decode_impl(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
+                              hipStream_t st) {
+  hipLaunchKernelGGL(k_append_decode<D>, dim3(sh.S * sh.Hkv), dim3(D), 0, st, dv.seqs, dv.state, k, v,
+                     dv.cbtab, sh.Hkv);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t prefill_impl(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq, const uint16_t *k,
+                        const uint16_t *v, hipStream_t st) {
+  const int n0 = hs.n0, Hkv = sh.Hkv;
+  hipLaunchKernelGGL(k_prefill_state, dim3(1), dim3(64 * ((Hkv + 63) / 64)), 0, st, dv.seqs, seq, dv.state, Hkv);
+  switch (hs.method) {
+    case FP16:
+    case H2O:
+    case ROCKET: {
+      const bool staged = hs.method != FP16;
+      uint16_t *dk = reinterpret_cast<uint16_t *>(staged ? hs.stage_k : hs.k);
+      uint16_t *dvp = reinterpret_cast<uint16_t *>(staged ? hs.stage_v : hs.v);
+      const int64_t hstride = staged ? stride_stage(hs, D) : stride_rows(hs, D);
+      const int64_t chunks = (int64_t)n0 * Hkv * (D / 8);
+      hipLaunchKernelGGL(k_prefill_copy<D>, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, st, k, v,
+                         dk, dvp, hstride, n0, Hkv);
+      break;
+    }
+    case UQ:
+      hipLaunchKernelGGL(k_prefill_uq_values<D>, dim3(n0, Hkv), dim3(D), 0, st, dv.seqs, seq, v, Hkv);
+      hipLaunchKernelGGL(k_prefill_uq_keys<D>, dim3(n0 / 64 + 1, Hkv), dim3(D), 0, st, dv.seqs, seq, k, Hkv, n0);
+      break;
+    case KVQ:
+      hipLaunchKernelGGL(k_kvq_calibrate<D>, dim3(Hkv), dim3(D), 0, st, dv.seqs, seq, k, Hkv, n0);
+      hipLaunchKernelGGL(k_kvq_keys<D>, dim3(n0, Hkv), dim3(D), 0, st, dv.seqs, seq, k, dv.cbtab, Hkv, 0);
+      hipLaunchKernelGGL(k_kvq_scan, dim3(Hkv), dim3(256), 0, st, dv.seqs, seq, dv.state, Hkv, n0);
+      hipLaunchKernelGGL(k_kvq_keys<D>, dim3(n0, Hkv), dim3(D), 0, st, dv.seqs, seq, k, dv.cbtab, Hkv, 1);
+      hipLaunchKernelGGL(k_prefill_kvq_values<D>, dim3(n0, Hkv), dim3(D), 0, st, dv.seqs, seq, v, dv.cbtab, Hkv);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_append_decode(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
+                                hipStream_t st) {
+  return sh.D == 64 ? append_decode_impl<64>(dv, sh, k, v, st) : append_decode_impl<128>(dv, sh, k, v, st);
+}
+
+hipError_t launch_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq, const uint16_t *k,
+                              const uint16_t *v, hipStream_t st) {
+  return sh.D == 64 ? prefill_impl<64>(dv, sh, hs, seq, k, v, st) : prefill_impl<128>(dv, sh, hs, seq, k, v, st);
+}
+
+hipError_t launch_init_state(const Dev &dv, const Shape &sh, hipStream_t st) {
+  const int n = sh.S * sh.Hkv * ST_WORDS;
+  hipLaunchKernelGGL(k_init_state, dim3((n + 255) / 256), dim3(256), 0, st, dv.state, n);
+  return hipGetLastError();
+}
+
+}  // namespace mkv

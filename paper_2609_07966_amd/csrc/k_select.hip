@@ -1,0 +1,603 @@
+// Token-selection kernels: RocketKV top-k, H2O eviction, H2O and SnapKV prefill eviction.
+//
+// MetaKV Section 2.1: H2O keeps the tokens with the highest accumulated attention and evicts the
+// lowest-scoring older token once over budget; RocketKV first keeps the prompt tokens the
+// observation window votes for (SnapKV), then attends to a top-k subset per decode step.
+// Selections are block-wide radix selects on order-preserving 32-bit keys followed by an
+// ascending-position compaction, so ties resolve by position exactly as specified.
+#include "kernels_common.h"
+
+namespace mkv {
+
+namespace {
+
+constexpr int NT = 256;
+
+// Compact positions [0, n) whose flag is set into ascending slots; calls emit(j, slot) for each.
+// flag(j, eq_before) may use eq_before = number of keys equal to the threshold at indices < j.
+template <typename Flag, typename IsEq, typename Emit>
+MKV_DEV int compact_ascending(int n, Flag flag, IsEq is_eq, Emit emit, int *s_tmp) {
+  int run = 0, eq_run = 0;
+  for (int a = 0; a < n; a += NT) {
+    const int j = a + (int)threadIdx.x;
+    const bool in = j < n;
+    const int e = (in && is_eq(j)) ? 1 : 0;
+    int eq_tot;
+    const int eq_before = eq_run + block_exclusive_scan<NT>(e, s_tmp, &eq_tot);
+    const int f = (in && flag(j, eq_before)) ? 1 : 0;
+    int tot;
+    const int ex = block_exclusive_scan<NT>(f, s_tmp, &tot);
+    if (f) emit(j, run + ex);
+    run += tot;
+    eq_run += eq_tot;
+  }
+  return run;
+}
+
+// ---- RocketKV decode top-k ---------------------------------------------------------------------
+template <int D, int G>
+__global__ __launch_bounds__(NT) void k_topk(const SeqDesc *__restrict__ seqs, int32_t *state,
+                                             const uint16_t *__restrict__ q, int32_t *pos_out, int topk_max,
+                                             int Hkv) {
+  __shared__ float s_a[D];
+  __shared__ float s_qb[D];
+  __shared__ int s_ch[D];
+  __shared__ int hist[256];
+  __shared__ int s3[3];
+  __shared__ int s_tmp[NT / 64];
+  const int seq = blockIdx.x / Hkv, h = blockIdx.x % Hkv;
+  const SeqDesc &sd = seqs[seq];
+  if (sd.method != ROCKET) return;
+  int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
+  const int n = st[ST_COUNT];
+  const int k = sd.topk;
+  int32_t *sel = reinterpret_cast<int32_t *>(sd.sel) + h * stride_sel(sd);
+  const int32_t *pos = reinterpret_cast<const int32_t *>(sd.pos) + h * stride_slots(sd);
+  int32_t *chan_out = reinterpret_cast<int32_t *>(sd.aux1) + (size_t)h * D;
+  const int Hq = Hkv * G;
+  const uint16_t *qh = q + ((size_t)seq * Hq + h * G) * D;
+
+  // channel magnitudes and head sums, float32 in ascending head order
+  for (int c = threadIdx.x; c < D; c += NT) {
+    float a = 0.f, qb = 0.f;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float x = h2f(qh[(size_t)g * D + c]);
+      a = __fadd_rn(a, fabsf(x));
+      qb = __fadd_rn(qb, x);
+    }
+    s_a[c] = a;
+    s_qb[c] = qb;
+  }
+  __syncthreads();
+  const int nch = min(sd.nch, D);
+  // channel c is selected iff fewer than nch channels beat it (larger a, or equal a and lower index)
+  for (int c = threadIdx.x; c < D; c += NT) {
+    const float a = s_a[c];
+    int beats = 0;
+    for (int c2 = 0; c2 < D; ++c2) {
+      const float b = s_a[c2];
+      beats += (b > a || (b == a && c2 < c)) ? 1 : 0;
+    }
+    s_ch[c] = beats < nch ? 1 : 0;
+  }
+  __syncthreads();
+  __shared__ int s_sel_ch[D];
+  __shared__ float s_sel_qb[D];
+  if (threadIdx.x == 0) {
+    int m = 0;
+    for (int c = 0; c < D; ++c)
+      if (s_ch[c]) {
+        s_sel_ch[m] = c;
+        s_sel_qb[m] = s_qb[c];
+        ++m;
+      }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nch; i += NT) chan_out[i] = s_sel_ch[i];
+
+  if (k >= n) {
+    for (int j = threadIdx.x; j < n; j += NT) sel[j] = j;
+    if (pos_out != nullptr)
+      for (int i = threadIdx.x; i < topk_max; i += NT)
+        pos_out[((size_t)seq * Hkv + h) * topk_max + i] = i < n ? pos[i] : -1;
+    if (threadIdx.x == 0) st[ST_SEL_COUNT] = n;
+    return;
+  }
+
+  // approximate scores from the channel-major key copy: one lane per token, channels ascending,
+  // acc = fl32(acc + fl32(qbar_c * k_jc))
+  const uint16_t *kcm = reinterpret_cast<const uint16_t *>(sd.kcm) + h * stride_rows(sd, D);
+  uint32_t *akeys = reinterpret_cast<uint32_t *>(sd.akeys) + h * stride_slots(sd);
+  for (int j = threadIdx.x; j < n; j += NT) {
+    float acc = 0.f;
+    for (int i = 0; i < nch; ++i) acc = __fadd_rn(acc, __fmul_rn(s_sel_qb[i], h2f(kcm[(size_t)s_sel_ch[i] * sd.cap + j])));
+    akeys[j] = float_key(acc);
+  }
+  __syncthreads();
+  uint32_t kth;
+  int n_eq, need;
+  radix_select_kth<NT>(n, k, [&](int i) { return akeys[i]; }, hist, s3, &kth, &n_eq, &need);
+  compact_ascending(
+      n, [&](int j, int eq_before) { const uint32_t kk = akeys[j]; return kk > kth || (kk == kth && eq_before < need); },
+      [&](int j) { return akeys[j] == kth; }, [&](int j, int slot) { if (slot < k) sel[slot] = j; }, s_tmp);
+  __syncthreads();
+  if (pos_out != nullptr)
+    for (int i = threadIdx.x; i < topk_max; i += NT)
+      pos_out[((size_t)seq * Hkv + h) * topk_max + i] = i < k ? pos[sel[i]] : -1;
+  if (threadIdx.x == 0) st[ST_SEL_COUNT] = k;
+}
+
+// ---- H2O decode eviction ------------------------------------------------------------------------
+__global__ __launch_bounds__(NT) void k_h2o_evict(const SeqDesc *__restrict__ seqs, int32_t *state, int Hkv) {
+  __shared__ unsigned long long s_best[NT / 64];
+  const int seq = blockIdx.x / Hkv, h = blockIdx.x % Hkv;
+  const SeqDesc &sd = seqs[seq];
+  if (sd.method != H2O) return;
+  int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
+  const int count = st[ST_COUNT];
+  if (count <= sd.B) return;
+  const int p = st[ST_NEXT_POS] - 1;
+  const int limit = p - sd.R + 1;
+  int32_t *pos = reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd);
+  const float *score = reinterpret_cast<const float *>(sd.score) + h * stride_slots(sd);
+  unsigned long long best = ~0ull;
+  for (int j = threadIdx.x; j < count; j += NT) {
+    const int pj = pos[j];
+    if (pj < limit) {
+      const unsigned long long key = ((unsigned long long)__builtin_bit_cast(uint32_t, score[j]) << 32) |
+                                     (unsigned long long)(uint32_t)pj;
+      best = key < best ? key : best;
+    }
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const unsigned long long o = __shfl_xor(best, m);
+    best = o < best ? o : best;
+  }
+  if ((threadIdx.x & 63) == 0) s_best[threadIdx.x >> 6] = best;
+  __syncthreads();
+  best = s_best[0];
+  for (int w = 1; w < NT / 64; ++w) best = s_best[w] < best ? s_best[w] : best;
+  const int victim = (int)(uint32_t)(best & 0xFFFFFFFFu);
+  __syncthreads();
+  for (int j = threadIdx.x; j < count; j += NT) {
+    if (pos[j] == victim) {
+      pos[j] = -1;
+      st[ST_FREE_SLOT] = j;
+      st[ST_COUNT] = count - 1;
+    }
+  }
+}
+
+// ---- causal prefill attention statistics (shared by H2O scoring) ---------------------------------
+// Tiles of 64 query rows x 64 keys; 256 threads as 16 x 16, each owning 4 rows x 4 keys.
+constexpr int TB = 64;
+
+template <int D>
+MKV_DEV void load_tile_f32(float (*dst)[D + 1], const uint16_t *src, int64_t row_stride, int r0, int nrows) {
+  for (int e = threadIdx.x; e < TB * D; e += NT) {
+    const int r = e / D, c = e % D;
+    dst[r][c] = (r0 + r < nrows) ? h2f(src[(int64_t)(r0 + r) * row_stride + c]) : 0.f;
+  }
+}
+
+// Row statistics (max, sum of exp2) of the causal logits of query head gq over all prompt keys.
+template <int D>
+__global__ __launch_bounds__(NT) void k_h2o_rowstats(const SeqDesc *__restrict__ seqs, int seq,
+                                                     const uint16_t *__restrict__ qrows, int Hq, int G,
+                                                     float scale2) {
+  __shared__ float sq[TB][D + 1];
+  __shared__ float sk[TB][D + 1];
+  const SeqDesc &sd = seqs[seq];
+  const int n0 = sd.n0;
+  const int rb = blockIdx.x, gq = blockIdx.y, h = gq / G, g = gq % G;
+  const int ty = threadIdx.x / 16, tx = threadIdx.x % 16;
+  const int i0 = rb * TB;
+  load_tile_f32<D>(sq, qrows + (size_t)gq * D, (int64_t)Hq * D, i0, n0);
+  const uint16_t *ks = reinterpret_cast<const uint16_t *>(sd.stage_k) + h * stride_stage(sd, D);
+  float m[4], l[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) { m[r] = -INFINITY; l[r] = 0.f; }
+  for (int kb = 0; kb <= rb; ++kb) {
+    __syncthreads();
+    load_tile_f32<D>(sk, ks, D, kb * TB, n0);
+    __syncthreads();
+    float s[4][4] = {};
+    for (int c = 0; c < D; ++c) {
+      float qv[4], kv[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) qv[r] = sq[ty * 4 + r][c];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) kv[j] = sk[tx * 4 + j][c];
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) s[r][j] = fmaf(qv[r], kv[j], s[r][j]);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = i0 + ty * 4 + r;
+      float mx = m[r];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int jj = kb * TB + tx * 4 + j;
+        s[r][j] = (jj <= i && jj < n0) ? s[r][j] * scale2 : -INFINITY;
+        mx = fmaxf(mx, s[r][j]);
+      }
+      if (mx != -INFINITY) {
+        float acc = l[r] * exp2f(m[r] - mx);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc += exp2f(s[r][j] - mx);
+        l[r] = acc;
+        m[r] = mx;
+      }
+    }
+  }
+  // merge the 16 threads of each row (consecutive lanes)
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float M = m[r];
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) M = fmaxf(M, __shfl_xor(M, o));
+    float L = (m[r] == -INFINITY) ? 0.f : l[r] * exp2f(m[r] - M);
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) L += __shfl_xor(L, o);
+    const int i = i0 + ty * 4 + r;
+    if (tx == 0 && i < n0)
+      (reinterpret_cast<float2 *>(sd.aux1) + (size_t)h * G * n0)[(size_t)g * n0 + i] = make_float2(M, L);
+  }
+}
+
+// Column sums S_j = sum_g sum_{i >= j} p_gij over a 64-key block.
+template <int D>
+__global__ __launch_bounds__(NT) void k_h2o_colsums(const SeqDesc *__restrict__ seqs, int seq,
+                                                    const uint16_t *__restrict__ qrows, int Hq, int G,
+                                                    float scale2) {
+  __shared__ float sq[TB][D + 1];
+  __shared__ float sk[TB][D + 1];
+  __shared__ float2 sstat[TB];
+  __shared__ float scol[16][TB];
+  const SeqDesc &sd = seqs[seq];
+  const int n0 = sd.n0;
+  const int kb = blockIdx.x, h = blockIdx.y;
+  const int ty = threadIdx.x / 16, tx = threadIdx.x % 16;
+  const uint16_t *ks = reinterpret_cast<const uint16_t *>(sd.stage_k) + h * stride_stage(sd, D);
+  load_tile_f32<D>(sk, ks, D, kb * TB, n0);
+  const int nrb = (n0 + TB - 1) / TB;
+  const float2 *stat = reinterpret_cast<const float2 *>(sd.aux1) + (size_t)h * G * n0;
+  float col[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int g = 0; g < G; ++g) {
+    const int gq = h * G + g;
+    for (int rb = kb; rb < nrb; ++rb) {
+      __syncthreads();
+      load_tile_f32<D>(sq, qrows + (size_t)gq * D, (int64_t)Hq * D, rb * TB, n0);
+      for (int r = threadIdx.x; r < TB; r += NT) {
+        const int i = rb * TB + r;
+        sstat[r] = i < n0 ? stat[(size_t)g * n0 + i] : make_float2(0.f, 1.f);
+      }
+      __syncthreads();
+      float s[4][4] = {};
+      for (int c = 0; c < D; ++c) {
+        float qv[4], kv[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) qv[r] = sq[ty * 4 + r][c];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) kv[j] = sk[tx * 4 + j][c];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) s[r][j] = fmaf(qv[r], kv[j], s[r][j]);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = rb * TB + ty * 4 + r;
+        const float2 ml = sstat[ty * 4 + r];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int jj = kb * TB + tx * 4 + j;
+          if (i < n0 && jj <= i && jj < n0) col[j] += exp2f(s[r][j] * scale2 - ml.x) / ml.y;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) scol[ty][tx * 4 + j] = col[j];
+  __syncthreads();
+  if (threadIdx.x < TB) {
+    float acc = 0.f;
+    for (int y = 0; y < 16; ++y) acc += scol[y][threadIdx.x];
+    const int jj = kb * TB + threadIdx.x;
+    if (jj < n0) (reinterpret_cast<float *>(sd.aux0) + (size_t)h * n0)[jj] = acc;
+  }
+}
+
+// Keep the R most recent prompt tokens plus the top B - R scores of the rest (newer on ties),
+// compact them into slots 0..kept-1 in ascending position order.
+template <int D>
+__global__ __launch_bounds__(NT) void k_h2o_keep(const SeqDesc *__restrict__ seqs, int seq, int32_t *state,
+                                                 int Hkv) {
+  __shared__ int hist[256];
+  __shared__ int s3[3];
+  __shared__ int s_tmp[NT / 64];
+  const SeqDesc &sd = seqs[seq];
+  const int h = blockIdx.x, n0 = sd.n0;
+  const float *S = reinterpret_cast<const float *>(sd.aux0) + (size_t)h * n0;
+  const int B = sd.B, R = sd.R;
+  const bool all = B >= n0;
+  const int ncand = all ? 0 : n0 - R;
+  const int H = all ? 0 : B - R;
+  uint32_t kth = 0xFFFFFFFFu;
+  int n_eq = 0, need = 0;
+  if (H > 0) radix_select_kth<NT>(ncand, H, [&](int i) { return float_key(S[i]); }, hist, s3, &kth, &n_eq, &need);
+  const uint16_t *sk = reinterpret_cast<const uint16_t *>(sd.stage_k) + h * stride_stage(sd, D);
+  const uint16_t *sv = reinterpret_cast<const uint16_t *>(sd.stage_v) + h * stride_stage(sd, D);
+  uint16_t *dk = reinterpret_cast<uint16_t *>(sd.k) + h * stride_rows(sd, D);
+  uint16_t *dvv = reinterpret_cast<uint16_t *>(sd.v) + h * stride_rows(sd, D);
+  int32_t *pos = reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd);
+  float *score = reinterpret_cast<float *>(sd.score) + h * stride_slots(sd);
+  const int kept = compact_ascending(
+      n0,
+      [&](int j, int eq_before) {
+        if (all || j >= ncand) return true;
+        if (H == 0) return false;
+        const uint32_t kk = float_key(S[j]);
+        return kk > kth || (kk == kth && eq_before >= n_eq - need);
+      },
+      [&](int j) { return !all && H > 0 && j < ncand && float_key(S[j]) == kth; },
+      [&](int j, int slot) {
+        if (slot >= sd.cap) return;
+        pos[slot] = j;
+        score[slot] = S[j];
+        for (int c = 0; c < D; c += 8) {
+          *reinterpret_cast<uint4 *>(dk + (size_t)slot * D + c) = *reinterpret_cast<const uint4 *>(sk + (size_t)j * D + c);
+          *reinterpret_cast<uint4 *>(dvv + (size_t)slot * D + c) = *reinterpret_cast<const uint4 *>(sv + (size_t)j * D + c);
+        }
+      },
+      s_tmp);
+  if (threadIdx.x == 0) {
+    int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
+    st[ST_COUNT] = kept;
+    st[ST_FREE_SLOT] = kept;
+    st[ST_KEPT] = kept;
+  }
+}
+
+// ---- SnapKV prefill -------------------------------------------------------------------------------
+// Window row r = i * G + g (query head h*G + g at position n0 - w + i).  Pass 1: per 256-key chunk
+// and wave, the partial (max, sum of exp2) of every row.  Pass 2: merge, then votes of the
+// chunk's keys.  Pass 3: pool, select, compact.
+constexpr int SNAP_CHUNK = 256;
+
+template <int D>
+MKV_DEV void load_key_row(const uint16_t *ks, int j, int n0, float *kr) {
+  if (j < n0) {
+#pragma unroll
+    for (int c = 0; c < D; c += 8) {
+      const uint4 u = *reinterpret_cast<const uint4 *>(ks + (size_t)j * D + c);
+      unpack8(u, kr + c);
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < D; ++c) kr[c] = 0.f;
+  }
+}
+
+template <int D>
+MKV_DEV void load_window(float (*sq)[D], const uint16_t *qw, int h, int G, int Hq, int w, int wfull,
+                         int r0, int nr) {
+  for (int e = threadIdx.x; e < nr * D; e += NT) {
+    const int rr = e / D, c = e % D;
+    const int r = r0 + rr, i = r / G, g = r % G;
+    // the last w of the `wfull` window rows
+    sq[rr][c] = h2f(qw[((size_t)(wfull - w + i) * Hq + h * G + g) * D + c]);
+  }
+}
+
+constexpr int SNAP_ROWS = 64;   // window rows staged in LDS at a time
+
+template <int D>
+__global__ __launch_bounds__(NT) void k_snap_rowstats(const SeqDesc *__restrict__ seqs, int seq,
+                                                      const uint16_t *__restrict__ qw, int Hq, int G,
+                                                      float scale2) {
+  __shared__ float sq[SNAP_ROWS][D];
+  const SeqDesc &sd = seqs[seq];
+  const int n0 = sd.n0, w = sd.w_eff, wfull = sd.window;
+  const int chunk = blockIdx.x, h = blockIdx.y;
+  const int nchunk = (n0 + SNAP_CHUNK - 1) / SNAP_CHUNK;
+  const int j = chunk * SNAP_CHUNK + (int)threadIdx.x;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const uint16_t *ks = reinterpret_cast<const uint16_t *>(sd.stage_k) + h * stride_stage(sd, D);
+  float kr[D];
+  load_key_row<D>(ks, j, n0, kr);
+  const int rows = w * G;
+  float2 *part = reinterpret_cast<float2 *>(sd.aux1) + (size_t)h * rows * nchunk * 4;
+  for (int r0 = 0; r0 < rows; r0 += SNAP_ROWS) {
+    const int nr = min(SNAP_ROWS, rows - r0);
+    __syncthreads();
+    load_window<D>(sq, qw, h, G, Hq, w, wfull, r0, nr);
+    __syncthreads();
+    for (int rr = 0; rr < nr; ++rr) {
+      const int r = r0 + rr, i = r / G;
+      const int posr = n0 - w + i;
+      float acc = 0.f;
+#pragma unroll
+      for (int c = 0; c < D; ++c) acc = fmaf(sq[rr][c], kr[c], acc);
+      const float s = (j <= posr && j < n0) ? acc * scale2 : -INFINITY;
+      const float M = wave_max(s);
+      const float L = wave_sum(M == -INFINITY ? 0.f : exp2f(s - M));
+      if (lane == 0) part[((size_t)r * nchunk + chunk) * 4 + wave] = make_float2(M, L);
+    }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(NT) void k_snap_votes(const SeqDesc *__restrict__ seqs, int seq,
+                                                   const uint16_t *__restrict__ qw, int Hq, int G,
+                                                   float scale2) {
+  __shared__ float sq[SNAP_ROWS][D];
+  __shared__ float2 sml[SNAP_ROWS];
+  const SeqDesc &sd = seqs[seq];
+  const int n0 = sd.n0, w = sd.w_eff, wfull = sd.window;
+  const int chunk = blockIdx.x, h = blockIdx.y;
+  const int nchunk = (n0 + SNAP_CHUNK - 1) / SNAP_CHUNK;
+  const int j = chunk * SNAP_CHUNK + (int)threadIdx.x;
+  const uint16_t *ks = reinterpret_cast<const uint16_t *>(sd.stage_k) + h * stride_stage(sd, D);
+  float kr[D];
+  load_key_row<D>(ks, j, n0, kr);
+  const int rows = w * G;
+  const float2 *part = reinterpret_cast<const float2 *>(sd.aux1) + (size_t)h * rows * nchunk * 4;
+  float vote = 0.f;
+  for (int r0 = 0; r0 < rows; r0 += SNAP_ROWS) {
+    const int nr = min(SNAP_ROWS, rows - r0);
+    __syncthreads();
+    load_window<D>(sq, qw, h, G, Hq, w, wfull, r0, nr);
+    for (int rr = threadIdx.x; rr < nr; rr += NT) {
+      const float2 *pp = part + (size_t)(r0 + rr) * nchunk * 4;
+      float M = -INFINITY;
+      for (int e = 0; e < nchunk * 4; ++e) M = fmaxf(M, pp[e].x);
+      float L = 0.f;
+      for (int e = 0; e < nchunk * 4; ++e)
+        if (pp[e].x != -INFINITY) L += pp[e].y * exp2f(pp[e].x - M);
+      sml[rr] = make_float2(M, L);
+    }
+    __syncthreads();
+    for (int rr = 0; rr < nr; ++rr) {
+      const int r = r0 + rr, i = r / G;
+      const int posr = n0 - w + i;
+      float acc = 0.f;
+#pragma unroll
+      for (int c = 0; c < D; ++c) acc = fmaf(sq[rr][c], kr[c], acc);
+      if (j <= posr && j < n0) vote += exp2f(acc * scale2 - sml[rr].x) / sml[rr].y;
+    }
+  }
+  if (j < n0 - w) (reinterpret_cast<float *>(sd.aux0) + (size_t)h * n0)[j] = vote;
+}
+
+template <int D>
+__global__ __launch_bounds__(NT) void k_snap_keep(const SeqDesc *__restrict__ seqs, int seq, int32_t *state,
+                                                  int Hkv) {
+  __shared__ int hist[256];
+  __shared__ int s3[3];
+  __shared__ int s_tmp[NT / 64];
+  const SeqDesc &sd = seqs[seq];
+  const int h = blockIdx.x, n0 = sd.n0, w = sd.w_eff;
+  const bool all = sd.T >= n0;
+  const int ncand = all ? 0 : n0 - w;
+  const int want = all ? 0 : sd.T - w;
+  const float *votes = reinterpret_cast<const float *>(sd.aux0) + (size_t)h * n0;
+  const int half = sd.pool / 2;
+  auto pooled = [&](int j) {
+    float m = votes[j];
+    const int lo = max(0, j - half), hi = min(ncand - 1, j + half);
+    for (int x = lo; x <= hi; ++x) m = fmaxf(m, votes[x]);
+    return float_key(m);
+  };
+  uint32_t kth = 0xFFFFFFFFu;
+  int n_eq = 0, need = 0;
+  if (want > 0) radix_select_kth<NT>(ncand, want, pooled, hist, s3, &kth, &n_eq, &need);
+  const uint16_t *sk = reinterpret_cast<const uint16_t *>(sd.stage_k) + h * stride_stage(sd, D);
+  const uint16_t *sv = reinterpret_cast<const uint16_t *>(sd.stage_v) + h * stride_stage(sd, D);
+  uint16_t *dk = reinterpret_cast<uint16_t *>(sd.k) + h * stride_rows(sd, D);
+  uint16_t *dvv = reinterpret_cast<uint16_t *>(sd.v) + h * stride_rows(sd, D);
+  uint16_t *kcm = reinterpret_cast<uint16_t *>(sd.kcm) + h * stride_rows(sd, D);
+  int32_t *pos = reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd);
+  const int cap = sd.cap;
+  const int kept = compact_ascending(
+      n0,
+      [&](int j, int eq_before) {
+        if (all || j >= ncand) return true;
+        if (want == 0) return false;
+        const uint32_t kk = pooled(j);
+        return kk > kth || (kk == kth && eq_before < need);
+      },
+      [&](int j) { return !all && want > 0 && j < ncand && pooled(j) == kth; },
+      [&](int j, int slot) {
+        if (slot >= cap) return;
+        pos[slot] = j;
+        for (int c = 0; c < D; c += 8) {
+          const uint4 a = *reinterpret_cast<const uint4 *>(sk + (size_t)j * D + c);
+          *reinterpret_cast<uint4 *>(dk + (size_t)slot * D + c) = a;
+          *reinterpret_cast<uint4 *>(dvv + (size_t)slot * D + c) = *reinterpret_cast<const uint4 *>(sv + (size_t)j * D + c);
+          const uint32_t wv[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+          for (int e = 0; e < 8; ++e) kcm[(size_t)(c + e) * cap + slot] = (uint16_t)(wv[e / 2] >> (16 * (e & 1)));
+        }
+      },
+      s_tmp);
+  if (threadIdx.x == 0) {
+    int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
+    st[ST_COUNT] = kept;
+    st[ST_KEPT] = kept;
+  }
+}
+
+template <int D, int G>
+hipError_t topk_impl(const Dev &dv, const Shape &sh, const uint16_t *q, int32_t *pos_out, int topk_max,
+                     hipStream_t st) {
+  hipLaunchKernelGGL((k_topk<D, G>), dim3(sh.S * sh.Hkv), dim3(NT), 0, st, dv.seqs, dv.state, q, pos_out,
+                     topk_max, sh.Hkv);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t h2o_prefill_impl(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq, const uint16_t *q,
+                            hipStream_t st) {
+  const float scale2 = kLog2e / sqrtf((float)D);
+  const int nb = (hs.n0 + TB - 1) / TB;
+  hipLaunchKernelGGL(k_h2o_rowstats<D>, dim3(nb, sh.Hq), dim3(NT), 0, st, dv.seqs, seq, q, sh.Hq, sh.G, scale2);
+  hipLaunchKernelGGL(k_h2o_colsums<D>, dim3(nb, sh.Hkv), dim3(NT), 0, st, dv.seqs, seq, q, sh.Hq, sh.G, scale2);
+  hipLaunchKernelGGL(k_h2o_keep<D>, dim3(sh.Hkv), dim3(NT), 0, st, dv.seqs, seq, dv.state, sh.Hkv);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t snap_prefill_impl(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq, const uint16_t *qw,
+                             hipStream_t st) {
+  const float scale2 = kLog2e / sqrtf((float)D);
+  if (hs.T < hs.n0) {
+    const int nchunk = (hs.n0 + SNAP_CHUNK - 1) / SNAP_CHUNK;
+    hipLaunchKernelGGL(k_snap_rowstats<D>, dim3(nchunk, sh.Hkv), dim3(NT), 0, st, dv.seqs, seq, qw, sh.Hq, sh.G,
+                       scale2);
+    hipLaunchKernelGGL(k_snap_votes<D>, dim3(nchunk, sh.Hkv), dim3(NT), 0, st, dv.seqs, seq, qw, sh.Hq, sh.G,
+                       scale2);
+  }
+  hipLaunchKernelGGL(k_snap_keep<D>, dim3(sh.Hkv), dim3(NT), 0, st, dv.seqs, seq, dv.state, sh.Hkv);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_topk(const Dev &dv, const Shape &sh, const uint16_t *q, int32_t *pos_out, int topk_max,
+                       hipStream_t st) {
+  switch (sh.D * 16 + sh.G) {
+    case 64 * 16 + 1: return topk_impl<64, 1>(dv, sh, q, pos_out, topk_max, st);
+    case 64 * 16 + 2: return topk_impl<64, 2>(dv, sh, q, pos_out, topk_max, st);
+    case 64 * 16 + 4: return topk_impl<64, 4>(dv, sh, q, pos_out, topk_max, st);
+    case 64 * 16 + 8: return topk_impl<64, 8>(dv, sh, q, pos_out, topk_max, st);
+    case 128 * 16 + 1: return topk_impl<128, 1>(dv, sh, q, pos_out, topk_max, st);
+    case 128 * 16 + 2: return topk_impl<128, 2>(dv, sh, q, pos_out, topk_max, st);
+    case 128 * 16 + 4: return topk_impl<128, 4>(dv, sh, q, pos_out, topk_max, st);
+    case 128 * 16 + 8: return topk_impl<128, 8>(dv, sh, q, pos_out, topk_max, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_h2o_evict(const Dev &dv, const Shape &sh, hipStream_t st) {
+  hipLaunchKernelGGL(k_h2o_evict, dim3(sh.S * sh.Hkv), dim3(NT), 0, st, dv.seqs, dv.state, sh.Hkv);
+  return hipGetLastError();
+}
+
+hipError_t launch_h2o_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
+                                  const uint16_t *q_rows, hipStream_t st) {
+  return sh.D == 64 ? h2o_prefill_impl<64>(dv, sh, hs, seq, q_rows, st)
+                    : h2o_prefill_impl<128>(dv, sh, hs, seq, q_rows, st);
+}
+
+hipError_t launch_snap_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
+                                   const uint16_t *q_window, hipStream_t st) {
+  return sh.D == 64 ? snap_prefill_impl<64>(dv, sh, hs, seq, q_window, st)
+                    : snap_prefill_impl<128>(dv, sh, hs, seq, q_window, st);
+}
+
+}  // namespace mkv

@@ -1,0 +1,143 @@
+// Device helpers shared by the HIP kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mkv_internal.h"
+
+namespace mkv {
+
+#define MKV_DEV __device__ __forceinline__
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+MKV_DEV float h2f(uint32_t bits16) {
+  return (float)__builtin_bit_cast(_Float16, (unsigned short)(bits16 & 0xFFFFu));
+}
+
+MKV_DEV uint16_t f2h_bits(float x) {
+  return __builtin_bit_cast(unsigned short, (_Float16)x);
+}
+
+// 8 fp16 values packed in a uint4 -> float[8]
+MKV_DEV void unpack8(const uint4 &u, float *f) {
+  f[0] = h2f(u.x); f[1] = h2f(u.x >> 16);
+  f[2] = h2f(u.y); f[3] = h2f(u.y >> 16);
+  f[4] = h2f(u.z); f[5] = h2f(u.z >> 16);
+  f[6] = h2f(u.w); f[7] = h2f(u.w >> 16);
+}
+
+template <typename T>
+MKV_DEV T ldg(const T *p) { return __builtin_nontemporal_load(p); }
+
+// ---- DPP row reductions ---------------------------------------------------------------------
+template <int CTRL>
+MKV_DEV float dpp(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL,
+                                                               0xF, 0xF, false));
+}
+
+// Sum over aligned groups of L lanes (L in {8, 16}); every lane of a group gets the total.
+template <int L>
+MKV_DEV float group_sum(float x) {
+  x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
+  x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
+  x += dpp<0x141>(x);  // row_half_mirror
+  if constexpr (L == 16) x += dpp<0x140>(x);  // row_mirror
+  return x;
+}
+
+MKV_DEV float wave_max(float x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m));
+  return x;
+}
+MKV_DEV float wave_min(float x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x = fminf(x, __shfl_xor(x, m));
+  return x;
+}
+MKV_DEV float wave_sum(float x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m);
+  return x;
+}
+MKV_DEV int wave_sum_i(int x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m);
+  return x;
+}
+
+// Order-preserving unsigned key of a float (-0 treated as +0).
+MKV_DEV uint32_t float_key(float f) {
+  uint32_t u = __builtin_bit_cast(uint32_t, f);
+  if (u == 0x80000000u) u = 0;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Exclusive prefix sum over a block of NT threads (NT multiple of 64).  `tmp` is NT/64 ints of LDS.
+template <int NT>
+MKV_DEV int block_exclusive_scan(int x, int *tmp, int *total) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  int inc = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int y = __shfl_up(inc, o);
+    if (lane >= o) inc += y;
+  }
+  if (lane == 63) tmp[wid] = inc;
+  __syncthreads();
+  int base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < NT / 64; ++w) {
+    int t = tmp[w];
+    if (w < wid) base += t;
+    tot += t;
+  }
+  __syncthreads();
+  *total = tot;
+  return base + inc - x;
+}
+
+// Block-wide radix select over n 32-bit keys read through `get(i)`: returns the k-th largest key
+// (1 <= k <= n), the number of keys equal to it, and how many of those equal keys are needed
+// to make k.  `hist` is 256 ints of LDS, `shared3` 3 ints of LDS.
+template <int NT, typename Get>
+MKV_DEV void radix_select_kth(int n, int k, Get get, int *hist, int *shared3, uint32_t *kth,
+                              int *n_equal, int *need) {
+  uint32_t prefix = 0, mask = 0;
+  int remaining = k;
+  int eq = 0;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    for (int i = threadIdx.x; i < 256; i += NT) hist[i] = 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < n; i += NT) {
+      uint32_t key = get(i);
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int cum = 0, dg = 0;
+      for (int d = 255; d >= 0; --d) {
+        if (cum + hist[d] >= remaining) { dg = d; break; }
+        cum += hist[d];
+      }
+      shared3[0] = dg;
+      shared3[1] = remaining - cum;
+      shared3[2] = hist[dg];
+    }
+    __syncthreads();
+    prefix |= (uint32_t)shared3[0] << shift;
+    mask |= 255u << shift;
+    remaining = shared3[1];
+    eq = shared3[2];
+    __syncthreads();
+  }
+  *kth = prefix;
+  *n_equal = eq;
+  *need = remaining;
+}
+
+}  // namespace mkv

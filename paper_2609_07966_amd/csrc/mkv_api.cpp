@@ -1,0 +1,717 @@
+// Host side of libmkv: argument validation, arena layout, call-order state machine, kernel
+// launches, state export and kernel timing.  See include/mkv.h for the contract.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "mkv.h"
+#include "mkv_internal.h"
+
+using namespace mkv;
+
+namespace {
+
+thread_local std::string g_err;
+
+mkv_status fail(mkv_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+mkv_status hip_fail(hipError_t e, const char *what) {
+  return fail(MKV_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+enum Phase { PH_CREATED, PH_PROMPT, PH_READY, PH_APPENDED, PH_SELECTED, PH_ATTENDED };
+
+constexpr int kProfKinds = 5;
+
+struct Layout {
+  std::vector<SeqDesc> seqs;  // offsets (relative to the arena) in the pointer fields
+  size_t off_seqs = 0, off_state = 0, off_tiles = 0, off_cbtab = 0, off_partials = 0, total = 0;
+  int n_tiles = 0;
+  std::vector<int4> tiles;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int tile_tokens(const SeqDesc &s, int D) {
+  // bytes each token costs the attention pass; tiles carry about 64 KiB
+  double bpt;
+  switch (s.method) {
+    case UQ: bpt = D + D / 64.0 * 8 + 8; break;
+    case KVQ: bpt = D * s.bits / 4.0 + 4 + 8 + 4; break;
+    default: bpt = 4.0 * D; break;
+  }
+  int t = (int)(65536.0 / bpt) & ~63;
+  if (const char *e = getenv("MKV_TILE_TOKENS")) t = atoi(e) & ~63;
+  return std::max(64, std::min(t, 4096));
+}
+
+mkv_status check_shape(const mkv_shape *sh) {
+  if (!sh) return fail(MKV_EINVAL, "shape is NULL");
+  if (sh->n_seqs < 1 || sh->n_kv_heads < 1 || sh->n_q_heads < 1 || sh->max_new_tokens < 0)
+    return fail(MKV_EINVAL, "shape fields must be positive (max_new_tokens >= 0)");
+  if (sh->n_q_heads % sh->n_kv_heads != 0) return fail(MKV_EINVAL, "n_q_heads %% n_kv_heads != 0");
+  const int G = sh->n_q_heads / sh->n_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(MKV_EUNSUPPORTED, "query heads per kv head must be 1, 2, 4 or 8 (got %d)", G);
+  if (sh->head_dim != 64 && sh->head_dim != 128)
+    return fail(MKV_EUNSUPPORTED, "head_dim must be 64 or 128 (got %d)", sh->head_dim);
+  return MKV_OK;
+}
+
+mkv_status check_config(const mkv_config &c, int n0, int D, int s) {
+  if (n0 < 1) return fail(MKV_EINVAL, "seq %d: prompt_len must be >= 1", s);
+  switch (c.method) {
+    case MKV_FP16: return MKV_OK;
+    case MKV_UQ:
+      if (c.bits != 4) return fail(MKV_EUNSUPPORTED, "seq %d: uniform quantization supports bits=4", s);
+      if (c.group != 64) return fail(MKV_EUNSUPPORTED, "seq %d: uniform quantization supports group=64", s);
+      return MKV_OK;
+    case MKV_KVQ:
+      if (c.bits < 2 || c.bits > 4) return fail(MKV_EINVAL, "seq %d: KVQ bits must be 2, 3 or 4", s);
+      if (c.outlier_bp < 0 || c.outlier_bp > 5000) return fail(MKV_EINVAL, "seq %d: outlier_bp in 0..5000", s);
+      if (n0 > 65535) return fail(MKV_EUNSUPPORTED, "seq %d: KVQ prompt longer than 65535", s);
+      return MKV_OK;
+    case MKV_H2O: {
+      if (c.budget_pct < 1 || c.budget_pct > 10000) return fail(MKV_EINVAL, "seq %d: budget_pct in 1..10000", s);
+      const long long B = (long long)c.budget_pct * n0 / 100;
+      if (B < 1) return fail(MKV_EINVAL, "seq %d: H2O budget is 0 tokens for prompt_len %d", s, n0);
+      return MKV_OK;
+    }
+    case MKV_ROCKET:
+      if (c.window < 1) return fail(MKV_EINVAL, "seq %d: window must be >= 1", s);
+      if (c.keep_tokens < c.window) return fail(MKV_EINVAL, "seq %d: keep_tokens must be >= window", s);
+      if (c.pool < 1 || (c.pool & 1) == 0) return fail(MKV_EINVAL, "seq %d: pool must be odd and >= 1", s);
+      if (c.n_channels < 1 || c.n_channels > D) return fail(MKV_EINVAL, "seq %d: n_channels in 1..head_dim", s);
+      if (c.topk < 0) return fail(MKV_EINVAL, "seq %d: topk must be >= 0", s);
+      if (c.topk == 0 && c.keep_tokens / 2 < 1) return fail(MKV_EINVAL, "seq %d: keep_tokens/2 is 0", s);
+      return MKV_OK;
+    default:
+      return fail(MKV_EINVAL, "seq %d: unknown method %d", s, c.method);
+  }
+}
+
+mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_t *plen, Layout *L) {
+  mkv_status st = check_shape(shp);
+  if (st != MKV_OK) return st;
+  if (!cfg || !plen) return fail(MKV_EINVAL, "cfg and prompt_len must be non-NULL");
+  const int S = shp->n_seqs, Hkv = shp->n_kv_heads, D = shp->head_dim, G = shp->n_q_heads / Hkv;
+  const int mn = shp->max_new_tokens;
+  for (int s = 0; s < S; ++s)
+    if ((st = check_config(cfg[s], plen[s], D, s)) != MKV_OK) return st;
+
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align256(off + std::max<size_t>(bytes, 1));
+    return (uint64_t)o;
+  };
+  L->off_seqs = take(sizeof(SeqDesc) * S);
+  L->off_state = take(sizeof(int32_t) * S * Hkv * ST_WORDS);
+  L->off_cbtab = take(sizeof(float) * kCbTableFloats);
+  L->seqs.assign(S, SeqDesc{});
+  int q_h2o = 0, q_rk = 0;
+  for (int s = 0; s < S; ++s) {
+    SeqDesc &d = L->seqs[s];
+    const mkv_config &c = cfg[s];
+    const int n0 = plen[s];
+    d.method = c.method;
+    d.n0 = n0;
+    d.bits = c.bits;
+    d.bp = c.outlier_bp;
+    const size_t H = Hkv;
+    switch (c.method) {
+      case FP16:
+        d.cap = n0 + mn;
+        d.k = take(H * d.cap * D * 2);
+        d.v = take(H * d.cap * D * 2);
+        break;
+      case UQ:
+        d.cap = n0 + mn;
+        d.rowbytes = D / 2;
+        d.nblk = d.cap / 64;
+        d.kc = take(H * d.cap * d.rowbytes);
+        d.vc = take(H * d.cap * d.rowbytes);
+        d.kmeta = take(H * std::max(d.nblk, 1) * D * 8);
+        d.vmeta = take(H * d.cap * (D / 64) * 8);
+        d.kres = take(H * 64 * D * 2);
+        break;
+      case KVQ: {
+        d.cap = n0 + mn;
+        d.rowbytes = D * c.bits / 8;
+        d.n_o = (int)(((long long)n0 * c.outlier_bp + 5000) / 10000);
+        d.n_ov = (int)(((long long)D * c.outlier_bp + 5000) / 10000);
+        d.nov_slots = c.outlier_bp > 0 ? std::max(1, d.n_ov) : 1;
+        d.pool_cap = c.outlier_bp > 0 ? (std::min(d.n_o, n0) + mn) * D : 1;
+        d.kc = take(H * d.cap * d.rowbytes);
+        d.vc = take(H * d.cap * d.rowbytes);
+        d.kmeta = take(H * D * 8);
+        d.vmeta = take(H * d.cap * 4);
+        d.krow = take(H * (d.cap + 1) * 4);
+        d.kout = take(H * d.pool_cap * 4);
+        d.vout = take(H * d.cap * d.nov_slots * 4);
+        break;
+      }
+      case H2O: {
+        d.B = (int)((long long)c.budget_pct * n0 / 100);
+        d.R = d.B / 2;
+        d.cap = (int)std::min<long long>((long long)d.B + 1, (long long)n0 + mn);
+        d.k = take(H * d.cap * D * 2);
+        d.v = take(H * d.cap * D * 2);
+        d.pos = take(H * d.cap * 4);
+        d.score = take(H * d.cap * 4);
+        d.logits = take(H * d.cap * G * 4);
+        d.stage_k = take(H * n0 * D * 2);
+        d.stage_v = take(H * n0 * D * 2);
+        d.aux0 = take(H * n0 * 4);
+        d.aux1 = take(H * G * n0 * 8);
+        d.q_off = q_h2o;
+        q_h2o += n0;
+        break;
+      }
+      case ROCKET: {
+        d.T = c.keep_tokens;
+        d.window = c.window;
+        d.w_eff = std::min(c.window, n0);
+        d.pool = c.pool;
+        d.nch = c.n_channels;
+        d.topk = c.topk > 0 ? c.topk : c.keep_tokens / 2;
+        const int kept = std::min(d.T, n0);
+        d.cap = kept + mn;
+        const int nchunk = (n0 + 255) / 256;
+        d.k = take(H * d.cap * D * 2);
+        d.v = take(H * d.cap * D * 2);
+        d.kcm = take(H * d.cap * D * 2);
+        d.pos = take(H * d.cap * 4);
+        d.sel = take(H * d.topk * 4);
+        d.akeys = take(H * d.cap * 4);
+        d.stage_k = take(H * n0 * D * 2);
+        d.stage_v = take(H * n0 * D * 2);
+        d.aux0 = take(H * n0 * 4);
+        d.aux1 = take(std::max(H * d.w_eff * G * nchunk * 4 * 8, H * D * 4));
+        d.q_off = q_rk;
+        q_rk += c.window;
+        break;
+      }
+    }
+  }
+  // attention tiles: per sequence and kv head, ranges of `chunk` tokens over its largest active set
+  L->tiles.clear();
+  for (int s = 0; s < S; ++s) {
+    SeqDesc &d = L->seqs[s];
+    const int amax = d.method == ROCKET ? d.topk : d.cap;
+    d.chunk = tile_tokens(d, D);
+    d.tile_count = std::max(1, (amax + d.chunk - 1) / d.chunk);
+    d.tile_first = (int)L->tiles.size();
+    for (int h = 0; h < Hkv; ++h)
+      for (int t = 0; t < d.tile_count; ++t)
+        L->tiles.push_back(make_int4(s, h, t * d.chunk, std::min(amax, (t + 1) * d.chunk)));
+  }
+  L->n_tiles = (int)L->tiles.size();
+  L->off_tiles = take(sizeof(int4) * L->n_tiles);
+  L->off_partials = take(sizeof(float) * (size_t)L->n_tiles * G * (D + 2));
+  L->total = off;
+  return MKV_OK;
+}
+
+}  // namespace
+
+struct mkv_cache {
+  Shape sh{};
+  std::vector<mkv_config> cfg;
+  std::vector<SeqDesc> hs;  // absolute device pointers
+  Layout L;
+  char *arena = nullptr;
+  Dev dv{};
+  Phase phase = PH_CREATED;
+  int steps = 0;
+  bool any_h2o = false, any_rocket = false, h2o_done = false, snap_done = false;
+  int topk_max = 0;
+  int h2o_rows = 0, rocket_rows = 0;
+  // profiling
+  bool prof = false;
+  int prof_cap = 0;
+  std::vector<hipEvent_t> ev[kProfKinds][2];
+  int prof_n[kProfKinds] = {};
+};
+
+namespace {
+
+void prof_mark(mkv_cache *c, int kind, int which, hipStream_t st) {
+  if (!c->prof) return;
+  const int i = c->prof_n[kind];
+  if (i >= c->prof_cap) return;
+  hipEventRecord(c->ev[kind][which][i], st);
+  if (which == 1) c->prof_n[kind] = i + 1;
+}
+
+mkv_status check_hip(hipError_t e, const char *what) {
+  return e == hipSuccess ? MKV_OK : hip_fail(e, what);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *mkv_status_str(mkv_status s) {
+  switch (s) {
+    case MKV_OK: return "ok";
+    case MKV_EINVAL: return "invalid argument";
+    case MKV_ENOMEM: return "arena too small";
+    case MKV_ECAPACITY: return "cache capacity exceeded";
+    case MKV_ESTATE: return "call out of order";
+    case MKV_EUNSUPPORTED: return "unsupported configuration";
+    case MKV_EHIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char *mkv_last_error(void) { return g_err.c_str(); }
+
+mkv_status mkv_cache_bytes(const mkv_shape *shape, const mkv_config *cfg, const int32_t *prompt_len,
+                           size_t *arena_bytes) {
+  if (!arena_bytes) return fail(MKV_EINVAL, "arena_bytes is NULL");
+  Layout L;
+  mkv_status st = make_layout(shape, cfg, prompt_len, &L);
+  if (st != MKV_OK) return st;
+  *arena_bytes = L.total;
+  return MKV_OK;
+}
+
+mkv_status mkv_cache_create(const mkv_shape *shape, const mkv_config *cfg, const int32_t *prompt_len,
+                            const float *codebooks, void *arena, size_t arena_bytes, void *stream,
+                            mkv_cache **out) {
+  if (!out) return fail(MKV_EINVAL, "out is NULL");
+  *out = nullptr;
+  Layout L;
+  mkv_status st = make_layout(shape, cfg, prompt_len, &L);
+  if (st != MKV_OK) return st;
+  if (!arena) return fail(MKV_EINVAL, "arena is NULL");
+  if (((uintptr_t)arena & 255) != 0) return fail(MKV_EINVAL, "arena must be 256-byte aligned");
+  if (arena_bytes < L.total)
+    return fail(MKV_ENOMEM, "arena has %zu bytes, the cache needs %zu", arena_bytes, L.total);
+  bool any_kvq = false;
+  for (int s = 0; s < shape->n_seqs; ++s) any_kvq |= cfg[s].method == MKV_KVQ;
+  float table[kCbTableFloats] = {};
+  if (any_kvq) {
+    if (!codebooks) return fail(MKV_EINVAL, "codebooks are required for KVQ sequences");
+    const float *src = codebooks;
+    for (int b = 2; b <= 4; ++b) {
+      const int nc = 1 << b;
+      float *dst = table + cb_offset(b);
+      for (int half = 0; half < 2; ++half) {
+        for (int i = 0; i < nc; ++i) {
+          const float x = src[half * nc + i];
+          if (!std::isfinite(x)) return fail(MKV_EINVAL, "codebook entry is not finite");
+          if (i > 0 && !(x >= src[half * nc + i - 1])) return fail(MKV_EINVAL, "codebooks must be ascending");
+          dst[half * nc + i] = x;
+        }
+        for (int i = 0; i + 1 < nc; ++i) {
+          volatile float sum = src[half * nc + i] + src[half * nc + i + 1];
+          dst[2 * nc + half * (nc - 1) + i] = sum * 0.5f;
+        }
+      }
+      src += 2 * nc;
+    }
+  }
+  mkv_cache *c = new mkv_cache();
+  c->sh = Shape{shape->n_seqs, shape->n_q_heads, shape->n_kv_heads, shape->head_dim,
+                shape->n_q_heads / shape->n_kv_heads, shape->max_new_tokens};
+  c->cfg.assign(cfg, cfg + shape->n_seqs);
+  c->arena = static_cast<char *>(arena);
+  c->L = L;
+  const uint64_t base = (uint64_t)(uintptr_t)arena;
+  c->hs = L.seqs;
+  for (auto &d : c->hs) {
+    uint64_t *ptrs[] = {&d.k, &d.v, &d.kc, &d.vc, &d.kmeta, &d.vmeta, &d.kres, &d.krow, &d.kout, &d.vout,
+                        &d.pos, &d.score, &d.logits, &d.stage_k, &d.stage_v, &d.kcm, &d.sel, &d.akeys,
+                        &d.aux0, &d.aux1};
+    // offset 0 holds the descriptor table, so a zero offset marks a region the method lacks
+    for (uint64_t *p : ptrs)
+      if (*p) *p += base;
+    if (d.method == H2O) {
+      c->any_h2o = true;
+      c->h2o_rows += d.n0;
+    }
+    if (d.method == ROCKET) {
+      c->any_rocket = true;
+      c->rocket_rows += d.window;
+      c->topk_max = std::max(c->topk_max, d.topk);
+    }
+  }
+  c->dv.seqs = reinterpret_cast<const SeqDesc *>(c->arena + L.off_seqs);
+  c->dv.state = reinterpret_cast<int32_t *>(c->arena + L.off_state);
+  c->dv.tiles = reinterpret_cast<const int4 *>(c->arena + L.off_tiles);
+  c->dv.partials = reinterpret_cast<float *>(c->arena + L.off_partials);
+  c->dv.cbtab = reinterpret_cast<const float *>(c->arena + L.off_cbtab);
+  c->dv.n_tiles = L.n_tiles;
+  hipStream_t hst = static_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(c->arena + L.off_seqs, c->hs.data(), sizeof(SeqDesc) * c->hs.size(),
+                                hipMemcpyHostToDevice, hst);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(c->arena + L.off_tiles, L.tiles.data(), sizeof(int4) * L.tiles.size(),
+                       hipMemcpyHostToDevice, hst);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(c->arena + L.off_cbtab, table, sizeof table, hipMemcpyHostToDevice, hst);
+  if (e == hipSuccess) e = launch_init_state(c->dv, c->sh, hst);
+  if (e == hipSuccess) e = hipStreamSynchronize(hst);
+  if (e != hipSuccess) {
+    delete c;
+    return hip_fail(e, "mkv_cache_create");
+  }
+  *out = c;
+  return MKV_OK;
+}
+
+mkv_status mkv_cache_destroy(mkv_cache *c) {
+  if (!c) return MKV_OK;
+  for (int k = 0; k < kProfKinds; ++k)
+    for (int w = 0; w < 2; ++w)
+      for (hipEvent_t e : c->ev[k][w]) hipEventDestroy(e);
+  delete c;
+  return MKV_OK;
+}
+
+mkv_status mkv_append_quantize(mkv_cache *c, const uint16_t *k, const uint16_t *v, const int32_t *cu_new,
+                               void *stream) {
+  if (!c) return fail(MKV_EINVAL, "cache is NULL");
+  if (!k || !v || !cu_new) return fail(MKV_EINVAL, "k, v and cu_new must be non-NULL");
+  const int S = c->sh.S;
+  hipStream_t hst = static_cast<hipStream_t>(stream);
+  if (cu_new[0] != 0) return fail(MKV_EINVAL, "cu_new[0] must be 0");
+  if (c->phase == PH_CREATED) {
+    for (int s = 0; s < S; ++s)
+      if (cu_new[s + 1] - cu_new[s] != c->hs[s].n0)
+        return fail(MKV_EINVAL, "prefill: seq %d appends %d rows, prompt_len is %d", s, cu_new[s + 1] - cu_new[s],
+                    c->hs[s].n0);
+    const size_t row = (size_t)c->sh.Hkv * c->sh.D;
+    for (int s = 0; s < S; ++s) {
+      hipError_t e = launch_prefill_seq(c->dv, c->sh, c->hs[s], s, k + (size_t)cu_new[s] * row,
+                                        v + (size_t)cu_new[s] * row, hst);
+      if (e != hipSuccess) return hip_fail(e, "prefill append");
+    }
+    c->phase = (c->any_h2o || c->any_rocket) ? PH_PROMPT : PH_READY;
+    return MKV_OK;
+  }
+  for (int s = 0; s < S; ++s)
+    if (cu_new[s + 1] - cu_new[s] != 1) return fail(MKV_EINVAL, "decode: seq %d must append exactly 1 row", s);
+  if (!(c->phase == PH_READY || (c->phase == PH_ATTENDED && !c->any_h2o)))
+    return fail(MKV_ESTATE, "decode append must follow prefill or a completed decode step");
+  if (c->steps >= c->sh.max_new)
+    return fail(MKV_ECAPACITY, "cache holds %d decode steps (max_new_tokens)", c->sh.max_new);
+  prof_mark(c, 2, 0, hst);
+  hipError_t e = launch_append_decode(c->dv, c->sh, k, v, hst);
+  prof_mark(c, 2, 1, hst);
+  if (e != hipSuccess) return hip_fail(e, "decode append");
+  c->steps++;
+  c->phase = PH_APPENDED;
+  return MKV_OK;
+}
+
+mkv_status mkv_h2o_update_evict(mkv_cache *c, const uint16_t *q_prompt, void *stream) {
+  if (!c) return fail(MKV_EINVAL, "cache is NULL");
+  hipStream_t hst = static_cast<hipStream_t>(stream);
+  if (q_prompt != nullptr) {
+    if (c->phase != PH_PROMPT || c->h2o_done)
+      return fail(MKV_ESTATE, "H2O prefill scoring runs once, after the prefill append");
+    const size_t row = (size_t)c->sh.Hq * c->sh.D;
+    for (int s = 0; s < c->sh.S; ++s) {
+      if (c->hs[s].method != H2O) continue;
+      hipError_t e = launch_h2o_prefill_seq(c->dv, c->sh, c->hs[s], s, q_prompt + (size_t)c->hs[s].q_off * row, hst);
+      if (e != hipSuccess) return hip_fail(e, "H2O prefill");
+    }
+    c->h2o_done = true;
+    if (!c->any_rocket || c->snap_done) c->phase = PH_READY;
+    return MKV_OK;
+  }
+  if (c->phase == PH_PROMPT && c->any_h2o) return fail(MKV_EINVAL, "H2O prefill needs q_prompt");
+  if (c->phase != PH_ATTENDED) return fail(MKV_ESTATE, "eviction must follow mkv_decode_attention");
+  if (c->any_h2o) {
+    prof_mark(c, 4, 0, hst);
+    hipError_t e = launch_h2o_evict(c->dv, c->sh, hst);
+    prof_mark(c, 4, 1, hst);
+    if (e != hipSuccess) return hip_fail(e, "H2O evict");
+  }
+  c->phase = PH_READY;
+  return MKV_OK;
+}
+
+mkv_status mkv_snap_prefill_evict(mkv_cache *c, const uint16_t *q_window, void *stream) {
+  if (!c) return fail(MKV_EINVAL, "cache is NULL");
+  if (!c->any_rocket) return MKV_OK;
+  if (c->phase != PH_PROMPT || c->snap_done)
+    return fail(MKV_ESTATE, "SnapKV prefill eviction runs once, after the prefill append");
+  if (!q_window) return fail(MKV_EINVAL, "q_window is NULL");
+  hipStream_t hst = static_cast<hipStream_t>(stream);
+  const size_t row = (size_t)c->sh.Hq * c->sh.D;
+  for (int s = 0; s < c->sh.S; ++s) {
+    if (c->hs[s].method != ROCKET) continue;
+    hipError_t e = launch_snap_prefill_seq(c->dv, c->sh, c->hs[s], s, q_window + (size_t)c->hs[s].q_off * row, hst);
+    if (e != hipSuccess) return hip_fail(e, "SnapKV prefill");
+  }
+  c->snap_done = true;
+  if (!c->any_h2o || c->h2o_done) c->phase = PH_READY;
+  return MKV_OK;
+}
+
+mkv_status mkv_topk_select(mkv_cache *c, const uint16_t *q, int32_t *pos_out, void *stream) {
+  if (!c) return fail(MKV_EINVAL, "cache is NULL");
+  if (c->phase != PH_APPENDED) return fail(MKV_ESTATE, "top-k selection must follow a decode append");
+  if (c->any_rocket) {
+    if (!q) return fail(MKV_EINVAL, "q is NULL");
+    hipStream_t hst = static_cast<hipStream_t>(stream);
+    prof_mark(c, 3, 0, hst);
+    hipError_t e = launch_topk(c->dv, c->sh, q, pos_out, c->topk_max, hst);
+    prof_mark(c, 3, 1, hst);
+    if (e != hipSuccess) return hip_fail(e, "top-k select");
+  }
+  c->phase = PH_SELECTED;
+  return MKV_OK;
+}
+
+mkv_status mkv_decode_attention(mkv_cache *c, const uint16_t *q, float *out, void *stream) {
+  if (!c) return fail(MKV_EINVAL, "cache is NULL");
+  if (!q || !out) return fail(MKV_EINVAL, "q and out must be non-NULL");
+  if (!(c->phase == PH_SELECTED || (c->phase == PH_APPENDED && !c->any_rocket)))
+    return fail(MKV_ESTATE, "attention must follow the decode append (and top-k selection)");
+  hipStream_t hst = static_cast<hipStream_t>(stream);
+  prof_mark(c, 0, 0, hst);
+  hipError_t e = launch_attention_partial(c->dv, c->sh, q, hst);
+  prof_mark(c, 0, 1, hst);
+  if (e != hipSuccess) return hip_fail(e, "attention partial");
+  prof_mark(c, 1, 0, hst);
+  e = launch_attention_combine(c->dv, c->sh, out, hst);
+  prof_mark(c, 1, 1, hst);
+  if (e != hipSuccess) return hip_fail(e, "attention combine");
+  c->phase = PH_ATTENDED;
+  return MKV_OK;
+}
+
+mkv_status mkv_decode_step(mkv_cache *c, const uint16_t *k, const uint16_t *v, const uint16_t *q, float *out,
+                           void *stream) {
+  if (!c) return fail(MKV_EINVAL, "cache is NULL");
+  std::vector<int32_t> cu(c->sh.S + 1);
+  for (int s = 0; s <= c->sh.S; ++s) cu[s] = s;
+  mkv_status st = mkv_append_quantize(c, k, v, cu.data(), stream);
+  if (st != MKV_OK) return st;
+  if ((st = mkv_topk_select(c, q, nullptr, stream)) != MKV_OK) return st;
+  if ((st = mkv_decode_attention(c, q, out, stream)) != MKV_OK) return st;
+  return mkv_h2o_update_evict(c, nullptr, stream);
+}
+
+mkv_status mkv_attention_tiles(mkv_cache *c, int32_t *n_tiles) {
+  if (!c || !n_tiles) return fail(MKV_EINVAL, "NULL argument");
+  *n_tiles = c->dv.n_tiles;
+  return MKV_OK;
+}
+
+mkv_status mkv_profile_enable(mkv_cache *c, int32_t enable, int32_t max_launches) {
+  if (!c) return fail(MKV_EINVAL, "cache is NULL");
+  if (enable && max_launches < 1) return fail(MKV_EINVAL, "max_launches must be >= 1");
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "profile enable");
+  for (int k = 0; k < kProfKinds; ++k) {
+    for (int w = 0; w < 2; ++w) {
+      for (hipEvent_t ev : c->ev[k][w]) hipEventDestroy(ev);
+      c->ev[k][w].clear();
+      if (enable)
+        for (int i = 0; i < max_launches; ++i) {
+          hipEvent_t ev;
+          if ((e = hipEventCreate(&ev)) != hipSuccess) return hip_fail(e, "hipEventCreate");
+          c->ev[k][w].push_back(ev);
+        }
+    }
+    c->prof_n[k] = 0;
+  }
+  c->prof = enable != 0;
+  c->prof_cap = enable ? max_launches : 0;
+  return MKV_OK;
+}
+
+mkv_status mkv_profile_read(mkv_cache *c, int32_t kind, int32_t *launches, double *total_ms) {
+  if (!c || !launches || !total_ms) return fail(MKV_EINVAL, "NULL argument");
+  if (kind < 0 || kind >= kProfKinds) return fail(MKV_EINVAL, "kind out of range");
+  double tot = 0.0;
+  for (int i = 0; i < c->prof_n[kind]; ++i) {
+    hipError_t e = hipEventSynchronize(c->ev[kind][1][i]);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    float ms = 0.f;
+    if ((e = hipEventElapsedTime(&ms, c->ev[kind][0][i], c->ev[kind][1][i])) != hipSuccess)
+      return hip_fail(e, "hipEventElapsedTime");
+    tot += ms;
+  }
+  *launches = c->prof_n[kind];
+  *total_ms = tot;
+  return MKV_OK;
+}
+
+}  // extern "C"
+
+// ---- export -------------------------------------------------------------------------------------
+namespace {
+
+template <typename T>
+mkv_status dget(std::vector<T> &dst, uint64_t src, size_t n) {
+  dst.resize(n);
+  if (n == 0) return MKV_OK;
+  hipError_t e = hipMemcpy(dst.data(), reinterpret_cast<const void *>(src), n * sizeof(T), hipMemcpyDeviceToHost);
+  return check_hip(e, "export copy");
+}
+
+int unpack_code(const uint8_t *row, int c, int bits, int D) {
+  if (bits == 4) return (row[c / 2] >> (4 * (c & 1))) & 15;
+  if (bits == 2) return (row[c / 4] >> (2 * (c & 3))) & 3;
+  return ((row[c / 4] >> (2 * (c & 3))) & 3) | (((row[D / 4 + c / 8] >> (c & 7)) & 1) << 2);
+}
+
+}  // namespace
+
+extern "C" mkv_status mkv_export(mkv_cache *c, int32_t seq, int32_t h, int32_t what, void *host_dst, size_t cap,
+                                 size_t *written) {
+  if (!c || !written) return fail(MKV_EINVAL, "NULL argument");
+  *written = 0;
+  if (seq < 0 || seq >= c->sh.S || h < 0 || h >= c->sh.Hkv) return fail(MKV_EINVAL, "seq or kv_head out of range");
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "export sync");
+  const SeqDesc &d = c->hs[seq];
+  const int D = c->sh.D, G = c->sh.G;
+  std::vector<int32_t> stv;
+  mkv_status st = dget(stv, (uint64_t)(uintptr_t)(c->dv.state + ((size_t)seq * c->sh.Hkv + h) * ST_WORDS), ST_WORDS);
+  if (st != MKV_OK) return st;
+  const int count = stv[ST_COUNT];
+  std::vector<uint8_t> out;
+  auto put = [&](const void *p, size_t bytes) {
+    const uint8_t *b = static_cast<const uint8_t *>(p);
+    out.insert(out.end(), b, b + bytes);
+  };
+  switch (what) {
+    case MKV_EXPORT_COUNTS: {
+      int32_t v[4] = {count, stv[ST_NEXT_POS], d.method == ROCKET ? stv[ST_SEL_COUNT] : count, stv[ST_KEPT]};
+      put(v, sizeof v);
+      break;
+    }
+    case MKV_EXPORT_POSITIONS:
+    case MKV_EXPORT_SCORES: {
+      if (d.method == H2O || d.method == ROCKET) {
+        std::vector<int32_t> pos;
+        if ((st = dget(pos, d.pos + (uint64_t)h * stride_slots(d) * 4, count)) != MKV_OK) return st;
+        std::vector<float> sc;
+        if (d.method == H2O && (st = dget(sc, d.score + (uint64_t)h * stride_slots(d) * 4, count)) != MKV_OK) return st;
+        std::vector<int> order(count);
+        for (int i = 0; i < count; ++i) order[i] = i;
+        std::sort(order.begin(), order.end(), [&](int a, int b) { return pos[a] < pos[b]; });
+        for (int i : order) {
+          if (what == MKV_EXPORT_POSITIONS) put(&pos[i], 4);
+          else if (d.method == H2O) put(&sc[i], 4);
+        }
+        if (what == MKV_EXPORT_SCORES && d.method != H2O) return fail(MKV_EINVAL, "SCORES is for H2O sequences");
+      } else {
+        if (what == MKV_EXPORT_SCORES) return fail(MKV_EINVAL, "SCORES is for H2O sequences");
+        for (int32_t i = 0; i < count; ++i) put(&i, 4);
+      }
+      break;
+    }
+    case MKV_EXPORT_CODES_K:
+    case MKV_EXPORT_CODES_V: {
+      if (d.method != KVQ && d.method != UQ) return fail(MKV_EINVAL, "codes exist for UQ and KVQ sequences");
+      const bool isk = what == MKV_EXPORT_CODES_K;
+      const int n = (d.method == UQ && isk) ? (count / 64) * 64 : count;
+      const int bits = d.method == UQ ? 4 : d.bits;
+      std::vector<uint8_t> raw;
+      if ((st = dget(raw, (isk ? d.kc : d.vc) + (uint64_t)h * stride_codes(d), (size_t)n * d.rowbytes)) != MKV_OK)
+        return st;
+      for (int t = 0; t < n; ++t)
+        for (int ch = 0; ch < D; ++ch) {
+          const uint8_t code = (uint8_t)unpack_code(raw.data() + (size_t)t * d.rowbytes, ch, bits, D);
+          put(&code, 1);
+        }
+      break;
+    }
+    case MKV_EXPORT_OUTLIERS_K:
+    case MKV_EXPORT_OUTLIERS_V: {
+      if (d.method != KVQ) return fail(MKV_EINVAL, "outliers exist for KVQ sequences");
+      std::vector<int32_t> m((size_t)count * D, -1);
+      if (what == MKV_EXPORT_OUTLIERS_K) {
+        std::vector<uint32_t> row, pool;
+        if ((st = dget(row, d.krow + (uint64_t)h * stride_krow(d) * 4, count + 1)) != MKV_OK) return st;
+        if ((st = dget(pool, d.kout + (uint64_t)h * stride_kout(d) * 4, row[count])) != MKV_OK) return st;
+        for (int t = 0; t < count; ++t)
+          for (uint32_t e2 = row[t]; e2 < row[t + 1]; ++e2) m[(size_t)t * D + (pool[e2] & 0xFF)] = (int32_t)(pool[e2] >> 16);
+      } else {
+        std::vector<uint32_t> vo;
+        if ((st = dget(vo, d.vout + (uint64_t)h * stride_vout(d) * 4, (size_t)count * d.nov_slots)) != MKV_OK) return st;
+        for (int t = 0; t < count; ++t)
+          for (int j = 0; j < d.nov_slots; ++j) {
+            const uint32_t ent = vo[(size_t)t * d.nov_slots + j];
+            if (ent == kNoOutlier) break;
+            m[(size_t)t * D + (ent & 0xFF)] = (int32_t)(ent >> 16);
+          }
+      }
+      put(m.data(), m.size() * 4);
+      break;
+    }
+    case MKV_EXPORT_SCALES_K:
+    case MKV_EXPORT_SCALES_V: {
+      if (d.method == KVQ) {
+        if (what == MKV_EXPORT_SCALES_K) {
+          std::vector<float> t2;
+          if ((st = dget(t2, d.kmeta + (uint64_t)h * D * 8, (size_t)2 * D)) != MKV_OK) return st;
+          for (int ch = 0; ch < D; ++ch) put(&t2[2 * ch], 4);
+        } else {
+          std::vector<float> s;
+          if ((st = dget(s, d.vmeta + (uint64_t)h * stride_slots(d) * 4, count)) != MKV_OK) return st;
+          put(s.data(), s.size() * 4);
+        }
+      } else if (d.method == UQ) {
+        std::vector<float> m;
+        if (what == MKV_EXPORT_SCALES_K) {
+          if ((st = dget(m, d.kmeta + (uint64_t)h * stride_uq_kmeta(d, D) * 8, (size_t)(count / 64) * D * 2)) != MKV_OK)
+            return st;
+        } else {
+          if ((st = dget(m, d.vmeta + (uint64_t)h * stride_uq_vmeta(d, D) * 8, (size_t)count * (D / 64) * 2)) != MKV_OK)
+            return st;
+        }
+        put(m.data(), m.size() * 4);
+      } else {
+        return fail(MKV_EINVAL, "scales exist for UQ and KVQ sequences");
+      }
+      break;
+    }
+    case MKV_EXPORT_TOPK: {
+      if (d.method != ROCKET) return fail(MKV_EINVAL, "TOPK is for ROCKET sequences");
+      const int m = stv[ST_SEL_COUNT];
+      std::vector<int32_t> sel, pos;
+      if ((st = dget(sel, d.sel + (uint64_t)h * stride_sel(d) * 4, m)) != MKV_OK) return st;
+      if ((st = dget(pos, d.pos + (uint64_t)h * stride_slots(d) * 4, count)) != MKV_OK) return st;
+      for (int i = 0; i < m; ++i) put(&pos[sel[i]], 4);
+      break;
+    }
+    case MKV_EXPORT_CHANNELS: {
+      if (d.method != ROCKET) return fail(MKV_EINVAL, "CHANNELS is for ROCKET sequences");
+      std::vector<int32_t> ch;
+      if ((st = dget(ch, d.aux1 + (uint64_t)h * D * 4, d.nch)) != MKV_OK) return st;
+      put(ch.data(), ch.size() * 4);
+      break;
+    }
+    default:
+      return fail(MKV_EINVAL, "unknown export kind %d", what);
+  }
+  (void)G;
+  if (out.size() > cap) return fail(MKV_EINVAL, "export needs %zu bytes, cap is %zu", out.size(), cap);
+  if (!out.empty()) std::memcpy(host_dst, out.data(), out.size());
+  *written = out.size();
+  return MKV_OK;
+}

@@ -1,0 +1,99 @@
+// Internal layout shared by the host library and the HIP kernels.
+#pragma once
+
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+namespace mkv {
+
+enum Method : int32_t { FP16 = 0, UQ = 1, KVQ = 2, H2O = 3, ROCKET = 4 };
+
+// Per-(sequence, kv head) device state words.
+enum StateWord : int32_t {
+  ST_COUNT = 0,      // tokens held in the decode region (slots 0..count-1 are valid at attention time)
+  ST_NEXT_POS = 1,   // position the next appended token gets
+  ST_FREE_SLOT = 2,  // H2O: slot the next token is written to
+  ST_KOUT_FILL = 3,  // KVQ: entries used in the key-outlier pool
+  ST_SEL_COUNT = 4,  // ROCKET: tokens selected by the last top-k
+  ST_KEPT = 5,       // tokens kept after prefill (H2O / ROCKET), prompt length otherwise
+  ST_WORDS = 8
+};
+
+constexpr int kTileThreads = 256;
+constexpr int kMaxG = 8;
+constexpr uint32_t kNoOutlier = 0xFFFFFFFFu;
+
+// One sequence's configuration and region base pointers (kv head 0); every
+// region is [Hkv][...] with the per-head stride given by the helpers below.
+struct SeqDesc {
+  int32_t method, bits, n0, cap;          // cap: decode-region slots per kv head
+  int32_t B, R, T, topk;                  // H2O budget/recent; ROCKET keep/topk
+  int32_t window, pool, nch, bp;          // ROCKET window/pool/channels; KVQ outlier bp
+  int32_t n_o, n_ov, nov_slots, rowbytes; // KVQ outlier counts; packed code row bytes
+  int32_t pool_cap, nblk, w_eff, chunk;   // KVQ outlier pool; UQ blocks; window rows; tile tokens
+  int32_t tile_first, tile_count, q_off, pad0;  // partial tiles (per kv head); prompt-q row offset
+  uint64_t k, v;            // fp16 [cap][d] rows (FP16 / H2O / ROCKET)
+  uint64_t kc, vc;          // packed codes [cap][rowbytes] (UQ / KVQ)
+  uint64_t kmeta, vmeta;    // UQ: float2 [nblk][d], float2 [cap][d/64]; KVQ: float2 tau/inv [d], float [cap]
+  uint64_t kres;            // UQ: fp16 [64][d] residual key block
+  uint64_t krow, kout, vout;// KVQ: u32 [cap+1] CSR, u32 [pool_cap], u32 [cap][nov_slots]
+  uint64_t pos, score;      // H2O / ROCKET: int32 [cap], float [cap]
+  uint64_t logits;          // H2O: float [cap][G] log2-domain logits of the last attention
+  uint64_t stage_k, stage_v;// H2O / ROCKET: fp16 [n0][d] prompt staging
+  uint64_t kcm;             // ROCKET: fp16 [d][cap] channel-major keys
+  uint64_t sel, akeys;      // ROCKET: int32 [topk] selected slots; u32 [cap] score keys
+  uint64_t aux0, aux1;      // prefill scratch: H2O float [n0] scores, float2 [G][n0] row stats;
+                            // ROCKET float [n0] votes, float2 [G*w][nchunk] partial row stats
+};
+
+struct Shape {
+  int32_t S, Hq, Hkv, D, G, max_new;
+};
+
+// Per-kv-head strides (in elements of the region's type).
+__host__ __device__ inline int64_t stride_rows(const SeqDesc &s, int D) { return (int64_t)s.cap * D; }
+__host__ __device__ inline int64_t stride_codes(const SeqDesc &s) { return (int64_t)s.cap * s.rowbytes; }
+__host__ __device__ inline int64_t stride_uq_kmeta(const SeqDesc &s, int D) { return (int64_t)s.nblk * D; }
+__host__ __device__ inline int64_t stride_uq_vmeta(const SeqDesc &s, int D) { return (int64_t)s.cap * (D / 64); }
+__host__ __device__ inline int64_t stride_krow(const SeqDesc &s) { return (int64_t)s.cap + 1; }
+__host__ __device__ inline int64_t stride_kout(const SeqDesc &s) { return (int64_t)s.pool_cap; }
+__host__ __device__ inline int64_t stride_vout(const SeqDesc &s) { return (int64_t)s.cap * s.nov_slots; }
+__host__ __device__ inline int64_t stride_slots(const SeqDesc &s) { return (int64_t)s.cap; }
+__host__ __device__ inline int64_t stride_logits(const SeqDesc &s, int G) { return (int64_t)s.cap * G; }
+__host__ __device__ inline int64_t stride_stage(const SeqDesc &s, int D) { return (int64_t)s.n0 * D; }
+__host__ __device__ inline int64_t stride_sel(const SeqDesc &s) { return (int64_t)(s.topk > 0 ? s.topk : 1); }
+
+// Codebook table: for b = 2, 3, 4: cbK[2^b], cbV[2^b], midK[2^b-1], midV[2^b-1].
+__host__ __device__ inline int cb_offset(int bits) {
+  // sizes: b=2: 4+4+3+3 = 14; b=3: 8+8+7+7 = 30; b=4: 16+16+15+15 = 62
+  return bits == 2 ? 0 : bits == 3 ? 14 : 44;
+}
+constexpr int kCbTableFloats = 14 + 30 + 62;
+
+// Kernel launchers (defined in the .hip files).  All enqueue on `st`.
+struct Dev {
+  const SeqDesc *seqs;   // device [S]
+  int32_t *state;        // device [S][Hkv][ST_WORDS]
+  const int4 *tiles;     // device [n_tiles]: seq, kv head, token begin, token end
+  float *partials;       // device [n_tiles][G][D+2]
+  const float *cbtab;    // device [kCbTableFloats]
+  int n_tiles;
+};
+
+hipError_t launch_append_decode(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
+                                hipStream_t st);
+hipError_t launch_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
+                              const uint16_t *k, const uint16_t *v, hipStream_t st);
+hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st);
+hipError_t launch_attention_combine(const Dev &dv, const Shape &sh, float *out, hipStream_t st);
+hipError_t launch_topk(const Dev &dv, const Shape &sh, const uint16_t *q, int32_t *pos_out, int topk_max,
+                       hipStream_t st);
+hipError_t launch_h2o_evict(const Dev &dv, const Shape &sh, hipStream_t st);
+hipError_t launch_h2o_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
+                                  const uint16_t *q_rows, hipStream_t st);
+hipError_t launch_snap_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
+                                   const uint16_t *q_window, hipStream_t st);
+hipError_t launch_init_state(const Dev &dv, const Shape &sh, hipStream_t st);
+
+}  // namespace mkv

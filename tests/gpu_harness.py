@@ -1,0 +1,273 @@
+"""Lock-step parity harness: the HIP path (through the C ABI) against the CPU oracle.
+
+Both sides consume the same seeded inputs from ``workloads``.  Integer results are compared
+exactly (quantization codes, outlier sets, RocketKV top-k positions); attention outputs within
+`tol` of the float64 oracle after dividing by the RMS of the effective values attended over.
+
+H2O evictions and SnapKV / H2O prefill keep-sets are decided on softmax-derived float scores,
+which the GPU accumulates in float32 and the oracle in float64.  Where the oracle's own margin at
+the decision is below TIE_BAND (relative), either choice is correct: the harness records a
+near-tie, adopts the GPU's choice into the oracle's state and continues.  Any other difference
+fails.
+"""
+import sys
+
+import numpy as np
+
+from oracle import codebook, h2o, kvquant, snapkv, uniform
+from oracle.sequence import Sequence
+from workloads import calib_kv, prompt_kv, prompt_q, step_inputs
+
+TIE_BAND = 1e-5
+TOL = 2e-3
+
+_CB_CACHE = {}
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def oracle_codebooks(wl, tokens=256, bp=100):
+    """Oracle-fitted codebooks for b = 2, 3, 4 on the workload's calibration draw."""
+    key = (wl.seed, wl.wid, wl.n_kv_heads, wl.head_dim, tokens, bp)
+    if key not in _CB_CACHE:
+        k, v = calib_kv(wl, tokens=tokens)
+        ks = np.concatenate([kvquant.normalised_inliers_keys(k[:, h], bp) for h in range(wl.n_kv_heads)])
+        vs = np.concatenate([kvquant.normalised_inliers_values(v[:, h], bp) for h in range(wl.n_kv_heads)])
+        cbs = {b: (codebook.lloyd_codebook(ks, b), codebook.lloyd_codebook(vs, b)) for b in (2, 3, 4)}
+        flat = np.concatenate([np.concatenate(cbs[b]) for b in (2, 3, 4)]).astype(np.float32)
+        _CB_CACHE[key] = (cbs, flat)
+    return _CB_CACHE[key]
+
+
+def _window_block(wl, s, window):
+    q = prompt_q(wl, s, last=window)
+    if q.shape[0] < window:
+        pad = np.zeros((window - q.shape[0],) + q.shape[1:], np.float16)
+        q = np.concatenate([pad, q])
+    return q
+
+
+def _keep_set_tie_ok(scores, gpu_keep, ora_keep, protected):
+    """True if the two keep-sets differ only at positions whose oracle scores sit within the
+    tie band of the selection threshold."""
+    g, o = set(int(x) for x in gpu_keep), set(int(x) for x in ora_keep)
+    if g == o:
+        return True, 0
+    if len(g) != len(o):
+        return False, -1
+    diff = sorted(g ^ o)
+    kept_cand = [j for j in o if j not in protected]
+    if not kept_cand:
+        return False, -1
+    thr = min(scores[j] for j in kept_cand)
+    for j in diff:
+        if j in protected or abs(scores[j] - thr) > TIE_BAND * max(abs(thr), 1e-30):
+            return False, -1
+    return True, len(diff) // 2
+
+
+class Run:
+    """One GPU cache and its oracle twins for a workload."""
+
+    def __init__(self, wl, steps, tile_tokens=None, device="cuda"):
+        import torch
+        from paper_2609_07966_amd.cache import KVCache
+        self.torch = torch
+        self.wl = wl
+        self.steps = steps
+        S = wl.n_seqs
+        self.cfgs = [wl.cfg(s) for s in range(S)]
+        self.need_cb = any(c["method"] == "kvq" for c in self.cfgs)
+        cbs, flat = oracle_codebooks(wl) if self.need_cb else (None, None)
+        self.cbs = cbs
+        self.cache = KVCache((S, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, steps), self.cfgs, wl.prompt_lens,
+                             codebooks=None if flat is None else list(flat), device=device)
+        self.dev = device
+        self.near_ties = 0
+        self.max_err = 0.0
+        self.oracle = []
+        self.prompts = []
+        for s in range(S):
+            kp, vp = prompt_kv(wl, s)
+            c = self.cfgs[s]
+            qp = None
+            if c["method"] == "h2o":
+                qp = prompt_q(wl, s)
+            elif c["method"] == "rocket":
+                qp = prompt_q(wl, s, last=c.get("window", 32))
+            self.prompts.append((kp, vp, qp))
+
+    def h(self, x):
+        return self.torch.from_numpy(np.ascontiguousarray(x)).to(self.dev)
+
+    # ---- prefill -----------------------------------------------------------------------------
+    def prefill(self, check_codes=True):
+        wl, cache = self.wl, self.cache
+        k = np.concatenate([p[0] for p in self.prompts])
+        v = np.concatenate([p[1] for p in self.prompts])
+        cache.append_prompt(self.h(k), self.h(v))
+        h2o_q = [self.prompts[s][2] for s in range(wl.n_seqs) if self.cfgs[s]["method"] == "h2o"]
+        if h2o_q:
+            cache.h2o_prefill(self.h(np.concatenate(h2o_q)))
+        rk = [_window_block(wl, s, self.cfgs[s].get("window", 32)) for s in range(wl.n_seqs)
+              if self.cfgs[s]["method"] == "rocket"]
+        if rk:
+            cache.snap_prefill(self.h(np.concatenate(rk)))
+        self.torch.cuda.synchronize()
+        for s in range(wl.n_seqs):
+            kp, vp, qp = self.prompts[s]
+            self.oracle.append(self._oracle_prefill(s, kp, vp, qp))
+            if check_codes:
+                self.check_codes(s)
+
+    def _oracle_prefill(self, s, kp, vp, qp):
+        c = self.cfgs[s]
+        wl = self.wl
+        seq = Sequence(c, kp, vp, wl.n_q_heads, q_prompt=qp, codebooks=self.cbs)
+        G = wl.group
+        if c["method"] == "h2o":
+            keeps = []
+            for h in range(wl.n_kv_heads):
+                gk = self.cache.export(s, h, "positions")
+                ok_keep = seq.heads[h].pos
+                n0 = kp.shape[0]
+                ok, nt = _keep_set_tie_ok(seq.S[h], gk, ok_keep, set(range(n0 - seq.R, n0)) if seq.B < n0 else set())
+                assert ok, f"H2O prefill keep-set differs beyond the tie band (seq {s} head {h})"
+                self.near_ties += nt
+                keeps.append(gk)
+                sc = self.cache.export(s, h, "scores")
+                ref = seq.S[h][gk]
+                np.testing.assert_allclose(sc, ref, rtol=1e-4, atol=1e-5)
+            seq.adopt_h2o_prefill(keeps)
+        elif c["method"] == "rocket":
+            keeps = []
+            for h in range(wl.n_kv_heads):
+                gk = self.cache.export(s, h, "positions")
+                n0 = kp.shape[0]
+                if seq.T >= n0:
+                    assert list(gk) == list(range(n0))
+                else:
+                    w = min(seq.w, n0)
+                    u = snapkv.pooled_votes(seq.qw[:, h * G:(h + 1) * G], kp[:, h], seq.w, seq.pool)
+                    u_full = np.concatenate([u, np.full(w, np.inf)])
+                    ok, nt = _keep_set_tie_ok(u_full, gk, seq.keep[h], set(range(n0 - w, n0)))
+                    assert ok, f"SnapKV keep-set differs beyond the tie band (seq {s} head {h})"
+                    self.near_ties += nt
+                keeps.append(gk)
+            seq.adopt_snap_keep(keeps)
+        return seq
+
+    def check_codes(self, s):
+        c = self.cfgs[s]
+        seq = None if not self.oracle or len(self.oracle) <= s else self.oracle[s]
+        wl = self.wl
+        kp, vp, _ = self.prompts[s]
+        for h in range(wl.n_kv_heads):
+            if c["method"] == "kvq":
+                b, bp = c["bits"], c.get("outlier_bp", 100)
+                cbk, cbv = self.cbs[b]
+                tau, inv = kvquant.calibrate_keys(kp[:, h], bp)
+                np.testing.assert_array_equal(self.cache.export(s, h, "scales_k"), tau)
+                ck, ok = kvquant.quantize_keys(kp[:, h], tau, inv, cbk, bp)
+                cv, sv, ov = kvquant.quantize_values(vp[:, h], cbv, bp)
+                n = kp.shape[0]
+                gk = self.cache.export(s, h, "codes_k").reshape(-1, wl.head_dim)[:n]
+                gv = self.cache.export(s, h, "codes_v").reshape(-1, wl.head_dim)[:n]
+                np.testing.assert_array_equal(gk, ck)
+                np.testing.assert_array_equal(gv, cv)
+                np.testing.assert_array_equal(self.cache.export(s, h, "scales_v")[:n], sv)
+                gok = self.cache.export(s, h, "outliers_k").reshape(-1, wl.head_dim)[:n]
+                gov = self.cache.export(s, h, "outliers_v").reshape(-1, wl.head_dim)[:n]
+                np.testing.assert_array_equal(gok >= 0, ok)
+                np.testing.assert_array_equal(gov >= 0, ov)
+                np.testing.assert_array_equal(gok[ok].astype(np.uint16), kp[:, h].view(np.uint16)[ok])
+                np.testing.assert_array_equal(gov[ov].astype(np.uint16), vp[:, h].view(np.uint16)[ov])
+            elif c["method"] == "uq":
+                n = kp.shape[0]
+                nb = n // 64
+                if nb:
+                    ck, _, _ = uniform.quantize_key_blocks(kp[:, h], 4)
+                    gk = self.cache.export(s, h, "codes_k").reshape(-1, wl.head_dim)
+                    np.testing.assert_array_equal(gk[:nb * 64], ck)
+                cv, _, _ = uniform.quantize_value_rows(vp[:, h], 4)
+                gv = self.cache.export(s, h, "codes_v").reshape(-1, wl.head_dim)[:n]
+                np.testing.assert_array_equal(gv, cv)
+
+    # ---- decode ------------------------------------------------------------------------------
+    def step(self, t, check_codes=False):
+        torch, wl, cache = self.torch, self.wl, self.cache
+        kn, vn, q = step_inputs(wl, t)
+        kd, vd, qd = self.h(kn), self.h(vn), self.h(q)
+        out = torch.empty((wl.n_seqs, wl.n_q_heads, wl.head_dim), dtype=torch.float32, device=self.dev)
+        cache.append(kd, vd)
+        cache.topk(qd)
+        cache.attention(qd, out)
+        cache.evict()
+        gout = out.cpu().numpy()
+        G = wl.group
+        for s, seq in enumerate(self.oracle):
+            ref, info = seq.step(kn[s], vn[s], q[s])
+            c = self.cfgs[s]
+            if c["method"] == "rocket":
+                for h in range(wl.n_kv_heads):
+                    gsel = cache.export(s, h, "topk")
+                    osel = info["selected"][h]["positions"]
+                    np.testing.assert_array_equal(gsel, osel, err_msg=f"top-k seq {s} head {h} step {t}")
+                    gch = cache.export(s, h, "channels")
+                    np.testing.assert_array_equal(gch, info["selected"][h]["channels"])
+            for h in range(wl.n_kv_heads):
+                rms = float(np.sqrt(np.mean(np.asarray(info["v_eff"][h], np.float64) ** 2)))
+                err = np.abs(gout[s, h * G:(h + 1) * G] - ref[h * G:(h + 1) * G]).max() / max(rms, 1e-30)
+                self.max_err = max(self.max_err, err)
+                assert err <= TOL, f"seq {s} ({c['method']}) head {h} step {t}: error {err:.3e} > {TOL}"
+            if c["method"] == "h2o":
+                ev = []
+                for h in range(wl.n_kv_heads):
+                    hd = seq.heads[h]
+                    gpos = set(int(x) for x in cache.export(s, h, "positions"))
+                    opos = set(int(x) for x in hd.pos)
+                    want = info["evict"][h]
+                    if want is None:
+                        assert gpos == opos, f"H2O seq {s} head {h} step {t}: unexpected eviction"
+                        ev.append(None)
+                        continue
+                    gone = opos - gpos
+                    assert len(gone) == 1 and gpos <= opos, f"H2O seq {s} head {h} step {t}: bad eviction"
+                    g_ev = gone.pop()
+                    if g_ev != want:
+                        i_g = int(np.nonzero(hd.pos == g_ev)[0][0])
+                        i_o = int(np.nonzero(hd.pos == want)[0][0])
+                        assert hd.pos[i_g] < t + seq.n0 - seq.R + 1, "evicted a protected recent token"
+                        a, b = hd.score[i_g], hd.score[i_o]
+                        assert abs(a - b) <= TIE_BAND * max(abs(b), 1e-30), \
+                            f"H2O seq {s} head {h} step {t}: evicted {g_ev} (score {a}) vs {want} ({b})"
+                        self.near_ties += 1
+                    ev.append(g_ev)
+                    gsc = cache.export(s, h, "scores")
+                    seq.apply_evictions([None] * h + [g_ev] + [None] * (wl.n_kv_heads - h - 1))
+                    np.testing.assert_allclose(gsc, hd.score, rtol=1e-4, atol=1e-5)
+                    continue
+            if check_codes and c["method"] in ("kvq",):
+                self._check_decode_codes(s, seq)
+        return gout
+
+    def _check_decode_codes(self, s, seq):
+        wl = self.wl
+        for h in range(wl.n_kv_heads):
+            n = seq.kq[h]["codes"].shape[0]
+            gk = self.cache.export(s, h, "codes_k").reshape(-1, wl.head_dim)[:n]
+            np.testing.assert_array_equal(gk, seq.kq[h]["codes"])
+            gv = self.cache.export(s, h, "codes_v").reshape(-1, wl.head_dim)[:n]
+            np.testing.assert_array_equal(gv, seq.vq[h]["codes"])
+            gok = self.cache.export(s, h, "outliers_k").reshape(-1, wl.head_dim)[:n]
+            np.testing.assert_array_equal(gok >= 0, seq.kq[h]["outlier"])
+
+    def run(self, check_codes=True):
+        self.prefill(check_codes=check_codes)
+        for t in range(self.steps):
+            self.step(t, check_codes=check_codes and t == self.steps - 1)
+        self.cache.close()
+        return self
