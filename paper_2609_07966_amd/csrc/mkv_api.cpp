@@ -606,12 +606,16 @@ extern "C" mkv_status mkv_export(mkv_cache *c, int32_t seq, int32_t h, int32_t w
     case MKV_EXPORT_POSITIONS:
     case MKV_EXPORT_SCORES: {
       if (d.method == H2O || d.method == ROCKET) {
+        // H2O: after an eviction the freed slot can lie below `count`, and then slots
+        // 0..count hold the count retained tokens around that hole (pos -1)
+        const int nread = (d.method == H2O && stv[ST_FREE_SLOT] < count) ? count + 1 : count;
         std::vector<int32_t> pos;
-        if ((st = dget(pos, d.pos + (uint64_t)h * stride_slots(d) * 4, count)) != MKV_OK) return st;
+        if ((st = dget(pos, d.pos + (uint64_t)h * stride_slots(d) * 4, nread)) != MKV_OK) return st;
         std::vector<float> sc;
-        if (d.method == H2O && (st = dget(sc, d.score + (uint64_t)h * stride_slots(d) * 4, count)) != MKV_OK) return st;
-        std::vector<int> order(count);
-        for (int i = 0; i < count; ++i) order[i] = i;
+        if (d.method == H2O && (st = dget(sc, d.score + (uint64_t)h * stride_slots(d) * 4, nread)) != MKV_OK) return st;
+        std::vector<int> order;
+        for (int i = 0; i < nread; ++i)
+          if (pos[i] >= 0) order.push_back(i);
         std::sort(order.begin(), order.end(), [&](int a, int b) { return pos[a] < pos[b]; });
         for (int i : order) {
           if (what == MKV_EXPORT_POSITIONS) put(&pos[i], 4);
