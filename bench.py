@@ -1,0 +1,312 @@
+"""Decode-attention benchmark on one MI355X.
+
+One step = every sequence of the batch advances one token through the whole hot path:
+append (and quantize) -> RocketKV top-k selection -> split-K attention + combine (H2O score
+accumulation) -> H2O eviction, all through the C ABI (mkv_decode_step).
+
+Headline workload: the per-prompt mixed batch — 64 sequences, 32 query / 8 kv heads x 128,
+prompt lengths log-uniform in [1024, 32768], each sequence carrying one of the 11 compression
+configurations (seeded).  It is the only workload whose step runs every hot-path kernel, and its
+~0.7 GB of compressed KV per step exceeds the 256 MB Infinity Cache, so it reads HBM.
+
+Also reported per configuration (``per_config``): the Llama-3-8B-shaped layer (8 seqs, prompt
+4096) under FP16 and KVQuant 4/3/2-bit, H2O-20 at prompt 8192, RocketKV-4096 at prompt 32768.
+Their working sets fit in the Infinity Cache, so each runs R independent cache replicas in
+round-robin, R x bytes >= 512 MiB, and each step reads cold data.
+
+Prints one JSON line.  Inputs are synthetic (workloads.gen), resident in HBM before timing.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+MALL_BYTES = 256 << 20
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ---- algorithmic bytes of the attention partial kernel ----------------------------------------
+
+def active_tokens(cfg, n0, step):
+    """Tokens attended per kv head at decode step `step` (0-based, after that step's append)."""
+    m = cfg["method"]
+    if m in ("fp16", "uq", "kvq"):
+        return n0 + step + 1
+    if m == "h2o":
+        B = cfg["budget_pct"] * n0 // 100
+        return min(min(B, n0) + step + 1, B + 1)
+    T = cfg["keep_tokens"]
+    k = cfg.get("topk", 0) or T // 2
+    return min(k, min(T, n0) + step + 1)
+
+
+def token_bytes(cfg, n0, step, D, G):
+    """Bytes one kv head's attention must read (and write) at this step."""
+    n = active_tokens(cfg, n0, step)
+    m = cfg["method"]
+    if m == "fp16":
+        return n * 4 * D
+    if m == "h2o":
+        return n * (4 * D + 4 * G)          # rows + the logits written for score accumulation
+    if m == "rocket":
+        return n * (4 * D + 4)              # gathered rows + selected index
+    if m == "uq":
+        full = (n // 64) * 64
+        k = full * (D // 2 + D // 8) + (n - full) * 2 * D   # codes + per-block (min, step); fp16 tail
+        v = n * (D // 2 + (D // 64) * 8)
+        return k + v
+    b = cfg["bits"]
+    bp = cfg.get("outlier_bp", 100)
+    nov = max(1, (D * bp + 5000) // 10000) if bp else 1
+    k_out = bp / 10000.0 * D                # expected key outliers per token
+    return n * (D * b // 4 + 4 + 4 + 4 * nov + 4 * k_out)
+
+
+def launch_bytes(wl, step, n_tiles):
+    D, G, Hkv = wl.head_dim, wl.group, wl.n_kv_heads
+    tot = 0.0
+    for s in range(wl.n_seqs):
+        tot += Hkv * token_bytes(wl.cfg(s), wl.prompt_lens[s], step, D, G)
+    tot += wl.n_seqs * wl.n_q_heads * D * 2             # q
+    tot += n_tiles * G * (D + 2) * 4                    # partial (m, l, o) writes
+    return tot
+
+
+# ---- GPU leg ----------------------------------------------------------------------------------
+
+def product_codebooks(wl, tokens=1024):
+    from paper_2609_07966_amd import _lib
+    from workloads import calib_kv
+    k, v = calib_kv(wl, tokens=tokens)
+    flat = []
+    for b in (2, 3, 4):
+        ck, cv = _lib.mkv_fit_codebooks(k.tobytes(), v.tobytes(), tokens, wl.n_kv_heads, wl.head_dim, b, 100)
+        flat += ck + cv
+    return flat
+
+
+def run_gpu(wl, steps, warmup, replicas=1, label=""):
+    import torch
+    from paper_2609_07966_amd import _lib
+    from paper_2609_07966_amd.cache import KVCache
+    from workloads import prompt_kv, prompt_q, step_inputs
+    S, Hq, Hkv, D = wl.n_seqs, wl.n_q_heads, wl.n_kv_heads, wl.head_dim
+    cfgs = [wl.cfg(s) for s in range(S)]
+    total_steps = warmup + steps
+    per_rep = math.ceil(total_steps / replicas)
+    t0 = time.time()
+    cb = product_codebooks(wl) if any(c["method"] == "kvq" for c in cfgs) else None
+    dev = "cuda"
+    stream = torch.cuda.current_stream()
+    caches = [KVCache((S, Hq, Hkv, D, per_rep), cfgs, wl.prompt_lens, codebooks=cb, device=dev, stream=stream)
+              for _ in range(replicas)]
+    # prompt K/V (all sequences), H2O prompt queries, RocketKV window queries
+    kp, vp = zip(*[prompt_kv(wl, s) for s in range(S)])
+    k_all = torch.from_numpy(np.concatenate(kp)).to(dev)
+    v_all = torch.from_numpy(np.concatenate(vp)).to(dev)
+    del kp, vp
+    qh = [prompt_q(wl, s) for s in range(S) if cfgs[s]["method"] == "h2o"]
+    q_h2o = torch.from_numpy(np.concatenate(qh)).to(dev) if qh else None
+    del qh
+    qw = []
+    for s in range(S):
+        if cfgs[s]["method"] == "rocket":
+            w = cfgs[s]["window"]
+            q = prompt_q(wl, s, last=w)
+            if q.shape[0] < w:
+                q = np.concatenate([np.zeros((w - q.shape[0],) + q.shape[1:], np.float16), q])
+            qw.append(q)
+    q_win = torch.from_numpy(np.concatenate(qw)).to(dev) if qw else None
+    for c in caches:
+        c.append_prompt(k_all, v_all)
+        if q_h2o is not None:
+            c.h2o_prefill(q_h2o)
+        if q_win is not None:
+            c.snap_prefill(q_win)
+    torch.cuda.synchronize()
+    del k_all, v_all, q_h2o, q_win
+    t_prefill = time.time() - t0
+    ins = [step_inputs(wl, t) for t in range(total_steps)]
+    kn = torch.from_numpy(np.stack([x[0] for x in ins])).to(dev)
+    vn = torch.from_numpy(np.stack([x[1] for x in ins])).to(dev)
+    qn = torch.from_numpy(np.stack([x[2] for x in ins])).to(dev)
+    out = torch.empty((S, Hq, D), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    log(f"[bench] {label}: prefill+inputs {time.time() - t0:.1f}s (prefill {t_prefill:.1f}s), replicas={replicas}")
+    for t in range(warmup):
+        caches[t % replicas].step(kn[t], vn[t], qn[t], out)
+    torch.cuda.synchronize()
+    for c in caches:
+        _lib.mkv_profile_enable(c.h, 1, per_rep + 1)
+    torch.cuda.synchronize()
+    a = time.perf_counter()
+    for i in range(steps):
+        t = warmup + i
+        caches[t % replicas].step(kn[t], vn[t], qn[t], out)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - a
+    kinds = {}
+    for kind in ("partial", "combine", "append", "topk", "evict"):
+        n, ms = 0, 0.0
+        for c in caches:
+            a_n, a_ms = _lib.mkv_profile_read(c.h, kind)
+            n += a_n
+            ms += a_ms
+        kinds[kind] = (n, ms)
+    n_tiles = caches[0].n_tiles()
+    bytes_steps = [launch_bytes(wl, warmup + i, n_tiles) for i in range(steps)]
+    avg_bytes = float(np.mean(bytes_steps))
+    n_part, ms_part = kinds["partial"]
+    avg_part_ms = ms_part / max(n_part, 1)
+    res = {
+        "steps": steps, "ms_per_step": elapsed / steps * 1e3, "steps_per_s": steps / elapsed,
+        "partial_ms": avg_part_ms, "partial_bytes": avg_bytes,
+        "partial_gbs": avg_bytes / (avg_part_ms * 1e-3) / 1e9,
+        "step_gbs": avg_bytes / (elapsed / steps) / 1e9,
+        "n_tiles": n_tiles, "replicas": replicas,
+        "kernel_ms": {k: (v[1] / max(v[0], 1)) for k, v in kinds.items() if v[0]},
+    }
+    for c in caches:
+        c.close()
+    del caches, kn, vn, qn, out
+    torch.cuda.empty_cache()
+    return res
+
+
+def per_config_runs(args):
+    from workloads import make_workload
+    runs = []
+    cases = [("llama_layer", "FP16"), ("llama_layer", "KVQ4"), ("llama_layer", "KVQ3"), ("llama_layer", "KVQ2"),
+             ("h2o", "H2O-20"), ("rocket", "Rocket-4096")]
+    for name, cfg in cases:
+        wl = make_workload(name, seed=args.seed, config_ids=cfg)
+        b1 = launch_bytes(wl, 0, 0)
+        reps = max(1, math.ceil(2 * MALL_BYTES / b1))
+        r = run_gpu(wl, args.cfg_steps, 2, replicas=reps, label=f"{name}/{cfg}")
+        runs.append({"workload": name, "config": cfg, "steps_per_s": round(r["steps_per_s"], 1),
+                     "ms_per_step": round(r["ms_per_step"], 4),
+                     "attn_partial_us": round(r["partial_ms"] * 1e3, 2),
+                     "attn_partial_GBs": round(r["partial_gbs"], 1),
+                     "attn_partial_frac_of_peak": round(r["partial_gbs"] / PEAK_HBM_GBS, 4),
+                     "step_GBs": round(r["step_gbs"], 1), "replicas": reps,
+                     "bytes_per_step_MB": round(r["partial_bytes"] / 1e6, 2)})
+        log(f"[bench] {name}/{cfg}: {json.dumps(runs[-1])}")
+    return runs
+
+
+# ---- CPU baseline: the oracle on the same workload ---------------------------------------------
+
+def cpu_baseline(wl, steps):
+    """The CPU oracle decodes the full batch for `steps` steps (prefill state built untimed;
+    H2O / RocketKV keep-sets taken as the most recent tokens so that no O(n^2) prefill scoring
+    runs on the host)."""
+    from oracle.codebook import lloyd_codebook
+    from oracle import kvquant
+    from oracle.sequence import Sequence
+    from workloads import calib_kv, prompt_kv, step_inputs
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    k, v = calib_kv(wl, tokens=64)
+    ks = np.concatenate([kvquant.normalised_inliers_keys(k[:, h], 100) for h in range(wl.n_kv_heads)])
+    vs = np.concatenate([kvquant.normalised_inliers_values(v[:, h], 100) for h in range(wl.n_kv_heads)])
+    cbs = {b: (lloyd_codebook(ks, b), lloyd_codebook(vs, b)) for b in (2, 3, 4)}
+    seqs = []
+    for s in range(wl.n_seqs):
+        c = wl.cfg(s)
+        kp, vp = prompt_kv(wl, s)
+        n0 = kp.shape[0]
+        keep = None
+        if c["method"] == "h2o":
+            B = c["budget_pct"] * n0 // 100
+            keep = [np.arange(n0 - min(B, n0), n0)] * wl.n_kv_heads
+        elif c["method"] == "rocket":
+            keep = [np.arange(n0 - min(c["keep_tokens"], n0), n0)] * wl.n_kv_heads
+        seqs.append(Sequence(c, kp, vp, wl.n_q_heads, codebooks=cbs, keep=keep))
+    a = time.perf_counter()
+    for t in range(steps):
+        kn, vn, q = step_inputs(wl, t)
+        for s, seq in enumerate(seqs):
+            _, info = seq.step(kn[s], vn[s], q[s])
+            if seq.method == "h2o":
+                seq.apply_evictions(info["evict"])
+    el = time.perf_counter() - a
+    return {"value": round(steps / el, 4), "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"the full {wl.n_seqs}-sequence mixed batch, {steps} decode steps of the float64 oracle "
+                      f"(prefill state built untimed; H2O/RocketKV keep-sets fixed to the most recent tokens)",
+            "seconds": round(el, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=120)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cfg-steps", type=int, default=48)
+    ap.add_argument("--cpu-steps", type=int, default=2)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-per-config", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the decode path shards by "
+              f"independent sequences with no exchange, so N GPUs run N copies of this benchmark.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2609_07966_amd import _lib
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2609_07966_amd import build
+        build.build()
+    _lib.lib()
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    from workloads import make_workload
+    wl = make_workload("mixed", seed=args.seed, steps=args.warmup + args.steps)
+    head = run_gpu(wl, args.steps, args.warmup, label="mixed")
+    per_cfg = [] if args.no_per_config else per_config_runs(args)
+    cpu = None if args.no_cpu else cpu_baseline(wl, args.cpu_steps)
+    counts = {}
+    for s in range(wl.n_seqs):
+        counts[wl.cfg(s)["name"]] = counts.get(wl.cfg(s)["name"], 0) + 1
+    line = {
+        "metric": "decode-attn steps/sec & achieved HBM TB/s (% of peak) per KV compression config",
+        "value": round(head["steps_per_s"], 2),
+        "unit": "steps/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(head["ms_per_step"], 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16 storage (fp16 / packed 2-4 bit codes), f32 compute",
+        "data": "synthetic (seeded; workloads.gen)",
+        "config": {"workload": "mixed: 64 seqs, 32q/8kv x 128, prompts log-uniform [1024, 32768], "
+                               "11 configs assigned uniformly (seed 0), one ragged launch per stage",
+                   "n_seqs": wl.n_seqs, "prompt_tokens": int(sum(wl.prompt_lens)), "configs": counts,
+                   "parallelism": "single GPU"},
+        "hbm_TBs_attention": round(head["partial_gbs"] / 1e3, 3),
+        "pct_of_peak_attention": round(100 * head["partial_gbs"] / PEAK_HBM_GBS, 1),
+        "roofline": {"bound": "hbm", "achieved": round(head["partial_gbs"], 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(head["partial_gbs"] / PEAK_HBM_GBS, 4), "traffic": None,
+                     "kernel": "k_attn_partial", "bytes_per_launch": round(head["partial_bytes"]),
+                     "avg_launch_us": round(head["partial_ms"] * 1e3, 2)},
+        "kernel_us": {k: round(v * 1e3, 2) for k, v in head["kernel_ms"].items()},
+        "per_config": per_cfg,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -21,10 +21,12 @@ from .attention import softmax_attention
 
 
 class Sequence:
-    def __init__(self, cfg, k_prompt, v_prompt, n_q_heads, q_prompt=None, codebooks=None):
+    def __init__(self, cfg, k_prompt, v_prompt, n_q_heads, q_prompt=None, codebooks=None, keep=None):
         """cfg: a configuration row (dict); k_prompt, v_prompt [n0][Hkv][d] fp16;
         q_prompt: [n0][Hq][d] (H2O) or at least the last `window` rows (RocketKV);
-        codebooks: {bits: (cb_k, cb_v)} float32 ascending (KVQuant)."""
+        codebooks: {bits: (cb_k, cb_v)} float32 ascending (KVQuant);
+        keep: optional per-kv-head prefill keep-sets for H2O / RocketKV, adopted instead of
+        scoring the prompt (H2O scores then start at 0) — for callers that time decode only."""
         self.cfg = dict(cfg)
         self.method = cfg["method"]
         self.kp = np.asarray(k_prompt)
@@ -41,23 +43,30 @@ class Sequence:
             self._init_kvq(codebooks)
         elif m == "h2o":
             self.B, self.R = h2o.budget(cfg["budget_pct"], self.n0)
-            self.qp = np.asarray(q_prompt)
-            self.S = [h2o.prefill_scores(self.qp[:, h * self.G:(h + 1) * self.G], self.kp[:, h])
-                      for h in range(self.hkv)]
             self.heads = None
-            self.adopt_h2o_prefill([h2o.prefill_keep(self.S[h], self.B, self.R)
-                                    for h in range(self.hkv)])
+            if keep is not None:
+                self.S = [np.zeros(self.n0) for _ in range(self.hkv)]
+                self.adopt_h2o_prefill(keep)
+            else:
+                self.qp = np.asarray(q_prompt)
+                self.S = [h2o.prefill_scores(self.qp[:, h * self.G:(h + 1) * self.G], self.kp[:, h])
+                          for h in range(self.hkv)]
+                self.adopt_h2o_prefill([h2o.prefill_keep(self.S[h], self.B, self.R)
+                                        for h in range(self.hkv)])
         elif m == "rocket":
             self.T = int(cfg["keep_tokens"])
             self.w = int(cfg.get("window", 32))
             self.pool = int(cfg.get("pool", 7))
             self.nc = int(cfg.get("n_channels", 32))
             self.topk = rocketkv.default_topk(self.T, cfg.get("topk", 0))
-            qw = np.asarray(q_prompt)[-min(self.w, self.n0):]
-            self.qw = qw
-            self.adopt_snap_keep([snapkv.snap_keep(qw[:, h * self.G:(h + 1) * self.G],
-                                                   self.kp[:, h], self.T, self.w, self.pool)
-                                  for h in range(self.hkv)])
+            if keep is not None:
+                self.adopt_snap_keep(keep)
+            else:
+                qw = np.asarray(q_prompt)[-min(self.w, self.n0):]
+                self.qw = qw
+                self.adopt_snap_keep([snapkv.snap_keep(qw[:, h * self.G:(h + 1) * self.G],
+                                                       self.kp[:, h], self.T, self.w, self.pool)
+                                      for h in range(self.hkv)])
         elif m != "fp16":
             raise ValueError(m)
 
