@@ -12,6 +12,7 @@ namespace mkv {
 namespace {
 
 constexpr int NT = 256;
+constexpr int kTopkLdsKeys = 10240;  // score keys of up to this many retained tokens stay in LDS
 
 // Compact positions [0, n) whose flag is set into ascending slots; calls emit(j, slot) for each.
 // flag(j, eq_before) may use eq_before = number of keys equal to the threshold at indices < j.
@@ -42,9 +43,10 @@ __global__ __launch_bounds__(NT) void k_topk(const SeqDesc *__restrict__ seqs, i
   __shared__ float s_a[D];
   __shared__ float s_qb[D];
   __shared__ int s_ch[D];
-  __shared__ int hist[256];
+  __shared__ int whist[NT / 64][256];
   __shared__ int s3[3];
   __shared__ int s_tmp[NT / 64];
+  __shared__ uint32_t s_keys[kTopkLdsKeys];
   const int seq = blockIdx.x / Hkv, h = blockIdx.x % Hkv;
   const SeqDesc &sd = seqs[seq];
   if (sd.method != ROCKET) return;
@@ -105,69 +107,85 @@ __global__ __launch_bounds__(NT) void k_topk(const SeqDesc *__restrict__ seqs, i
     return;
   }
 
-  // approximate scores from the channel-major key copy: one lane per token, channels ascending,
-  // acc = fl32(acc + fl32(qbar_c * k_jc))
+  // approximate scores from the channel-major key copy: one lane per token (4 independent tokens
+  // per lane in flight), channels ascending, acc = fl32(acc + fl32(qbar_c * k_jc)); the keys stay
+  // in LDS when they fit
   const uint16_t *kcm = reinterpret_cast<const uint16_t *>(sd.kcm) + h * stride_rows(sd, D);
   uint32_t *akeys = reinterpret_cast<uint32_t *>(sd.akeys) + h * stride_slots(sd);
-  for (int j = threadIdx.x; j < n; j += NT) {
-    float acc = 0.f;
-    for (int i = 0; i < nch; ++i) acc = __fadd_rn(acc, __fmul_rn(s_sel_qb[i], h2f(kcm[(size_t)s_sel_ch[i] * sd.cap + j])));
-    akeys[j] = float_key(acc);
+  const bool in_lds = n <= kTopkLdsKeys;
+  const int cap = sd.cap;
+  for (int j0 = threadIdx.x; j0 < n; j0 += 4 * NT) {
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < nch; ++i) {
+      const float qb = s_sel_qb[i];
+      const uint16_t *row = kcm + (size_t)s_sel_ch[i] * cap;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int j = j0 + r * NT;
+        if (j < n) acc[r] = __fadd_rn(acc[r], __fmul_rn(qb, h2f(gld(row + j))));
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int j = j0 + r * NT;
+      if (j < n) {
+        if (in_lds) s_keys[j] = float_key(acc[r]);
+        else gst(akeys + j, float_key(acc[r]));
+      }
+    }
   }
   __syncthreads();
+  auto getk = [&](int i) { return in_lds ? s_keys[i] : gld(akeys + i); };
   uint32_t kth;
   int n_eq, need;
-  radix_select_kth<NT>(n, k, [&](int i) { return akeys[i]; }, hist, s3, &kth, &n_eq, &need);
-  compact_ascending(
-      n, [&](int j, int eq_before) { const uint32_t kk = akeys[j]; return kk > kth || (kk == kth && eq_before < need); },
-      [&](int j) { return akeys[j] == kth; }, [&](int j, int slot) { if (slot < k) sel[slot] = j; }, s_tmp);
+  radix_select_kth_waves<NT>(n, k, getk, whist, s3, s_tmp, &kth, &n_eq, &need);
+  // each thread takes a contiguous run of tokens; counts of keys above and equal to the
+  // threshold before its run place its selected tokens in ascending order
+  const int per = (n + NT - 1) / NT;
+  const int ja = min(n, (int)threadIdx.x * per), jb = min(n, ja + per);
+  int gt = 0, eq = 0;
+  for (int j = ja; j < jb; ++j) {
+    const uint32_t kk = getk(j);
+    gt += kk > kth ? 1 : 0;
+    eq += kk == kth ? 1 : 0;
+  }
+  int tot;
+  const int gt_before = block_exclusive_scan<NT>(gt, s_tmp, &tot);
+  int eq_run = block_exclusive_scan<NT>(eq, s_tmp, &tot);
+  int slot = gt_before + min(eq_run, need);
+  for (int j = ja; j < jb; ++j) {
+    const uint32_t kk = getk(j);
+    const bool take = kk > kth || (kk == kth && eq_run < need);
+    eq_run += kk == kth ? 1 : 0;
+    if (take && slot < k) gst(sel + slot, j);
+    slot += take ? 1 : 0;
+  }
   __syncthreads();
   if (pos_out != nullptr)
     for (int i = threadIdx.x; i < topk_max; i += NT)
-      pos_out[((size_t)seq * Hkv + h) * topk_max + i] = i < k ? pos[sel[i]] : -1;
+      pos_out[((size_t)seq * Hkv + h) * topk_max + i] = i < k ? gld(pos + gld(sel + i)) : -1;
   if (threadIdx.x == 0) st[ST_SEL_COUNT] = k;
 }
 
 // ---- H2O decode eviction ------------------------------------------------------------------------
-__global__ __launch_bounds__(NT) void k_h2o_evict(const SeqDesc *__restrict__ seqs, int32_t *state, int Hkv) {
-  __shared__ unsigned long long s_best[NT / 64];
-  const int seq = blockIdx.x / Hkv, h = blockIdx.x % Hkv;
+// The attention combine pass has already accumulated the scores and picked the victim slot (the
+// lowest score among positions older than the R most recent, lower position on a tie); this
+// applies it.  One thread per (sequence, kv head).
+__global__ __launch_bounds__(64) void k_h2o_evict(const SeqDesc *__restrict__ seqs, int32_t *state, int Hkv,
+                                                  int n_pairs) {
+  const int i = blockIdx.x * 64 + (int)threadIdx.x;
+  if (i >= n_pairs) return;
+  const int seq = i / Hkv, h = i % Hkv;
   const SeqDesc &sd = seqs[seq];
   if (sd.method != H2O) return;
-  int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
+  int32_t *st = state + (size_t)i * ST_WORDS;
   const int count = st[ST_COUNT];
   if (count <= sd.B) return;
-  const int p = st[ST_NEXT_POS] - 1;
-  const int limit = p - sd.R + 1;
-  int32_t *pos = reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd);
-  const float *score = reinterpret_cast<const float *>(sd.score) + h * stride_slots(sd);
-  unsigned long long best = ~0ull;
-  for (int j = threadIdx.x; j < count; j += NT) {
-    const int pj = pos[j];
-    if (pj < limit) {
-      const unsigned long long key = ((unsigned long long)__builtin_bit_cast(uint32_t, score[j]) << 32) |
-                                     (unsigned long long)(uint32_t)pj;
-      best = key < best ? key : best;
-    }
-  }
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    const unsigned long long o = __shfl_xor(best, m);
-    best = o < best ? o : best;
-  }
-  if ((threadIdx.x & 63) == 0) s_best[threadIdx.x >> 6] = best;
-  __syncthreads();
-  best = s_best[0];
-  for (int w = 1; w < NT / 64; ++w) best = s_best[w] < best ? s_best[w] : best;
-  const int victim = (int)(uint32_t)(best & 0xFFFFFFFFu);
-  __syncthreads();
-  for (int j = threadIdx.x; j < count; j += NT) {
-    if (pos[j] == victim) {
-      pos[j] = -1;
-      st[ST_FREE_SLOT] = j;
-      st[ST_COUNT] = count - 1;
-    }
-  }
+  const int slot = st[ST_VICTIM];
+  if (slot < 0 || slot >= count) return;
+  gst(reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd) + slot, -1);
+  st[ST_FREE_SLOT] = slot;
+  st[ST_COUNT] = count - 1;
 }
 
 // ---- causal prefill attention statistics (shared by H2O scoring) ---------------------------------
@@ -584,7 +602,8 @@ hipError_t launch_topk(const Dev &dv, const Shape &sh, const uint16_t *q, int32_
 }
 
 hipError_t launch_h2o_evict(const Dev &dv, const Shape &sh, hipStream_t st) {
-  hipLaunchKernelGGL(k_h2o_evict, dim3(sh.S * sh.Hkv), dim3(NT), 0, st, dv.seqs, dv.state, sh.Hkv);
+  const int n_pairs = sh.S * sh.Hkv;
+  hipLaunchKernelGGL(k_h2o_evict, dim3((n_pairs + 63) / 64), dim3(64), 0, st, dv.seqs, dv.state, sh.Hkv, n_pairs);
   return hipGetLastError();
 }
 

@@ -28,8 +28,42 @@ MKV_DEV void unpack8(const uint4 &u, float *f) {
   f[6] = h2f(u.w); f[7] = h2f(u.w >> 16);
 }
 
+// Loads and stores through pointers known to be in global memory.  Region pointers come from
+// the descriptor table, so without the address-space cast the compiler emits flat accesses,
+// which share the LDS wait counter and serialise against LDS traffic.
+#define MKV_GLOBAL __attribute__((address_space(1)))
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
 template <typename T>
-MKV_DEV T ldg(const T *p) { return __builtin_nontemporal_load(p); }
+MKV_DEV T gld(const T *p) { return *(const MKV_GLOBAL T *)p; }
+template <typename T>
+MKV_DEV void gst(T *p, T v) { *(MKV_GLOBAL T *)p = v; }
+MKV_DEV uint4 gld16(const void *p) {
+  const u32x4 v = *(const MKV_GLOBAL u32x4 *)p;
+  // element subscripts, not .x/.y: with hipcc 7.2, __builtin_bit_cast of an ext_vector_type
+  // swizzle element (e.g. .y) has been seen to read element 0 instead
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+// 16 bytes as four scalars (the backend merges the four loads into one 16-byte load); loader
+// state holds plain scalars rather than vector types
+struct U4 {
+  uint32_t x, y, z, w;
+};
+MKV_DEV U4 gld16u(const void *p) {
+  const uint32_t *q = reinterpret_cast<const uint32_t *>(p);
+  return U4{gld(q), gld(q + 1), gld(q + 2), gld(q + 3)};
+}
+MKV_DEV void unpack8(const U4 &u, float *f) {
+  f[0] = h2f(u.x); f[1] = h2f(u.x >> 16);
+  f[2] = h2f(u.y); f[3] = h2f(u.y >> 16);
+  f[4] = h2f(u.z); f[5] = h2f(u.z >> 16);
+  f[6] = h2f(u.w); f[7] = h2f(u.w >> 16);
+}
+
+// 2^x on the hardware exponential unit (inputs here are <= 0; -inf gives 0)
+MKV_DEV float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // ---- DPP row reductions ---------------------------------------------------------------------
 template <int CTRL>
@@ -137,6 +171,47 @@ MKV_DEV void radix_select_kth(int n, int k, Get get, int *hist, int *shared3, ui
   }
   *kth = prefix;
   *n_equal = eq;
+  *need = remaining;
+}
+
+// Radix select as above with one histogram per wave (less atomic contention on popular digits)
+// and a parallel digit search.  `whist` is NT/64 x 256 ints, `s_tmp` NT/64 ints, `shared3` 3 ints.
+template <int NT, typename Get>
+MKV_DEV void radix_select_kth_waves(int n, int k, Get get, int (*whist)[256], int *shared3, int *s_tmp,
+                                    uint32_t *kth, int *n_equal, int *need) {
+  static_assert(NT == 256, "one thread per digit");
+  const int wid = threadIdx.x >> 6;
+  uint32_t prefix = 0, mask = 0;
+  int remaining = k;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    for (int w = 0; w < NT / 64; ++w) whist[w][threadIdx.x] = 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < n; i += NT) {
+      const uint32_t key = get(i);
+      if ((key & mask) == prefix) atomicAdd(&whist[wid][(key >> shift) & 255u], 1);
+    }
+    __syncthreads();
+    // thread b owns digit 255 - b, so the exclusive scan gives the count of larger digits
+    const int dgt = 255 - (int)threadIdx.x;
+    int cnt = 0;
+#pragma unroll
+    for (int w = 0; w < NT / 64; ++w) cnt += whist[w][dgt];
+    int tot;
+    const int above = block_exclusive_scan<NT>(cnt, s_tmp, &tot);
+    if (above < remaining && remaining <= above + cnt) {
+      shared3[0] = dgt;
+      shared3[1] = remaining - above;
+      shared3[2] = cnt;
+    }
+    __syncthreads();
+    prefix |= (uint32_t)shared3[0] << shift;
+    mask |= 255u << shift;
+    remaining = shared3[1];
+    *n_equal = shared3[2];
+    __syncthreads();
+  }
+  *kth = prefix;
   *need = remaining;
 }
 

@@ -46,6 +46,8 @@ struct Layout {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+constexpr int kMaxTiles = 32;  // per (sequence, kv head); the combine kernel holds up to 64
+
 int tile_tokens(const SeqDesc &s, int D) {
   // bytes each token costs the attention pass; tiles carry about 64 KiB
   double bpt;
@@ -215,6 +217,10 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
     const int amax = d.method == ROCKET ? d.topk : d.cap;
     d.chunk = tile_tokens(d, D);
     d.tile_count = std::max(1, (amax + d.chunk - 1) / d.chunk);
+    if (d.tile_count > kMaxTiles) {  // long sequences: fewer, larger tiles keep the combine short
+      d.chunk = (((amax + kMaxTiles - 1) / kMaxTiles) + 63) & ~63;
+      d.tile_count = (amax + d.chunk - 1) / d.chunk;
+    }
     d.tile_first = (int)L->tiles.size();
     for (int h = 0; h < Hkv; ++h)
       for (int t = 0; t < d.tile_count; ++t)

@@ -17,6 +17,7 @@ enum StateWord : int32_t {
   ST_KOUT_FILL = 3,  // KVQ: entries used in the key-outlier pool
   ST_SEL_COUNT = 4,  // ROCKET: tokens selected by the last top-k
   ST_KEPT = 5,       // tokens kept after prefill (H2O / ROCKET), prompt length otherwise
+  ST_VICTIM = 6,     // H2O: slot chosen for eviction by the last attention pass
   ST_WORDS = 8
 };
 
