@@ -73,12 +73,16 @@ def token_bytes(cfg, n0, step, D, G):
     return n * (D * b // 4 + 4 + 4 + 4 * nov + 4 * k_out)
 
 
-def launch_bytes(wl, step, n_tiles):
+def launch_bytes(wl, step, n_tiles, part="mx"):
+    """Algorithmic bytes of one launch of a partial kernel: "mx" (every method but uniform
+    4-bit) or "uq" (uniform 4-bit sequences); `n_tiles` is that kernel's workgroup count."""
     D, G, Hkv = wl.head_dim, wl.group, wl.n_kv_heads
     tot = 0.0
     for s in range(wl.n_seqs):
+        if (wl.cfg(s)["method"] == "uq") != (part == "uq"):
+            continue
         tot += Hkv * token_bytes(wl.cfg(s), wl.prompt_lens[s], step, D, G)
-    tot += wl.n_seqs * wl.n_q_heads * D * 2             # q
+        tot += wl.n_q_heads * D * 2                     # q
     tot += n_tiles * G * (D + 2) * 4                    # partial (m, l, o) writes
     return tot
 
@@ -157,15 +161,15 @@ def run_gpu(wl, steps, warmup, replicas=1, label=""):
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - a
     kinds = {}
-    for kind in ("partial", "combine", "append", "topk", "evict"):
+    for kind in ("partial", "partial_uq", "combine", "append", "topk", "evict"):
         n, ms = 0, 0.0
         for c in caches:
             a_n, a_ms = _lib.mkv_profile_read(c.h, kind)
             n += a_n
             ms += a_ms
         kinds[kind] = (n, ms)
-    n_tiles = caches[0].n_tiles()
-    bytes_steps = [launch_bytes(wl, warmup + i, n_tiles) for i in range(steps)]
+    n_tiles, n_uq = caches[0].n_tiles()
+    bytes_steps = [launch_bytes(wl, warmup + i, n_tiles - n_uq) for i in range(steps)]
     avg_bytes = float(np.mean(bytes_steps))
     n_part, ms_part = kinds["partial"]
     avg_part_ms = ms_part / max(n_part, 1)
@@ -174,7 +178,7 @@ def run_gpu(wl, steps, warmup, replicas=1, label=""):
         "partial_ms": avg_part_ms, "partial_bytes": avg_bytes,
         "partial_gbs": avg_bytes / (avg_part_ms * 1e-3) / 1e9,
         "step_gbs": avg_bytes / (elapsed / steps) / 1e9,
-        "n_tiles": n_tiles, "replicas": replicas,
+        "n_tiles": n_tiles, "n_tiles_uq": n_uq, "replicas": replicas,
         "kernel_ms": {k: (v[1] / max(v[0], 1)) for k, v in kinds.items() if v[0]},
     }
     for c in caches:
@@ -191,7 +195,7 @@ def per_config_runs(args):
              ("h2o", "H2O-20"), ("rocket", "Rocket-4096")]
     for name, cfg in cases:
         wl = make_workload(name, seed=args.seed, config_ids=cfg)
-        b1 = launch_bytes(wl, 0, 0)
+        b1 = launch_bytes(wl, 0, 0, "mx") + launch_bytes(wl, 0, 0, "uq")
         reps = max(1, math.ceil(2 * MALL_BYTES / b1))
         r = run_gpu(wl, args.cfg_steps, 2, replicas=reps, label=f"{name}/{cfg}")
         runs.append({"workload": name, "config": cfg, "steps_per_s": round(r["steps_per_s"], 1),

@@ -19,32 +19,46 @@ MKV_DEV int code_from_mid(float xhat, const float *mid, int nmid) {
   return c;
 }
 
-// Pack one code per thread (thread c = channel c, blockDim.x == D) into `row` with the layout
-// of `bits` (4: two per byte, low nibble first; 2: four per byte; 3: a 2-bit plane of D/4 bytes
-// followed by a 1-bit plane of D/8 bytes).  `s_code` is D bytes of LDS.
+// Outlier entry: fp16 value in bits 16..31, the (clamped) code in bits 8..11, channel in 0..7.
+MKV_DEV uint32_t outlier_entry(uint32_t bits16, int code, int ch) {
+  return ((bits16 & 0xFFFFu) << 16) | ((uint32_t)code << 8) | (uint32_t)ch;
+}
+
+// Word w of a packed code row: code i sits at bits [bits*i, bits*i + bits) of the row (bit 0 =
+// least significant bit of byte 0), so two consecutive codes form one 2*bits-bit field.
+MKV_DEV uint32_t packed_word(const uint8_t *codes, int n, int bits, int w) {
+  uint32_t word = 0;
+  const int lo = 32 * w;
+  const int first = max(0, lo / bits - 1), last = min(n, (lo + 32) / bits + 1);
+  for (int i = first; i < last; ++i) {
+    const int off = bits * i - lo;
+    const uint32_t code = codes[i];
+    if (off >= 0 && off < 32) word |= code << off;
+    else if (off < 0 && off > -bits) word |= code >> (-off);
+  }
+  return word;
+}
+
+// Pack one code per thread (thread c = channel c, blockDim.x == D) into a key row (see
+// packed_word).  `s_code` is D bytes of LDS.
 template <int D>
 MKV_DEV void pack_row(int code, int bits, uint8_t *s_code, uint8_t *row) {
   const int c = threadIdx.x;
   s_code[c] = (uint8_t)code;
   __syncthreads();
-  if (bits == 4) {
-    if (c < D / 2) row[c] = (uint8_t)(s_code[2 * c] | (s_code[2 * c + 1] << 4));
-  } else if (bits == 2) {
-    if (c < D / 4)
-      row[c] = (uint8_t)(s_code[4 * c] | (s_code[4 * c + 1] << 2) | (s_code[4 * c + 2] << 4) |
-                         (s_code[4 * c + 3] << 6));
-  } else {
-    if (c < D / 4)
-      row[c] = (uint8_t)((s_code[4 * c] & 3) | ((s_code[4 * c + 1] & 3) << 2) |
-                         ((s_code[4 * c + 2] & 3) << 4) | ((s_code[4 * c + 3] & 3) << 6));
-    if (c < D / 8) {
-      uint32_t b = 0;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) b |= (uint32_t)((s_code[8 * c + i] >> 2) & 1) << i;
-      row[D / 4 + c] = (uint8_t)b;
-    }
-  }
+  const int words = D * bits / 32;
+  if (c < words) gst(reinterpret_cast<uint32_t *>(row) + c, packed_word(s_code, D, bits, c));
   __syncthreads();
+}
+
+// Value codes are stored in blocks of 4 tokens: code (channel c, token j) at bit bits*(4c + j)
+// of the block, so the 4 tokens of a channel form two 2*bits-bit fields.  OR one code per thread
+// into the LDS copy `s_blk` of a block.
+MKV_DEV void or_quad_code(uint32_t *s_blk, int c, int j, int code, int bits) {
+  const int bit = bits * (4 * c + j);
+  atomicOr(&s_blk[bit >> 5], (uint32_t)code << (bit & 31));
+  const int spill = (bit & 31) + bits - 32;
+  if (spill > 0) atomicOr(&s_blk[(bit >> 5) + 1], (uint32_t)code >> (bits - spill));
 }
 
 // Inclusive rank among flagged threads of the block (blockDim.x == D <= 128) and the total.
@@ -65,10 +79,11 @@ MKV_DEV int flag_rank(bool f, int *s_tmp, int *total) {
   return base + before;
 }
 
-// KVQ value row of one token: per-token scale = n_ov-th largest |v| (0-based), codes, outliers.
+// KVQ value of one token: per-token scale = n_ov-th largest |v| (0-based), outliers (written),
+// and this thread's code (returned; the caller places it in the token's 4-token block).
 template <int D>
-MKV_DEV void kvq_value_token(const SeqDesc &sd, int h, int t, uint32_t vbits, const float *cbtab,
-                             float *s_abs, float *s_scale, uint8_t *s_code, int *s_tmp) {
+MKV_DEV int kvq_value_token(const SeqDesc &sd, int h, int t, uint32_t vbits, const float *cbtab,
+                            float *s_abs, float *s_scale, int *s_tmp) {
   const int c = threadIdx.x;
   const float x = h2f(vbits);
   const float ax = fabsf(x);
@@ -90,14 +105,21 @@ MKV_DEV void kvq_value_token(const SeqDesc &sd, int h, int t, uint32_t vbits, co
   const float *mid = cbtab + cb_offset(sd.bits) + 2 * nc + (nc - 1);
   const int code = code_from_mid(xhat, mid, nc - 1);
   const bool outl = sd.bp > 0 && ax > s;
-  uint8_t *row = reinterpret_cast<uint8_t *>(sd.vc) + h * stride_codes(sd) + (size_t)t * sd.rowbytes;
-  pack_row<D>(code, sd.bits, s_code, row);
   int total;
   const int r = flag_rank<D>(outl, s_tmp, &total);
   uint32_t *vo = reinterpret_cast<uint32_t *>(sd.vout) + h * stride_vout(sd) + (size_t)t * sd.nov_slots;
-  if (outl && r < sd.nov_slots) vo[r] = ((vbits & 0xFFFFu) << 16) | (uint32_t)c;
+  if (outl && r < sd.nov_slots) vo[r] = outlier_entry(vbits, code, c);
   if (c >= total && c < sd.nov_slots) vo[c] = kNoOutlier;
   if (c == 0) (reinterpret_cast<float *>(sd.vmeta) + h * stride_slots(sd))[t] = s;
+  return code;
+}
+
+// Write the value codes of tokens t0..t0+3 (one 4-token block) from an LDS block image.
+MKV_DEV void store_quad(const SeqDesc &sd, int h, int t0, const uint32_t *s_blk, int D) {
+  const int words = D * sd.bits / 8;  // 4 tokens x D codes x bits / 32
+  uint32_t *dst = reinterpret_cast<uint32_t *>(reinterpret_cast<uint8_t *>(sd.vc) + h * stride_codes(sd) +
+                                               (size_t)(t0 / 4) * 4 * sd.rowbytes);
+  for (int w = threadIdx.x; w < words; w += blockDim.x) gst(dst + w, s_blk[w]);
 }
 
 // KVQ key of one token: code under the frozen per-channel threshold, and the outlier flag.
@@ -164,6 +186,7 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
   __shared__ float s_scale;
   __shared__ uint8_t s_code[D];
   __shared__ int s_tmp[4];
+  __shared__ uint32_t s_blk[D / 2];
   const int seq = blockIdx.x / Hkv, h = blockIdx.x % Hkv, c = threadIdx.x;
   const SeqDesc &sd = seqs[seq];
   int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
@@ -194,7 +217,7 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
     case ROCKET: {
       (reinterpret_cast<uint16_t *>(sd.k) + h * stride_rows(sd, D))[(size_t)count * D + c] = (uint16_t)kb;
       (reinterpret_cast<uint16_t *>(sd.v) + h * stride_rows(sd, D))[(size_t)count * D + c] = (uint16_t)vb;
-      (reinterpret_cast<uint16_t *>(sd.kcm) + h * stride_rows(sd, D))[(size_t)c * sd.cap + count] = (uint16_t)kb;
+      (reinterpret_cast<uint16_t *>(sd.kcm) + h * stride_kcm(sd, D))[(size_t)c * sd.cstride + count] = (uint16_t)kb;
       if (c == 0) {
         (reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd))[count] = pos;
         st[ST_COUNT] = count + 1;
@@ -222,8 +245,18 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
       const int r = flag_rank<D>(outl, s_tmp, &total);
       const int fill = st[ST_KOUT_FILL];
       uint32_t *ko = reinterpret_cast<uint32_t *>(sd.kout) + h * stride_kout(sd);
-      if (outl) ko[fill + r] = ((kb & 0xFFFFu) << 16) | (uint32_t)c;
-      kvq_value_token<D>(sd, h, count, vb, cbtab, s_abs, &s_scale, s_code, s_tmp);
+      if (outl) ko[fill + r] = outlier_entry(kb, code, c);
+      const int vcode = kvq_value_token<D>(sd, h, count, vb, cbtab, s_abs, &s_scale, s_tmp);
+      // the value code goes into its 4-token block: start from zero for the block's first token,
+      // otherwise from the stored block
+      const int j = count & 3, words = D * sd.bits / 8;
+      const uint32_t *blk = reinterpret_cast<const uint32_t *>(reinterpret_cast<const uint8_t *>(sd.vc) +
+                                                               h * stride_codes(sd) + (size_t)(count / 4) * 4 * sd.rowbytes);
+      for (int w = c; w < words; w += D) s_blk[w] = j == 0 ? 0u : gld(blk + w);
+      __syncthreads();
+      or_quad_code(s_blk, c, j, vcode, sd.bits);
+      __syncthreads();
+      store_quad(sd, h, count & ~3, s_blk, D);
       __syncthreads();
       if (c == 0) {
         (reinterpret_cast<uint32_t *>(sd.krow) + h * stride_krow(sd))[count + 1] = (uint32_t)(fill + total);
@@ -335,8 +368,7 @@ __global__ __launch_bounds__(128) void k_kvq_keys(const SeqDesc *__restrict__ se
   } else {
     int total;
     const int r = flag_rank<D>(outl, s_tmp, &total);
-    if (outl) (reinterpret_cast<uint32_t *>(sd.kout) + h * stride_kout(sd))[krow[t] + r] =
-        ((kb & 0xFFFFu) << 16) | (uint32_t)c;
+    if (outl) (reinterpret_cast<uint32_t *>(sd.kout) + h * stride_kout(sd))[krow[t] + r] = outlier_entry(kb, code, c);
   }
 }
 
@@ -362,17 +394,28 @@ __global__ __launch_bounds__(256) void k_kvq_scan(const SeqDesc *__restrict__ se
   }
 }
 
+// KVQ prompt values: one workgroup per (4-token block, kv head) quantizes the block's tokens and
+// writes the block.
 template <int D>
 __global__ __launch_bounds__(128) void k_prefill_kvq_values(const SeqDesc *__restrict__ seqs, int seq,
                                                            const uint16_t *__restrict__ v,
-                                                           const float *__restrict__ cbtab, int Hkv) {
+                                                           const float *__restrict__ cbtab, int Hkv, int n0) {
   __shared__ float s_abs[D];
   __shared__ float s_scale;
-  __shared__ uint8_t s_code[D];
   __shared__ int s_tmp[4];
+  __shared__ uint32_t s_blk[D / 2];
   const SeqDesc &sd = seqs[seq];
-  const int t = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
-  kvq_value_token<D>(sd, h, t, v[((size_t)t * Hkv + h) * D + c], cbtab, s_abs, &s_scale, s_code, s_tmp);
+  const int q = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
+  const int words = D * sd.bits / 8;
+  for (int w = c; w < words; w += D) s_blk[w] = 0;
+  __syncthreads();
+  for (int j = 0; j < 4 && 4 * q + j < n0; ++j) {
+    const int t = 4 * q + j;
+    const int code = kvq_value_token<D>(sd, h, t, v[((size_t)t * Hkv + h) * D + c], cbtab, s_abs, &s_scale, s_tmp);
+    or_quad_code(s_blk, c, j, code, sd.bits);
+  }
+  __syncthreads();
+  store_quad(sd, h, 4 * q, s_blk, D);
 }
 
 __global__ void k_prefill_state(const SeqDesc *__restrict__ seqs, int seq, int32_t *state, int Hkv) {
@@ -427,7 +470,8 @@ hipError_t prefill_impl(const Dev &dv, const Shape &sh, const SeqDesc &hs, int s
       hipLaunchKernelGGL(k_kvq_keys<D>, dim3(n0, Hkv), dim3(D), 0, st, dv.seqs, seq, k, dv.cbtab, Hkv, 0);
       hipLaunchKernelGGL(k_kvq_scan, dim3(Hkv), dim3(256), 0, st, dv.seqs, seq, dv.state, Hkv, n0);
       hipLaunchKernelGGL(k_kvq_keys<D>, dim3(n0, Hkv), dim3(D), 0, st, dv.seqs, seq, k, dv.cbtab, Hkv, 1);
-      hipLaunchKernelGGL(k_prefill_kvq_values<D>, dim3(n0, Hkv), dim3(D), 0, st, dv.seqs, seq, v, dv.cbtab, Hkv);
+      hipLaunchKernelGGL(k_prefill_kvq_values<D>, dim3((n0 + 3) / 4, Hkv), dim3(D), 0, st, dv.seqs, seq, v, dv.cbtab,
+                         Hkv, n0);
       break;
     default:
       return hipErrorInvalidValue;

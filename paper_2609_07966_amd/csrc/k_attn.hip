@@ -3,16 +3,25 @@
 // Every configuration's decode step ends in softmax attention over the tokens its cache keeps
 // (MetaKV Section 2.1): all tokens with dequantized values (uniform / KVQuant), the retained
 // set (H2O) or the selected set (RocketKV).  One launch covers all sequences: each workgroup
-// takes one tile = (sequence, kv head, token range) and runs the loop for that sequence's
-// method.
+// takes one tile = (sequence, kv head, token range) and runs the loop for that sequence's method;
+// the 4 waves of a workgroup split the tile's tokens into contiguous ranges.
 //
-// Tile work: 4 waves split the tile's tokens into contiguous ranges.  Within a wave, D/8 lanes
-// share a token (8 channels each: one 16-byte fp16 load per row, or the matching packed-code
-// bytes), so one wave load reads whole rows of 64/(D/8) consecutive tokens.  Each lane group
-// issues the loads of U tokens before computing any of them (32 tokens per wave in flight), then
-// reduces q . k over the group with DPP row ops, updates the wave-uniform running maximum once
-// per batch, and accumulates p . v in registers.  Logits use the base-2 exponent (scaled by
-// log2(e) / sqrt(d) after the reduction).
+// Matrix path (fp16 rows, gathered rows, KVQuant): a wave handles 16 tokens per step with
+// v_mfma_f32_16x16x16_f16.  q.k is S^T = K Q^T (tokens x query heads; channels permuted so a
+// lane reads 32 contiguous channels of one token), and its result layout is exactly the operand
+// layout of P^T in O^T = V^T P^T (channels x query heads), so probabilities feed the second
+// product without moving.  KVQuant codes are turned into packed fp16 pairs by one LDS table
+// lookup per two codes; its key thresholds are folded into q and its value scales into p, and
+// outliers are applied as sparse corrections.  fp16 operands would cost KVQuant about 1e-3 of
+// the value RMS (codebook entries are not fp16 values), so codebook entries, q and p are split
+// into high and low fp16 parts: the low part of q or p rides in spare columns G..2G-1 of the
+// same product, and the low part of the codebook takes a second product.
+//
+// Vector path (uniform 4-bit): D/8 lanes share a token (8 channels each) and reduce q.k with DPP
+// row ops; per-block key scales are folded into q once per 64-token block.
+//
+// Logits use the base-2 exponent (scaled by log2(e)/sqrt(d) after the dot product); each lane
+// group issues the loads of 32 tokens per wave before computing any of them.
 #include "kernels_common.h"
 
 namespace mkv {
@@ -20,11 +29,313 @@ namespace mkv {
 namespace {
 
 typedef _Float16 h2v __attribute__((ext_vector_type(2)));
+typedef _Float16 h4v __attribute__((ext_vector_type(4)));
+typedef float f4v __attribute__((ext_vector_type(4)));
 
 MKV_DEV float dot2(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2(__builtin_bit_cast(h2v, a), __builtin_bit_cast(h2v, b), c, false);
 }
 
+MKV_DEV h4v mk_h4(uint32_t lo, uint32_t hi) {
+  return __builtin_bit_cast(h4v, ((uint64_t)hi << 32) | (uint64_t)lo);
+}
+MKV_DEV f4v mfma16(h4v a, h4v b, f4v c) { return __builtin_amdgcn_mfma_f32_16x16x16f16(a, b, c, 0, 0, 0); }
+// low halves of a and b packed (a in bits 0..15), and the high halves
+MKV_DEV uint32_t pk_lo(uint32_t a, uint32_t b) { return __builtin_amdgcn_perm(b, a, 0x05040100u); }
+MKV_DEV uint32_t pk_hi(uint32_t a, uint32_t b) { return __builtin_amdgcn_perm(b, a, 0x07060302u); }
+MKV_DEV uint32_t f16bits(float x) { return (uint32_t)__builtin_bit_cast(unsigned short, (_Float16)x); }
+MKV_DEV uint32_t pk_f16(float lo, float hi) { return f16bits(lo) | (f16bits(hi) << 16); }
+
+// ================================================================================================
+// Matrix path
+// ================================================================================================
+// Lane roles (lr = lane % 16, lq = lane / 16):
+//   q.k operand A  token row lr, channels CPL*lq + 4m + j (m = MFMA index, j = element)
+//   q.k operand B  query head lr, same channels
+//   S              token rows 4*lq + j, query head lr
+//   p.v operand A  channel VPL*lr + m, tokens 4*lq + j
+//   O^T            channel VPL*(4*lq + i) + m, query head lr
+template <int D>
+struct MG {
+  static constexpr int NM = D / 16;   // MFMAs per 16-token step, for q.k and for p.v
+  static constexpr int CPL = D / 4;   // key channels per lane
+  static constexpr int VPL = D / 16;  // value channels per lane
+  static constexpr int NS = 2;        // 16-token steps per batch
+};
+
+// q.k operand B per MFMA.  fp16 rows: hi = q in columns 0..G-1.  KVQuant (q' = q tau):
+// hi = high part of q' in columns 0..G-1 and its low part in G..2G-1; lo = high part only,
+// multiplied by the low part of the codebook.
+template <int D>
+struct QB {
+  h4v hi[MG<D>::NM];
+  h4v lo[MG<D>::NM];
+};
+
+// fp16 rows.  Gather: token t of the tile is the t-th selected slot (RocketKV).
+template <int D, int G, bool GATHER>
+struct MRows {
+  static constexpr int NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
+  static constexpr bool kSplitQ = false, kQuant = false;
+  const uint16_t *K, *V;
+  const int32_t *sel;
+  int lr, lq;
+  struct Raw {
+    uint32_t kw[CPL / 2];
+    uint32_t vw[4][VPL / 2];
+    int ks, vs[4];
+  };
+  MKV_DEV int slot_of(int t) const { return GATHER ? gld(sel + t) : t; }
+  MKV_DEV void load_rows(Raw &r) const {
+    const uint32_t *kp = reinterpret_cast<const uint32_t *>(K + (size_t)r.ks * D + CPL * lq);
+#pragma unroll
+    for (int i = 0; i < CPL / 2; ++i) r.kw[i] = gld(kp + i);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t *vp = reinterpret_cast<const uint32_t *>(V + (size_t)r.vs[j] * D + VPL * lr);
+#pragma unroll
+      for (int i = 0; i < VPL / 2; ++i) r.vw[j][i] = gld(vp + i);
+    }
+  }
+  MKV_DEV void fetch(int base, int b, Raw &r) const {
+    r.ks = slot_of(min(base + lr, b - 1));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r.vs[j] = slot_of(min(base + 4 * lq + j, b - 1));
+    if (!GATHER) load_rows(r);
+  }
+  MKV_DEV void fetch2(Raw &r) const {
+    if (GATHER) load_rows(r);
+  }
+  MKV_DEV int slot(const Raw &r, int j) const { return r.vs[j]; }
+  MKV_DEV void qk(const Raw &r, const QB<D> &qb, f4v &S) const {
+#pragma unroll
+    for (int m = 0; m < NM; ++m) S = mfma16(mk_h4(r.kw[2 * m], r.kw[2 * m + 1]), qb.hi[m], S);
+  }
+  MKV_DEV void kfix(const Raw &, float (&)[4]) const {}
+  MKV_DEV void combine(float (&)[4]) const {}
+  MKV_DEV float vscale(const Raw &, int) const { return 1.f; }
+  MKV_DEV void vfix(const Raw &, const float (&)[4], const float (&)[4], int) const {}
+  MKV_DEV void rescale_fix(float) const {}
+  MKV_DEV void pv(const Raw &r, const float (&pp)[4], f4v (&O)[NM]) const {
+    const h4v P = mk_h4(pk_f16(pp[0], pp[1]), pk_f16(pp[2], pp[3]));
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      const int w = m / 2;
+      const uint32_t x01 = (m & 1) ? pk_hi(r.vw[0][w], r.vw[1][w]) : pk_lo(r.vw[0][w], r.vw[1][w]);
+      const uint32_t x23 = (m & 1) ? pk_hi(r.vw[2][w], r.vw[3][w]) : pk_lo(r.vw[2][w], r.vw[3][w]);
+      O[m] = mfma16(mk_h4(x01, x23), P, O[m]);
+    }
+  }
+};
+
+// KVQuant-style b-bit codes.  Key codes: code c of a row at bit b*c, so channels (2p, 2p+1)
+// form a 2b-bit field p.  Value codes: 4-token blocks with code (channel c, token j) at bit
+// b*(4c + j), so the tokens (0,1) and (2,3) of a channel form two 2b-bit fields.  A field
+// indexes a table of two packed fp16 pairs: high parts (cb[low code], cb[high code]) and the
+// low parts cb - high.
+template <int D, int G, int BITS>
+struct MKVQ {
+  static constexpr int NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
+  static constexpr bool kSplitQ = true, kQuant = true;
+  static constexpr int SEG = CPL * BITS;  // bits per lane segment (keys; values alike)
+  // words per segment: a segment starts at bit SEG * lane_index, which is word aligned unless
+  // SEG = 48 (d = 64, 3 bits), where it starts at bit 0 or 16 of a word and still spans 2 words
+  static constexpr int NW = (SEG + 31) / 32;
+  static constexpr int FMASK = (1 << (2 * BITS)) - 1;
+  const uint8_t *kc, *vc;
+  const uint32_t *krow, *kout, *vout;
+  const float *vsc;
+  const uint2 *lutk, *lutv;       // LDS pair tables
+  const float *cbk, *cbv;         // LDS codebooks
+  const float *q32, *qp32;        // LDS [G][D]: q and q * tau
+  float *vcorr;                   // LDS [G][D]: this wave's value-outlier corrections
+  int lr, lq, rowbytes, nov;
+  int prole;                      // p operand: 0 high part, 1 low part, 2 none (columns >= 2G)
+  struct Raw {
+    uint32_t kw[NW], vw[NW];
+    float sv[4];
+    uint32_t ka[4], kb[4], e0[4], vo[4];
+    int t[4];
+  };
+  // load a segment and shift it to start at bit 0 of w[0]
+  MKV_DEV void seg(const uint8_t *base, int bitoff, uint32_t (&w)[NW]) const {
+    const uint32_t *p = reinterpret_cast<const uint32_t *>(base) + (bitoff >> 5);
+#pragma unroll
+    for (int i = 0; i < NW; ++i) w[i] = gld(p + i);
+    if (SEG % 32 != 0) {
+      const int sh = bitoff & 31;
+      w[0] = __builtin_amdgcn_alignbit(w[1], w[0], sh);
+      w[1] >>= sh;
+    }
+  }
+  // the 2b-bit field f of a segment (compile-time position once unrolled)
+  MKV_DEV uint32_t field(const uint32_t (&w)[NW], int f) const {
+    const int bit = 2 * BITS * f, i = bit >> 5, s = bit & 31;
+    if (s + 2 * BITS <= 32) return (w[i] >> s) & FMASK;
+    return __builtin_amdgcn_alignbit(w[i + 1], w[i], s) & FMASK;
+  }
+  MKV_DEV void fetch(int base, int b, Raw &r) const {
+    const int tk = min(base + lr, b - 1);
+    seg(kc + (size_t)tk * rowbytes, SEG * lq, r.kw);
+    // this lane's 4 tokens form one 4-token block (tile and wave ranges start at multiples of
+    // 32); past the end, the last block is re-read, whose slots all lie below the slot capacity
+    // (a multiple of 4)
+    const int t0 = min(base + 4 * lq, (b - 1) & ~3);
+    seg(vc + (size_t)t0 * rowbytes, SEG * lr, r.vw);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      r.t[j] = t0 + j;
+      r.sv[j] = gld(vsc + t0 + j);
+      r.ka[j] = gld(krow + t0 + j);
+      r.vo[j] = gld(vout + (size_t)(t0 + j) * nov);
+    }
+    uint32_t end = gld(krow + t0 + 4);
+    // slots at or past the count have no outlier range (their CSR words are not written)
+#pragma unroll
+    for (int j = 3; j >= 0; --j) {
+      const bool in = t0 + j < b;
+      r.kb[j] = in ? end : 0u;
+      end = r.ka[j];
+      r.ka[j] = in ? r.ka[j] : 0u;
+    }
+  }
+  MKV_DEV void fetch2(Raw &r) const {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r.e0[j] = r.ka[j] < r.kb[j] ? gld(kout + r.ka[j]) : kNoOutlier;
+  }
+  MKV_DEV int slot(const Raw &r, int j) const { return r.t[j]; }
+  MKV_DEV void qk(const Raw &r, const QB<D> &qb, f4v &S) const {
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      const uint2 e0 = lutk[field(r.kw, 2 * m)], e1 = lutk[field(r.kw, 2 * m + 1)];
+      S = mfma16(mk_h4(e0.x, e1.x), qb.hi[m], S);
+      S = mfma16(mk_h4(e0.y, e1.y), qb.lo[m], S);
+    }
+  }
+  // column g + G holds the low part of head g's logit
+  MKV_DEV void combine(float (&x)[4]) const {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) x[j] += __shfl_xor(x[j], G);
+  }
+  // key outliers replace their channel: add q x - q' cb16[code] to the raw logit
+  MKV_DEV void kfix_one(uint32_t ent, float &s) const {
+    const int ch = (int)(ent & 0xFFu), code = (int)((ent >> 8) & 15u);
+    s += q32[lr * D + ch] * h2f(ent >> 16) - qp32[lr * D + ch] * cbk[code];
+  }
+  MKV_DEV void kfix(const Raw &r, float (&s)[4]) const {
+    if (lr >= G) return;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (r.e0[j] == kNoOutlier) continue;
+      kfix_one(r.e0[j], s[j]);
+      for (uint32_t e = r.ka[j] + 1; e < r.kb[j]; ++e) kfix_one(gld(kout + e), s[j]);
+    }
+  }
+  MKV_DEV float vscale(const Raw &r, int j) const { return r.sv[j]; }
+  // value outliers replace their channel: p x - p' cb16[code] accumulates in LDS per channel
+  MKV_DEV void vfix(const Raw &r, const float (&p)[4], const float (&pp)[4], int valid_mask) const {
+    if (lr >= G) return;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (!((valid_mask >> j) & 1)) continue;
+      for (int i = 0; i < nov; ++i) {
+        const uint32_t ent = i == 0 ? r.vo[j] : gld(vout + (size_t)r.t[j] * nov + i);
+        if (ent == kNoOutlier) break;
+        const int ch = (int)(ent & 0xFFu), code = (int)((ent >> 8) & 15u);
+        atomicAdd(&vcorr[lr * D + ch], p[j] * h2f(ent >> 16) - pp[j] * cbv[code]);
+      }
+    }
+  }
+  MKV_DEV void rescale_fix(float corr) const {
+    if (lr >= G || corr == 1.f) return;
+    for (int c = lq * (D / 4); c < (lq + 1) * (D / 4); ++c) vcorr[lr * D + c] *= corr;
+  }
+  MKV_DEV void pv(const Raw &r, const float (&pp)[4], f4v (&O)[NM]) const {
+    uint32_t w1[2], w2[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const float a = pp[2 * i], b = pp[2 * i + 1];
+      const float ah = (float)(_Float16)a, bh = (float)(_Float16)b;
+      w1[i] = prole == 0 ? pk_f16(ah, bh) : prole == 1 ? pk_f16(a - ah, b - bh) : 0u;
+      w2[i] = prole == 0 ? pk_f16(ah, bh) : 0u;
+    }
+    const h4v P1 = mk_h4(w1[0], w1[1]), P2 = mk_h4(w2[0], w2[1]);
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      const uint2 e0 = lutv[field(r.vw, 2 * m)], e1 = lutv[field(r.vw, 2 * m + 1)];
+      O[m] = mfma16(mk_h4(e0.x, e1.x), P1, O[m]);
+      O[m] = mfma16(mk_h4(e0.y, e1.y), P2, O[m]);
+    }
+  }
+};
+
+// One wave over tokens [a, b) of its tile, 32 tokens per batch.  m_run / l_part belong to this
+// lane's query head (lr); O holds this lane's part of O^T.
+template <int D, int G, class L>
+MKV_DEV void wave_mfma(L &ld, int a, int b, const QB<D> &qb, float qscale, float &m_run, float &l_part,
+                       f4v (&O)[MG<D>::NM], float *logit_out) {
+  constexpr int NS = MG<D>::NS;
+  const int lane = threadIdx.x & 63, lr = lane & 15, lq = lane >> 4;
+  for (int base = a; base < b; base += 16 * NS) {
+    typename L::Raw raw[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) ld.fetch(base + 16 * s, b, raw[s]);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) ld.fetch2(raw[s]);
+    float sc[NS][4];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      f4v S = {0.f, 0.f, 0.f, 0.f};
+      ld.qk(raw[s], qb, S);
+      float x[4] = {S[0], S[1], S[2], S[3]};
+      ld.kfix(raw[s], x);
+      ld.combine(x);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bool valid = base + 16 * s + 4 * lq + j < b;
+        sc[s][j] = valid ? x[j] * qscale : -INFINITY;
+        mx = fmaxf(mx, sc[s][j]);
+      }
+    }
+    if (logit_out != nullptr && lr < G) {
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (sc[s][j] != -INFINITY) gst(logit_out + (size_t)ld.slot(raw[s], j) * G + lr, sc[s][j]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    if (mx > m_run) {
+      const float corr = fexp2(m_run - mx);
+      l_part *= corr;
+#pragma unroll
+      for (int m = 0; m < MG<D>::NM; ++m) O[m] *= corr;
+      ld.rescale_fix(corr);
+      m_run = mx;
+    }
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      float p[4], pp[4];
+      int valid_mask = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        p[j] = sc[s][j] == -INFINITY ? 0.f : fexp2(sc[s][j] - m_run);
+        valid_mask |= (sc[s][j] != -INFINITY) << j;
+        l_part += p[j];
+        // slots past the count may hold any bits: their scale must not reach the product
+        pp[j] = sc[s][j] == -INFINITY ? 0.f : p[j] * ld.vscale(raw[s], j);
+      }
+      ld.vfix(raw[s], p, pp, valid_mask);
+      ld.pv(raw[s], pp, O);
+    }
+  }
+}
+
+// ================================================================================================
+// Vector path (uniform 4-bit)
+// ================================================================================================
 template <int D, int G>
 struct Geo {
   static constexpr int LPT = D / 8;      // lanes per token
@@ -37,72 +348,6 @@ template <int G>
 struct Qs {
   uint32_t h[G][4];  // fp16 pairs of channels c0..c0+7, unscaled
   float f[G][8];     // the same in fp32
-};
-
-MKV_DEV U4 ld16(const void *p) { return gld16u(p); }
-
-// ---- per-method loaders ------------------------------------------------------------------------
-// fetch(t, raw): the loads of token t that depend only on t;  fetch2(raw): loads that depend on
-// fetch's results;  dot(raw, q, part): this lane's partial q . k for every head (unscaled);
-// pv(raw, p, o): o += p * v for this lane's 8 channels.
-
-template <int D, int G>
-struct LdRows {  // fp16 rows, token t = slot t (FP16, H2O)
-  const uint16_t *K, *V;
-  int c0;
-  struct Raw { U4 k, v; };
-  MKV_DEV void prep(int, const Qs<G> &) {}
-  MKV_DEV void rescale(int, float) {}
-  MKV_DEV void finish(float (&)[G][8]) const {}
-  MKV_DEV int slot(const Raw &, int t) const { return t; }
-  MKV_DEV void fetch(int t, Raw &r) const {
-    r.k = ld16(K + (size_t)t * D + c0);
-    r.v = ld16(V + (size_t)t * D + c0);
-  }
-  MKV_DEV void fetch2(Raw &) const {}
-  MKV_DEV void dot(const Raw &r, const Qs<G> &q, float (&part)[G]) const {
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-      part[g] = dot2(q.h[g][3], r.k.w, dot2(q.h[g][2], r.k.z, dot2(q.h[g][1], r.k.y, dot2(q.h[g][0], r.k.x, 0.f))));
-  }
-  MKV_DEV void pv(const Raw &r, const float (&p)[G], float (&o)[G][8]) const {
-    float vf[8];
-    unpack8(r.v, vf);
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o[g][i] = fmaf(p[g], vf[i], o[g][i]);
-  }
-};
-
-template <int D, int G>
-struct LdGather {  // RocketKV: token t of the tile is the t-th selected slot
-  const uint16_t *K, *V;
-  const int32_t *sel;
-  int c0;
-  struct Raw { U4 k, v; int s; };
-  MKV_DEV void prep(int, const Qs<G> &) {}
-  MKV_DEV void rescale(int, float) {}
-  MKV_DEV void finish(float (&)[G][8]) const {}
-  MKV_DEV int slot(const Raw &r, int) const { return r.s; }
-  MKV_DEV void fetch(int t, Raw &r) const { r.s = gld(sel + t); }
-  MKV_DEV void fetch2(Raw &r) const {
-    r.k = ld16(K + (size_t)r.s * D + c0);
-    r.v = ld16(V + (size_t)r.s * D + c0);
-  }
-  MKV_DEV void dot(const Raw &r, const Qs<G> &q, float (&part)[G]) const {
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-      part[g] = dot2(q.h[g][3], r.k.w, dot2(q.h[g][2], r.k.z, dot2(q.h[g][1], r.k.y, dot2(q.h[g][0], r.k.x, 0.f))));
-  }
-  MKV_DEV void pv(const Raw &r, const float (&p)[G], float (&o)[G][8]) const {
-    float vf[8];
-    unpack8(r.v, vf);
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o[g][i] = fmaf(p[g], vf[i], o[g][i]);
-  }
 };
 
 // Uniform 4-bit: k = mn_c + code * st_c per (64-token block, channel), so q . k = sum q mn +
@@ -143,7 +388,6 @@ struct LdUQ {
       }
     }
   }
-  MKV_DEV int slot(const Raw &, int t) const { return t; }
   MKV_DEV void fetch(int t, Raw &r) const {
     r.quant = t < full;
     r.kw = 0;
@@ -162,7 +406,6 @@ struct LdUQ {
     r.vmn = gld(mp);
     r.vst = gld(mp + 1);
   }
-  MKV_DEV void fetch2(Raw &) const {}
   MKV_DEV void dot(const Raw &r, const Qs<G> &q, float (&part)[G]) const {
     if (r.quant) {
       float cf[8];
@@ -195,95 +438,10 @@ struct LdUQ {
   }
 };
 
-// KVQuant-style: codebooks in LDS; the per-channel key threshold is folded into q (q' = q tau),
-// so a non-outlier key contributes q' cb[code]; outliers replace their channel's value.  The
-// per-token value scale multiplies the dequantized row.
-template <int D, int G, int BITS>
-struct LdKVQ {
-  static constexpr int bits = BITS;
-  const uint8_t *kc, *vc;
-  const uint32_t *krow, *kout, *vout;
-  const float *vs;
-  const float *cbk, *cbv;   // LDS
-  const float *qlds;        // LDS [G][D]: unscaled q, for outlier corrections
-  int c0, rowbytes, nov;
-  float qp[G][8];
-  struct Raw { uint32_t kw, vw; float sv; uint32_t ka, kb, e0, e1, vo; int t; };
-  MKV_DEV void prep(int, const Qs<G> &) {}
-  MKV_DEV void rescale(int, float) {}
-  MKV_DEV void finish(float (&)[G][8]) const {}
-  MKV_DEV int slot(const Raw &, int t) const { return t; }
-  MKV_DEV uint32_t codes_word(const uint8_t *row) const {
-    if (bits == 4) return gld(reinterpret_cast<const uint32_t *>(row + c0 / 2));
-    if (bits == 2) return gld(reinterpret_cast<const uint16_t *>(row + c0 / 4));
-    return (uint32_t)gld(reinterpret_cast<const uint16_t *>(row + c0 / 4)) | ((uint32_t)gld(row + D / 4 + c0 / 8) << 16);
-  }
-  MKV_DEV int code_at(uint32_t w, int i) const {
-    if (bits == 4) return (w >> (4 * i)) & 15u;
-    if (bits == 2) return (w >> (2 * i)) & 3u;
-    return ((w >> (2 * i)) & 3u) | (((w >> (16 + i)) & 1u) << 2);
-  }
-  MKV_DEV void fetch(int t, Raw &r) const {
-    r.kw = codes_word(kc + (size_t)t * rowbytes);
-    r.vw = codes_word(vc + (size_t)t * rowbytes);
-    r.sv = gld(vs + t);
-    r.ka = gld(krow + t);
-    r.kb = gld(krow + t + 1);
-    r.vo = gld(vout + (size_t)t * nov);
-    r.t = t;
-  }
-  MKV_DEV void fetch2(Raw &r) const {
-    r.e0 = r.ka < r.kb ? gld(kout + r.ka) : kNoOutlier;
-    r.e1 = r.ka + 1 < r.kb ? gld(kout + r.ka + 1) : kNoOutlier;
-  }
-  // correction of one key outlier entry: q . (x - tau cb[code]) on its channel
-  MKV_DEV void k_fix(uint32_t ent, uint32_t kw, float (&part)[G]) const {
-    const int ch = (int)(ent & 0xFFu);
-    if (ch < c0 || ch >= c0 + 8) return;
-    const float x = h2f(ent >> 16);
-    const float cb = cbk[code_at(kw, ch - c0)];
-#pragma unroll
-    for (int g = 0; g < G; ++g) part[g] += qlds[g * D + ch] * x - qlds[G * D + g * D + ch] * cb;
-  }
-  MKV_DEV void dot(const Raw &r, const Qs<G> &, float (&part)[G]) const {
-    float kf[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) kf[i] = cbk[code_at(r.kw, i)];
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      float acc = 0.f;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) acc = fmaf(qp[g][i], kf[i], acc);
-      part[g] = acc;
-    }
-    if (r.e0 != kNoOutlier) k_fix(r.e0, r.kw, part);
-    if (r.e1 != kNoOutlier) k_fix(r.e1, r.kw, part);
-    for (uint32_t e = r.ka + 2; e < r.kb; ++e) k_fix(gld(kout + e), r.kw, part);
-  }
-  MKV_DEV void pv(const Raw &r, const float (&p)[G], float (&o)[G][8]) const {
-    float vf[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) vf[i] = cbv[code_at(r.vw, i)] * r.sv;
-    // value outliers replace their channel (the first slot comes with the row; more are rare)
-    for (int j = 0; j < nov; ++j) {
-      const uint32_t ent = j == 0 ? r.vo : gld(vout + (size_t)r.t * nov + j);
-      if (ent == kNoOutlier) break;
-      const int ch = (int)(ent & 0xFFu) - c0;
-      const float x = h2f(ent >> 16);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) vf[i] = (ch == i) ? x : vf[i];
-    }
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o[g][i] = fmaf(p[g], vf[i], o[g][i]);
-  }
-};
-
-// Run one wave over tokens [a, b) of its tile, 32 tokens per batch.
+// Run one wave over tokens [a, b) of its tile.
 template <int D, int G, class L>
 MKV_DEV void wave_attend(L &ld, int a, int b, const Qs<G> &q, float qscale, float (&m_run)[G], float (&l)[G],
-                         float (&o)[G][8], int grp, int sub, float *logit_out) {
+                         float (&o)[G][8], int grp) {
   constexpr int LPT = Geo<D, G>::LPT, TPW = Geo<D, G>::TPW, U = Geo<D, G>::U;
   for (int base = a; base < b; base += U * TPW) {
     ld.prep(base, q);
@@ -292,8 +450,6 @@ MKV_DEV void wave_attend(L &ld, int a, int b, const Qs<G> &q, float qscale, floa
     typename L::Raw raw[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) ld.fetch(min(base + u * TPW + grp, b - 1), raw[u]);
-#pragma unroll
-    for (int u = 0; u < U; ++u) ld.fetch2(raw[u]);
     float s[U][G];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -304,17 +460,6 @@ MKV_DEV void wave_attend(L &ld, int a, int b, const Qs<G> &q, float qscale, floa
       for (int g = 0; g < G; ++g) {
         const float x = group_sum<LPT>(part[g]) * qscale;
         s[u][g] = valid ? x : -INFINITY;
-      }
-    }
-    if (logit_out != nullptr && sub == 0) {
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int t = base + u * TPW + grp;
-        if (t < b) {
-          const int sl = ld.slot(raw[u], t);
-#pragma unroll
-          for (int g = 0; g < G; ++g) gst(logit_out + (size_t)sl * G + g, s[u][g]);
-        }
       }
     }
 #pragma unroll
@@ -346,141 +491,25 @@ MKV_DEV void wave_attend(L &ld, int a, int b, const Qs<G> &q, float qscale, floa
   }
 }
 
-template <int D, int G>
-__global__ __launch_bounds__(kTileThreads) void k_attn_partial(
-    const SeqDesc *__restrict__ seqs, const int32_t *__restrict__ state, const int4 *__restrict__ tiles,
-    const uint16_t *__restrict__ q, float *__restrict__ partials, const float *__restrict__ cbtab,
-    int Hkv, float qscale) {
-  constexpr int LPT = Geo<D, G>::LPT, NW = kTileThreads / 64;
-  __shared__ float s_cb[32];
-  __shared__ float s_q[2 * G * D];            // KVQ: q and q * tau for outlier corrections
-  __shared__ float s_red[NW][G][D + 2];
-
-  const int4 tile = tiles[blockIdx.x];
-  const int seq = tile.x, h = tile.y;
-  const SeqDesc &sd = seqs[seq];
-  const int method = sd.method;
-  const int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
-  const int n_act = (method == ROCKET) ? st[ST_SEL_COUNT] : st[ST_COUNT];
-  const int t0 = tile.z, t1 = min(tile.w, n_act);
-
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int grp = lane / LPT, sub = lane % LPT, c0 = sub * 8;
-  const int Hq = Hkv * G;
-
-  Qs<G> qv;
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const U4 u = ld16(q + ((size_t)seq * Hq + h * G + g) * D + c0);
-    qv.h[g][0] = u.x; qv.h[g][1] = u.y; qv.h[g][2] = u.z; qv.h[g][3] = u.w;
-    unpack8(u, qv.f[g]);
-  }
-
-  float m_run[G], l[G], o[G][8];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    m_run[g] = -INFINITY;
-    l[g] = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) o[g][i] = 0.f;
-  }
-
-  // contiguous token range per wave, a multiple of 32 tokens (one batch)
+// ================================================================================================
+// The partial kernels: one over the tiles of matrix-path sequences, one over the uniform 4-bit
+// ones (kept apart so that neither's register budget limits the other's occupancy).
+// ================================================================================================
+// Contiguous token range [a, b) of this wave within its tile, a multiple of 32 tokens.
+struct WaveRange {
+  int a, b;
+};
+MKV_DEV WaveRange wave_range(int t0, int t1, int wave, int nw) {
   const int end = max(t1, t0);
-  const int span = ((end - t0 + NW - 1) / NW + 31) & ~31;
+  const int span = ((end - t0 + nw - 1) / nw + 31) & ~31;
   const int a = min(t0 + wave * span, end);
-  const int b = min(a + span, end);
+  return {a, min(a + span, end)};
+}
 
-  if (method == KVQ) {
-    const int nc = 1 << sd.bits;
-    const float *cb = cbtab + cb_offset(sd.bits);
-    if (threadIdx.x < nc) s_cb[threadIdx.x] = cb[threadIdx.x];
-    if (threadIdx.x < nc) s_cb[16 + threadIdx.x] = cb[nc + threadIdx.x];
-    const float2 *tt = reinterpret_cast<const float2 *>(sd.kmeta) + (size_t)h * D;
-    for (int e = threadIdx.x; e < G * D; e += kTileThreads) {
-      const int g = e / D, c = e % D;
-      const float qx = h2f(q[((size_t)seq * Hq + h * G + g) * D + c]);
-      s_q[e] = qx;
-      s_q[G * D + e] = qx * tt[c].x;
-    }
-  }
-  __syncthreads();
-
-  if (method == FP16 || method == H2O) {
-    LdRows<D, G> ld{reinterpret_cast<const uint16_t *>(sd.k) + h * stride_rows(sd, D),
-                    reinterpret_cast<const uint16_t *>(sd.v) + h * stride_rows(sd, D), c0};
-    float *lg = (method == H2O) ? reinterpret_cast<float *>(sd.logits) + h * stride_logits(sd, G) : nullptr;
-    wave_attend<D, G>(ld, a, b, qv, qscale, m_run, l, o, grp, sub, lg);
-  } else if (method == ROCKET) {
-    LdGather<D, G> ld{reinterpret_cast<const uint16_t *>(sd.k) + h * stride_rows(sd, D),
-                      reinterpret_cast<const uint16_t *>(sd.v) + h * stride_rows(sd, D),
-                      reinterpret_cast<const int32_t *>(sd.sel) + h * stride_sel(sd), c0};
-    wave_attend<D, G>(ld, a, b, qv, qscale, m_run, l, o, grp, sub, nullptr);
-  } else if (method == UQ) {
-    LdUQ<D, G> ld;
-    ld.kc = reinterpret_cast<const uint8_t *>(sd.kc) + h * stride_codes(sd);
-    ld.vc = reinterpret_cast<const uint8_t *>(sd.vc) + h * stride_codes(sd);
-    ld.kmeta = reinterpret_cast<const float2 *>(sd.kmeta) + h * stride_uq_kmeta(sd, D);
-    ld.vmeta = reinterpret_cast<const float2 *>(sd.vmeta) + h * stride_uq_vmeta(sd, D);
-    ld.kres = reinterpret_cast<const uint16_t *>(sd.kres) + (size_t)h * 64 * D;
-    ld.c0 = c0;
-    ld.full = (st[ST_COUNT] / 64) * 64;
-    ld.cur_blk = -1;
-#pragma unroll
-    for (int g = 0; g < G; ++g) ld.om[g] = 0.f;
-    wave_attend<D, G>(ld, a, b, qv, qscale, m_run, l, o, grp, sub, nullptr);
-    ld.finish(o);
-  } else if (method == KVQ) {
-    auto run = [&](auto bits_tag) {
-      constexpr int BITS = decltype(bits_tag)::value;
-      LdKVQ<D, G, BITS> ld;
-      ld.kc = reinterpret_cast<const uint8_t *>(sd.kc) + h * stride_codes(sd);
-      ld.vc = reinterpret_cast<const uint8_t *>(sd.vc) + h * stride_codes(sd);
-      ld.krow = reinterpret_cast<const uint32_t *>(sd.krow) + h * stride_krow(sd);
-      ld.kout = reinterpret_cast<const uint32_t *>(sd.kout) + h * stride_kout(sd);
-      ld.vout = reinterpret_cast<const uint32_t *>(sd.vout) + h * stride_vout(sd);
-      ld.vs = reinterpret_cast<const float *>(sd.vmeta) + h * stride_slots(sd);
-      ld.cbk = s_cb;
-      ld.cbv = s_cb + 16;
-      ld.qlds = s_q;
-      ld.c0 = c0;
-      ld.rowbytes = sd.rowbytes;
-      ld.nov = sd.nov_slots;
-#pragma unroll
-      for (int g = 0; g < G; ++g)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) ld.qp[g][i] = s_q[G * D + g * D + c0 + i];
-      wave_attend<D, G>(ld, a, b, qv, qscale, m_run, l, o, grp, sub, nullptr);
-    };
-    if (sd.bits == 4) run(std::integral_constant<int, 4>{});
-    else if (sd.bits == 3) run(std::integral_constant<int, 3>{});
-    else run(std::integral_constant<int, 2>{});
-  }
-
-  // reduce over the lane groups of the wave (they share m_run), then across waves via LDS
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-#pragma unroll
-    for (int m = LPT; m < 64; m <<= 1) {
-      l[g] += __shfl_xor(l[g], m);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o[g][i] += __shfl_xor(o[g][i], m);
-    }
-  }
-  // l was accumulated once per lane of a group; every lane of a group holds the same l
-  if (grp == 0) {
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) s_red[wave][g][2 + c0 + i] = o[g][i];
-      if (sub == 0) {
-        s_red[wave][g][0] = m_run[g];
-        s_red[wave][g][1] = l[g];
-      }
-    }
-  }
-  __syncthreads();
-  float *dst = partials + (size_t)blockIdx.x * G * (D + 2);
+// Merge the waves' (max, sum, o) into the tile's partial; `vc` (or null) holds per-wave additive
+// terms of o that share each wave's max.
+template <int D, int G, int NW>
+MKV_DEV void merge_waves(const float (*s_red)[G][D + 2], const float (*vc)[G][D], float *dst) {
   for (int e = threadIdx.x; e < G * (D + 2); e += kTileThreads) {
     const int g = e / (D + 2), c = e % (D + 2);
     float M = -INFINITY;
@@ -494,11 +523,232 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial(
     } else {
       val = 0.f;
 #pragma unroll
-      for (int w = 0; w < NW; ++w)
-        if (s_red[w][g][0] != -INFINITY) val += s_red[w][g][c] * exp2f(s_red[w][g][0] - M);
+      for (int w = 0; w < NW; ++w) {
+        if (s_red[w][g][0] == -INFINITY) continue;
+        float x = s_red[w][g][c];
+        if (vc != nullptr && c >= 2) x += vc[w][g][c - 2];
+        val += x * exp2f(s_red[w][g][0] - M);
+      }
     }
     dst[e] = val;
   }
+}
+
+template <int D, int G>
+__global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
+    const SeqDesc *__restrict__ seqs, const int32_t *__restrict__ state, const int4 *__restrict__ tiles,
+    const uint16_t *__restrict__ q, float *__restrict__ partials, const float *__restrict__ cbtab,
+    int Hkv, float qscale, int tile_base) {
+  constexpr int NW = kTileThreads / 64, NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
+  __shared__ float s_red[NW][G][D + 2];
+  __shared__ float s_vc[NW][G][D];           // KVQuant value-outlier corrections, per wave
+  __shared__ float s_q[2][G][D];             // KVQuant: q and q * tau
+  __shared__ uint2 s_lut[2][256];            // KVQuant: key and value pair tables
+  __shared__ float s_cb[2][16];              // KVQuant: codebooks
+
+  const int tid = tile_base + blockIdx.x;
+  const int4 tile = tiles[tid];
+  const int seq = tile.x, h = tile.y;
+  const SeqDesc &sd = seqs[seq];
+  const int method = sd.method;
+  const int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
+  const int n_act = (method == ROCKET) ? st[ST_SEL_COUNT] : st[ST_COUNT];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int Hq = Hkv * G;
+  const uint16_t *qh = q + ((size_t)seq * Hq + h * G) * D;
+  const WaveRange wr = wave_range(tile.z, min(tile.w, n_act), wave, NW);
+  const int lr = lane & 15, lq = lane >> 4;
+  const bool kvq = method == KVQ;
+  if (kvq) {
+    // codebook tables and q, q * tau for this kv head
+    const int bits = sd.bits, nc = 1 << bits;
+    const float *cb = cbtab + cb_offset(bits);
+    if (threadIdx.x < 32) {
+      const int which = threadIdx.x >> 4, i = threadIdx.x & 15;
+      s_cb[which][i] = i < nc ? cb[which * nc + i] : 0.f;
+    }
+    for (int e = threadIdx.x; e < 2 * (1 << (2 * bits)); e += kTileThreads) {
+      const int which = e >> (2 * bits), f = e & ((1 << (2 * bits)) - 1);
+      const float *c = cb + which * nc;
+      const float x0 = c[f & (nc - 1)], x1 = c[f >> bits];  // first, second code of the field
+      const float h0 = (float)(_Float16)x0, h1 = (float)(_Float16)x1;
+      s_lut[which][f] = make_uint2(pk_f16(h0, h1), pk_f16(x0 - h0, x1 - h1));
+    }
+    const float *tau = reinterpret_cast<const float *>(sd.kmeta) + (size_t)h * D * 2;
+    for (int e = threadIdx.x; e < G * D; e += kTileThreads) {
+      const int g = e / D, c = e % D;
+      const float qx = h2f(qh[(size_t)g * D + c]);
+      s_q[0][g][c] = qx;
+      s_q[1][g][c] = qx * gld(tau + 2 * c);
+    }
+    for (int e = lane; e < G * D; e += 64) (&s_vc[wave][0][0])[e] = 0.f;
+  }
+  __syncthreads();
+  // q.k operand B: query head lr (KVQuant: columns G..2G-1 carry the low part of q' of head
+  // lr - G), channels CPL*lq + 4m .. +3
+  QB<D> qb;
+#pragma unroll
+  for (int m = 0; m < NM; ++m) {
+    uint32_t hw[2] = {0u, 0u}, lw[2] = {0u, 0u};
+    const int c = CPL * lq + 4 * m;
+    if (kvq) {
+      if (lr < 2 * G) {
+        const int g = lr < G ? lr : lr - G;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const float x0 = s_q[1][g][c + 2 * j], x1 = s_q[1][g][c + 2 * j + 1];
+          const float h0 = (float)(_Float16)x0, h1 = (float)(_Float16)x1;
+          hw[j] = lr < G ? pk_f16(h0, h1) : pk_f16(x0 - h0, x1 - h1);
+          lw[j] = lr < G ? hw[j] : 0u;
+        }
+      }
+    } else if (lr < G) {
+      const uint32_t *qp = reinterpret_cast<const uint32_t *>(qh + (size_t)lr * D + c);
+      hw[0] = gld(qp);
+      hw[1] = gld(qp + 1);
+    }
+    qb.hi[m] = mk_h4(hw[0], hw[1]);
+    qb.lo[m] = mk_h4(lw[0], lw[1]);
+  }
+  float m_run = -INFINITY, l_part = 0.f;
+  f4v O[NM];
+#pragma unroll
+  for (int m = 0; m < NM; ++m) O[m] = f4v{0.f, 0.f, 0.f, 0.f};
+  if (method == FP16 || method == H2O) {
+    MRows<D, G, false> ld;
+    ld.K = reinterpret_cast<const uint16_t *>(sd.k) + h * stride_rows(sd, D);
+    ld.V = reinterpret_cast<const uint16_t *>(sd.v) + h * stride_rows(sd, D);
+    ld.sel = nullptr;
+    ld.lr = lr;
+    ld.lq = lq;
+    float *lg = (method == H2O) ? reinterpret_cast<float *>(sd.logits) + h * stride_logits(sd, G) : nullptr;
+    wave_mfma<D, G>(ld, wr.a, wr.b, qb, qscale, m_run, l_part, O, lg);
+  } else if (method == ROCKET) {
+    MRows<D, G, true> ld;
+    ld.K = reinterpret_cast<const uint16_t *>(sd.k) + h * stride_rows(sd, D);
+    ld.V = reinterpret_cast<const uint16_t *>(sd.v) + h * stride_rows(sd, D);
+    ld.sel = reinterpret_cast<const int32_t *>(sd.sel) + h * stride_sel(sd);
+    ld.lr = lr;
+    ld.lq = lq;
+    wave_mfma<D, G>(ld, wr.a, wr.b, qb, qscale, m_run, l_part, O, nullptr);
+  } else if (kvq) {
+    auto run = [&](auto bits_tag) {
+      constexpr int BITS = decltype(bits_tag)::value;
+      MKVQ<D, G, BITS> ld;
+      ld.kc = reinterpret_cast<const uint8_t *>(sd.kc) + h * stride_codes(sd);
+      ld.vc = reinterpret_cast<const uint8_t *>(sd.vc) + h * stride_codes(sd);
+      ld.krow = reinterpret_cast<const uint32_t *>(sd.krow) + h * stride_krow(sd);
+      ld.kout = reinterpret_cast<const uint32_t *>(sd.kout) + h * stride_kout(sd);
+      ld.vout = reinterpret_cast<const uint32_t *>(sd.vout) + h * stride_vout(sd);
+      ld.vsc = reinterpret_cast<const float *>(sd.vmeta) + h * stride_slots(sd);
+      ld.lutk = s_lut[0];
+      ld.lutv = s_lut[1];
+      ld.cbk = s_cb[0];
+      ld.cbv = s_cb[1];
+      ld.q32 = &s_q[0][0][0];
+      ld.qp32 = &s_q[1][0][0];
+      ld.vcorr = &s_vc[wave][0][0];
+      ld.lr = lr;
+      ld.lq = lq;
+      ld.rowbytes = sd.rowbytes;
+      ld.nov = sd.nov_slots;
+      ld.prole = lr < G ? 0 : lr < 2 * G ? 1 : 2;
+      wave_mfma<D, G>(ld, wr.a, wr.b, qb, qscale, m_run, l_part, O, nullptr);
+    };
+    if (sd.bits == 4) run(std::integral_constant<int, 4>{});
+    else if (sd.bits == 3) run(std::integral_constant<int, 3>{});
+    else run(std::integral_constant<int, 2>{});
+  }
+  // KVQuant: column lr + G holds the low-part products of head lr
+  if (kvq) {
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) O[m][i] += __shfl_xor(O[m][i], G);
+  }
+  // the 4 quads of a query head hold disjoint tokens
+  l_part += __shfl_xor(l_part, 16);
+  l_part += __shfl_xor(l_part, 32);
+  if (lr < G) {
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s_red[wave][lr][2 + VPL * (4 * lq + i) + m] = O[m][i];
+    if (lq == 0) {
+      s_red[wave][lr][0] = m_run;
+      s_red[wave][lr][1] = l_part;
+    }
+  }
+  __syncthreads();
+  merge_waves<D, G, NW>(s_red, kvq ? s_vc : nullptr, partials + (size_t)tid * G * (D + 2));
+}
+
+template <int D, int G>
+__global__ __launch_bounds__(kTileThreads) void k_attn_partial_uq(
+    const SeqDesc *__restrict__ seqs, const int32_t *__restrict__ state, const int4 *__restrict__ tiles,
+    const uint16_t *__restrict__ q, float *__restrict__ partials, int Hkv, float qscale, int tile_base) {
+  constexpr int NW = kTileThreads / 64, LPT = Geo<D, G>::LPT;
+  __shared__ float s_red[NW][G][D + 2];
+  const int tid = tile_base + blockIdx.x;
+  const int4 tile = tiles[tid];
+  const int seq = tile.x, h = tile.y;
+  const SeqDesc &sd = seqs[seq];
+  const int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint16_t *qh = q + ((size_t)seq * Hkv * G + h * G) * D;
+  const WaveRange wr = wave_range(tile.z, min(tile.w, st[ST_COUNT]), wave, NW);
+  const int grp = lane / LPT, sub = lane % LPT, c0 = sub * 8;
+  Qs<G> qv;
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const U4 u = gld16u(qh + (size_t)g * D + c0);
+    qv.h[g][0] = u.x; qv.h[g][1] = u.y; qv.h[g][2] = u.z; qv.h[g][3] = u.w;
+    unpack8(u, qv.f[g]);
+  }
+  float m_run[G], l[G], o[G][8];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m_run[g] = -INFINITY;
+    l[g] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[g][i] = 0.f;
+  }
+  LdUQ<D, G> ld;
+  ld.kc = reinterpret_cast<const uint8_t *>(sd.kc) + h * stride_codes(sd);
+  ld.vc = reinterpret_cast<const uint8_t *>(sd.vc) + h * stride_codes(sd);
+  ld.kmeta = reinterpret_cast<const float2 *>(sd.kmeta) + h * stride_uq_kmeta(sd, D);
+  ld.vmeta = reinterpret_cast<const float2 *>(sd.vmeta) + h * stride_uq_vmeta(sd, D);
+  ld.kres = reinterpret_cast<const uint16_t *>(sd.kres) + (size_t)h * 64 * D;
+  ld.c0 = c0;
+  ld.full = (st[ST_COUNT] / 64) * 64;
+  ld.cur_blk = -1;
+#pragma unroll
+  for (int g = 0; g < G; ++g) ld.om[g] = 0.f;
+  wave_attend<D, G>(ld, wr.a, wr.b, qv, qscale, m_run, l, o, grp);
+  ld.finish(o);
+  // reduce over the lane groups of the wave (they share m_run)
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+#pragma unroll
+    for (int m = LPT; m < 64; m <<= 1) {
+      l[g] += __shfl_xor(l[g], m);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[g][i] += __shfl_xor(o[g][i], m);
+    }
+  }
+  if (grp == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s_red[wave][g][2 + c0 + i] = o[g][i];
+      if (sub == 0) {
+        s_red[wave][g][0] = m_run[g];
+        s_red[wave][g][1] = l[g];
+      }
+    }
+  }
+  __syncthreads();
+  merge_waves<D, G, NW>(s_red, nullptr, partials + (size_t)tid * G * (D + 2));
 }
 
 // Log-sum-exp merge of one (sequence, kv head)'s tiles; H2O also adds every query head's
@@ -597,10 +847,15 @@ __global__ __launch_bounds__(256) void k_attn_combine(const SeqDesc *__restrict_
 }
 
 template <int D, int G>
-hipError_t partial_impl(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st) {
+hipError_t partial_impl(const Dev &dv, const Shape &sh, const uint16_t *q, int part, hipStream_t st) {
   const float qscale = kLog2e / sqrtf((float)D);
-  hipLaunchKernelGGL((k_attn_partial<D, G>), dim3(dv.n_tiles), dim3(kTileThreads), 0, st, dv.seqs,
-                     dv.state, dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale);
+  const int n_mx = dv.n_tiles - dv.n_tiles_uq;
+  if (part == 0 && n_mx > 0)
+    hipLaunchKernelGGL((k_attn_partial_mx<D, G>), dim3(n_mx), dim3(kTileThreads), 0, st, dv.seqs, dv.state,
+                       dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale, 0);
+  if (part == 1 && dv.n_tiles_uq > 0)
+    hipLaunchKernelGGL((k_attn_partial_uq<D, G>), dim3(dv.n_tiles_uq), dim3(kTileThreads), 0, st, dv.seqs,
+                       dv.state, dv.tiles, q, dv.partials, sh.Hkv, qscale, n_mx);
   return hipGetLastError();
 }
 
@@ -626,8 +881,8 @@ hipError_t combine_impl(const Dev &dv, const Shape &sh, float *out, hipStream_t 
     default: return hipErrorInvalidValue;                                     \
   }
 
-hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st) {
-  MKV_DISPATCH_DG(partial_impl, dv, sh, q, st)
+hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, int part, hipStream_t st) {
+  MKV_DISPATCH_DG(partial_impl, dv, sh, q, part, st)
 }
 
 hipError_t launch_attention_combine(const Dev &dv, const Shape &sh, float *out, hipStream_t st) {

@@ -110,24 +110,38 @@ __global__ __launch_bounds__(NT) void k_topk(const SeqDesc *__restrict__ seqs, i
   // approximate scores from the channel-major key copy: one lane per token (4 independent tokens
   // per lane in flight), channels ascending, acc = fl32(acc + fl32(qbar_c * k_jc)); the keys stay
   // in LDS when they fit
-  const uint16_t *kcm = reinterpret_cast<const uint16_t *>(sd.kcm) + h * stride_rows(sd, D);
+  const uint16_t *kcm = reinterpret_cast<const uint16_t *>(sd.kcm) + h * stride_kcm(sd, D);
   uint32_t *akeys = reinterpret_cast<uint32_t *>(sd.akeys) + h * stride_slots(sd);
   const bool in_lds = n <= kTopkLdsKeys;
-  const int cap = sd.cap;
-  for (int j0 = threadIdx.x; j0 < n; j0 += 4 * NT) {
+  const int cstride = sd.cstride;
+  // each lane scores 4 consecutive tokens from one 8-byte load per channel; the loads of 16
+  // channels are issued before any is used (rows are padded to 8 tokens, so the load never
+  // leaves the row)
+  for (int j0 = 4 * (int)threadIdx.x; j0 < n; j0 += 4 * NT) {
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int i = 0; i < nch; ++i) {
-      const float qb = s_sel_qb[i];
-      const uint16_t *row = kcm + (size_t)s_sel_ch[i] * cap;
+    for (int i0 = 0; i0 < nch; i0 += 16) {
+      uint32_t lo[16], hi[16];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int j = j0 + r * NT;
-        if (j < n) acc[r] = __fadd_rn(acc[r], __fmul_rn(qb, h2f(gld(row + j))));
+      for (int ii = 0; ii < 16; ++ii) {
+        const int i = min(i0 + ii, nch - 1);
+        const uint32_t *p = reinterpret_cast<const uint32_t *>(kcm + (size_t)s_sel_ch[i] * cstride + j0);
+        lo[ii] = gld(p);
+        hi[ii] = gld(p + 1);
+      }
+#pragma unroll
+      for (int ii = 0; ii < 16; ++ii) {
+        if (i0 + ii < nch) {
+          const float qb = s_sel_qb[i0 + ii];
+          acc[0] = __fadd_rn(acc[0], __fmul_rn(qb, h2f(lo[ii])));
+          acc[1] = __fadd_rn(acc[1], __fmul_rn(qb, h2f(lo[ii] >> 16)));
+          acc[2] = __fadd_rn(acc[2], __fmul_rn(qb, h2f(hi[ii])));
+          acc[3] = __fadd_rn(acc[3], __fmul_rn(qb, h2f(hi[ii] >> 16)));
+        }
       }
     }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int j = j0 + r * NT;
+      const int j = j0 + r;
       if (j < n) {
         if (in_lds) s_keys[j] = float_key(acc[r]);
         else gst(akeys + j, float_key(acc[r]));
@@ -518,9 +532,9 @@ __global__ __launch_bounds__(NT) void k_snap_keep(const SeqDesc *__restrict__ se
   const uint16_t *sv = reinterpret_cast<const uint16_t *>(sd.stage_v) + h * stride_stage(sd, D);
   uint16_t *dk = reinterpret_cast<uint16_t *>(sd.k) + h * stride_rows(sd, D);
   uint16_t *dvv = reinterpret_cast<uint16_t *>(sd.v) + h * stride_rows(sd, D);
-  uint16_t *kcm = reinterpret_cast<uint16_t *>(sd.kcm) + h * stride_rows(sd, D);
+  uint16_t *kcm = reinterpret_cast<uint16_t *>(sd.kcm) + h * stride_kcm(sd, D);
   int32_t *pos = reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd);
-  const int cap = sd.cap;
+  const int cap = sd.cap, cstride = sd.cstride;
   const int kept = compact_ascending(
       n0,
       [&](int j, int eq_before) {
@@ -539,7 +553,7 @@ __global__ __launch_bounds__(NT) void k_snap_keep(const SeqDesc *__restrict__ se
           *reinterpret_cast<uint4 *>(dvv + (size_t)slot * D + c) = *reinterpret_cast<const uint4 *>(sv + (size_t)j * D + c);
           const uint32_t wv[4] = {a.x, a.y, a.z, a.w};
 #pragma unroll
-          for (int e = 0; e < 8; ++e) kcm[(size_t)(c + e) * cap + slot] = (uint16_t)(wv[e / 2] >> (16 * (e & 1)));
+          for (int e = 0; e < 8; ++e) kcm[(size_t)(c + e) * cstride + slot] = (uint16_t)(wv[e / 2] >> (16 * (e & 1)));
         }
       },
       s_tmp);

@@ -35,12 +35,12 @@ mkv_status hip_fail(hipError_t e, const char *what) {
 
 enum Phase { PH_CREATED, PH_PROMPT, PH_READY, PH_APPENDED, PH_SELECTED, PH_ATTENDED };
 
-constexpr int kProfKinds = 5;
+constexpr int kProfKinds = 6;
 
 struct Layout {
   std::vector<SeqDesc> seqs;  // offsets (relative to the arena) in the pointer fields
   size_t off_seqs = 0, off_state = 0, off_tiles = 0, off_cbtab = 0, off_partials = 0, total = 0;
-  int n_tiles = 0;
+  int n_tiles = 0, n_tiles_uq = 0;
   std::vector<int4> tiles;
 };
 
@@ -152,7 +152,7 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
         d.kres = take(H * 64 * D * 2);
         break;
       case KVQ: {
-        d.cap = n0 + mn;
+        d.cap = (n0 + mn + 3) & ~3;  // value codes are stored in 4-token blocks
         d.rowbytes = D * c.bits / 8;
         d.n_o = (int)(((long long)n0 * c.outlier_bp + 5000) / 10000);
         d.n_ov = (int)(((long long)D * c.outlier_bp + 5000) / 10000);
@@ -196,7 +196,8 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
         const int nchunk = (n0 + 255) / 256;
         d.k = take(H * d.cap * D * 2);
         d.v = take(H * d.cap * D * 2);
-        d.kcm = take(H * d.cap * D * 2);
+        d.cstride = (d.cap + 7) & ~7;
+        d.kcm = take(H * d.cstride * D * 2);
         d.pos = take(H * d.cap * 4);
         d.sel = take(H * d.topk * 4);
         d.akeys = take(H * d.cap * 4);
@@ -210,10 +211,14 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
       }
     }
   }
-  // attention tiles: per sequence and kv head, ranges of `chunk` tokens over its largest active set
+  // attention tiles: per sequence and kv head, ranges of `chunk` tokens over its largest active set;
+  // sequences of the uniform 4-bit method last (their partial kernel runs on its own)
   L->tiles.clear();
+  L->n_tiles_uq = 0;
+  for (int pass = 0; pass < 2; ++pass)
   for (int s = 0; s < S; ++s) {
     SeqDesc &d = L->seqs[s];
+    if ((d.method == UQ) != (pass == 1)) continue;
     const int amax = d.method == ROCKET ? d.topk : d.cap;
     d.chunk = tile_tokens(d, D);
     d.tile_count = std::max(1, (amax + d.chunk - 1) / d.chunk);
@@ -225,6 +230,7 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
     for (int h = 0; h < Hkv; ++h)
       for (int t = 0; t < d.tile_count; ++t)
         L->tiles.push_back(make_int4(s, h, t * d.chunk, std::min(amax, (t + 1) * d.chunk)));
+    if (pass == 1) L->n_tiles_uq += Hkv * d.tile_count;
   }
   L->n_tiles = (int)L->tiles.size();
   L->off_tiles = take(sizeof(int4) * L->n_tiles);
@@ -364,6 +370,7 @@ mkv_status mkv_cache_create(const mkv_shape *shape, const mkv_config *cfg, const
   c->dv.partials = reinterpret_cast<float *>(c->arena + L.off_partials);
   c->dv.cbtab = reinterpret_cast<const float *>(c->arena + L.off_cbtab);
   c->dv.n_tiles = L.n_tiles;
+  c->dv.n_tiles_uq = L.n_tiles_uq;
   hipStream_t hst = static_cast<hipStream_t>(stream);
   hipError_t e = hipMemcpyAsync(c->arena + L.off_seqs, c->hs.data(), sizeof(SeqDesc) * c->hs.size(),
                                 hipMemcpyHostToDevice, hst);
@@ -495,9 +502,15 @@ mkv_status mkv_decode_attention(mkv_cache *c, const uint16_t *q, float *out, voi
     return fail(MKV_ESTATE, "attention must follow the decode append (and top-k selection)");
   hipStream_t hst = static_cast<hipStream_t>(stream);
   prof_mark(c, 0, 0, hst);
-  hipError_t e = launch_attention_partial(c->dv, c->sh, q, hst);
+  hipError_t e = launch_attention_partial(c->dv, c->sh, q, 0, hst);
   prof_mark(c, 0, 1, hst);
   if (e != hipSuccess) return hip_fail(e, "attention partial");
+  if (c->dv.n_tiles_uq > 0) {
+    prof_mark(c, 5, 0, hst);
+    e = launch_attention_partial(c->dv, c->sh, q, 1, hst);
+    prof_mark(c, 5, 1, hst);
+    if (e != hipSuccess) return hip_fail(e, "attention partial (uniform)");
+  }
   prof_mark(c, 1, 0, hst);
   e = launch_attention_combine(c->dv, c->sh, out, hst);
   prof_mark(c, 1, 1, hst);
@@ -518,9 +531,10 @@ mkv_status mkv_decode_step(mkv_cache *c, const uint16_t *k, const uint16_t *v, c
   return mkv_h2o_update_evict(c, nullptr, stream);
 }
 
-mkv_status mkv_attention_tiles(mkv_cache *c, int32_t *n_tiles) {
+mkv_status mkv_attention_tiles(mkv_cache *c, int32_t *n_tiles, int32_t *n_tiles_uq) {
   if (!c || !n_tiles) return fail(MKV_EINVAL, "NULL argument");
   *n_tiles = c->dv.n_tiles;
+  if (n_tiles_uq) *n_tiles_uq = c->dv.n_tiles_uq;
   return MKV_OK;
 }
 
@@ -577,10 +591,12 @@ mkv_status dget(std::vector<T> &dst, uint64_t src, size_t n) {
   return check_hip(e, "export copy");
 }
 
-int unpack_code(const uint8_t *row, int c, int bits, int D) {
-  if (bits == 4) return (row[c / 2] >> (4 * (c & 1))) & 15;
-  if (bits == 2) return (row[c / 4] >> (2 * (c & 3))) & 3;
-  return ((row[c / 4] >> (2 * (c & 3))) & 3) | (((row[D / 4 + c / 8] >> (c & 7)) & 1) << 2);
+// Code `i` of a packed bit string: bits [bits*i, bits*i + bits), little-endian.
+int unpack_bits(const uint8_t *p, int i, int bits) {
+  const int bit = bits * i;
+  uint32_t w = p[bit >> 3];
+  if ((bit & 7) + bits > 8) w |= (uint32_t)p[(bit >> 3) + 1] << 8;
+  return (int)((w >> (bit & 7)) & ((1u << bits) - 1));
 }
 
 }  // namespace
@@ -640,12 +656,17 @@ extern "C" mkv_status mkv_export(mkv_cache *c, int32_t seq, int32_t h, int32_t w
       const bool isk = what == MKV_EXPORT_CODES_K;
       const int n = (d.method == UQ && isk) ? (count / 64) * 64 : count;
       const int bits = d.method == UQ ? 4 : d.bits;
+      // KVQ values sit in 4-token blocks (code of channel c, token j at bit bits*(4c + j));
+      // every other code row is one token
+      const bool quad = d.method == KVQ && !isk;
+      const size_t nbytes = (size_t)(quad ? (n + 3) & ~3 : n) * d.rowbytes;
       std::vector<uint8_t> raw;
-      if ((st = dget(raw, (isk ? d.kc : d.vc) + (uint64_t)h * stride_codes(d), (size_t)n * d.rowbytes)) != MKV_OK)
-        return st;
+      if ((st = dget(raw, (isk ? d.kc : d.vc) + (uint64_t)h * stride_codes(d), nbytes)) != MKV_OK) return st;
       for (int t = 0; t < n; ++t)
         for (int ch = 0; ch < D; ++ch) {
-          const uint8_t code = (uint8_t)unpack_code(raw.data() + (size_t)t * d.rowbytes, ch, bits, D);
+          const uint8_t code = quad ? (uint8_t)unpack_bits(raw.data() + (size_t)(t / 4) * 4 * d.rowbytes,
+                                                           4 * ch + (t & 3), bits)
+                                    : (uint8_t)unpack_bits(raw.data() + (size_t)t * d.rowbytes, ch, bits);
           put(&code, 1);
         }
       break;

@@ -33,7 +33,8 @@ struct SeqDesc {
   int32_t window, pool, nch, bp;          // ROCKET window/pool/channels; KVQ outlier bp
   int32_t n_o, n_ov, nov_slots, rowbytes; // KVQ outlier counts; packed code row bytes
   int32_t pool_cap, nblk, w_eff, chunk;   // KVQ outlier pool; UQ blocks; window rows; tile tokens
-  int32_t tile_first, tile_count, q_off, pad0;  // partial tiles (per kv head); prompt-q row offset
+  int32_t tile_first, tile_count, q_off, cstride;  // partial tiles (per kv head); prompt-q row offset;
+                                                   // ROCKET channel-major row stride (cap rounded to 8)
   uint64_t k, v;            // fp16 [cap][d] rows (FP16 / H2O / ROCKET)
   uint64_t kc, vc;          // packed codes [cap][rowbytes] (UQ / KVQ)
   uint64_t kmeta, vmeta;    // UQ: float2 [nblk][d], float2 [cap][d/64]; KVQ: float2 tau/inv [d], float [cap]
@@ -64,6 +65,7 @@ __host__ __device__ inline int64_t stride_slots(const SeqDesc &s) { return (int6
 __host__ __device__ inline int64_t stride_logits(const SeqDesc &s, int G) { return (int64_t)s.cap * G; }
 __host__ __device__ inline int64_t stride_stage(const SeqDesc &s, int D) { return (int64_t)s.n0 * D; }
 __host__ __device__ inline int64_t stride_sel(const SeqDesc &s) { return (int64_t)(s.topk > 0 ? s.topk : 1); }
+__host__ __device__ inline int64_t stride_kcm(const SeqDesc &s, int D) { return (int64_t)s.cstride * D; }
 
 // Codebook table: for b = 2, 3, 4: cbK[2^b], cbV[2^b], midK[2^b-1], midV[2^b-1].
 __host__ __device__ inline int cb_offset(int bits) {
@@ -80,13 +82,15 @@ struct Dev {
   float *partials;       // device [n_tiles][G][D+2]
   const float *cbtab;    // device [kCbTableFloats]
   int n_tiles;
+  int n_tiles_uq;        // the last n_tiles_uq tiles belong to uniform 4-bit sequences
 };
 
 hipError_t launch_append_decode(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
                                 hipStream_t st);
 hipError_t launch_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
                               const uint16_t *k, const uint16_t *v, hipStream_t st);
-hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st);
+// part 0: matrix-path tiles (all but the last n_tiles_uq); part 1: uniform 4-bit tiles.
+hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, int part, hipStream_t st);
 hipError_t launch_attention_combine(const Dev &dv, const Shape &sh, float *out, hipStream_t st);
 hipError_t launch_topk(const Dev &dv, const Shape &sh, const uint16_t *q, int32_t *pos_out, int topk_max,
                        hipStream_t st);
