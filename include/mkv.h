@@ -104,7 +104,9 @@ mkv_status mkv_cache_bytes(const mkv_shape *shape, const mkv_config *cfg,
  * initialisation before returning).  codebooks: host float32, required when
  * any sequence uses MKV_KVQ, else may be NULL: for b = 2, 3, 4 in that order,
  * the key codebook (2^b ascending entries) then the value codebook (2^b
- * ascending entries): 56 floats in all.  They are copied.
+ * ascending entries): 56 floats in all, each exactly an fp16 value (the
+ * codebook is stored in fp16, like the cache's other values; MKV_EINVAL
+ * otherwise).  They are copied.
  * On success *out owns host metadata only; the arena stays the caller's.
  */
 mkv_status mkv_cache_create(const mkv_shape *shape, const mkv_config *cfg,
@@ -215,9 +217,10 @@ mkv_status mkv_export(mkv_cache *cache, int32_t seq, int32_t kv_head, int32_t wh
  * n_tokens rows, the values per token by theirs (same rules as the cache),
  * and a 2^bits-entry codebook is fitted by 1-D Lloyd k-means (quantile
  * start, nearest entry with ties to the lower one, empty clusters keep their
- * centre, at most 100 iterations) to the non-outlier normalised values.
+ * centre, at most 100 iterations) to the non-outlier normalised values; the
+ * centres are then rounded to fp16 (nearest even), the codebook's stored form.
  *   k, v     host fp16 [n_tokens][n_kv_heads][head_dim]
- *   cb_k, cb_v  host float32 [2^bits], ascending on return
+ *   cb_k, cb_v  host float32 [2^bits] holding fp16 values, ascending on return
  */
 mkv_status mkv_fit_codebooks(const uint16_t *k, const uint16_t *v, int32_t n_tokens,
                              int32_t n_kv_heads, int32_t head_dim, int32_t bits,

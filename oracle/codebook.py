@@ -10,14 +10,17 @@ calibration draw:
     the lower index) and moves each centroid to the mean of its samples; a
     centroid with no samples keeps its value;
   * iteration stops when no assignment changes, or after max_iter iterations;
-  * the result is cast to float32 and sorted ascending.
+  * the codebook is stored like every other value of the cache, in fp16: the
+    final centroids are rounded (once, to nearest even) to fp16 and sorted
+    ascending (returned as float32 holding fp16 values).
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 """
 import numpy as np
 
 
-def lloyd_codebook(samples, bits, max_iter=100, chunk=1 << 18):
+def lloyd_centroids(samples, bits, max_iter=100, chunk=1 << 18):
+    """Lloyd centroids in float64 (unrounded), in centroid-index order."""
     x = np.sort(np.asarray(samples, np.float64).ravel())
     n = x.size
     kk = 1 << int(bits)
@@ -37,4 +40,10 @@ def lloyd_codebook(samples, bits, max_iter=100, chunk=1 << 18):
         sums = np.bincount(assign, weights=x, minlength=kk)
         cnts = np.bincount(assign, minlength=kk)
         c = np.where(cnts > 0, sums / np.maximum(cnts, 1), c)
-    return np.sort(c.astype(np.float32))
+    return c
+
+
+def lloyd_codebook(samples, bits, max_iter=100, chunk=1 << 18):
+    """The stored codebook: Lloyd centroids rounded to fp16, ascending, as float32."""
+    c = lloyd_centroids(samples, bits, max_iter, chunk)
+    return np.sort(c.astype(np.float16).astype(np.float32))

@@ -6,6 +6,9 @@
 #include <vector>
 
 #include "mkv.h"
+#include "mkv_internal.h"
+
+using mkv::round_to_half;
 
 namespace {
 
@@ -71,8 +74,9 @@ std::vector<float> lloyd(std::vector<double> x, int bits) {
     for (int i = 0; i < K; ++i)
       if (cnt[i] > 0) c[i] = sum[i] / (double)cnt[i];
   }
+  // the codebook is stored in fp16, like the cache's other values
   std::vector<float> out(K);
-  for (int i = 0; i < K; ++i) out[i] = (float)c[i];
+  for (int i = 0; i < K; ++i) out[i] = round_to_half(c[i]);
   std::sort(out.begin(), out.end());
   return out;
 }

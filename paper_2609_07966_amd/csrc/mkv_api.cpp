@@ -328,6 +328,7 @@ mkv_status mkv_cache_create(const mkv_shape *shape, const mkv_config *cfg, const
         for (int i = 0; i < nc; ++i) {
           const float x = src[half * nc + i];
           if (!std::isfinite(x)) return fail(MKV_EINVAL, "codebook entry is not finite");
+          if (round_to_half(x) != x) return fail(MKV_EINVAL, "codebook entry %g is not an fp16 value", (double)x);
           if (i > 0 && !(x >= src[half * nc + i - 1])) return fail(MKV_EINVAL, "codebooks must be ascending");
           dst[half * nc + i] = x;
         }

@@ -1,6 +1,7 @@
 // Internal layout shared by the host library and the HIP kernels.
 #pragma once
 
+#include <math.h>
 #include <stdint.h>
 
 #include <hip/hip_runtime.h>
@@ -73,6 +74,15 @@ __host__ __device__ inline int cb_offset(int bits) {
   return bits == 2 ? 0 : bits == 3 ? 14 : 44;
 }
 constexpr int kCbTableFloats = 14 + 30 + 62;
+
+// Host: x rounded once, to nearest even, to the nearest fp16 value (finite |x| < 65520).
+inline float round_to_half(double x) {
+  if (x == 0.0 || !isfinite(x)) return (float)x;
+  int e;
+  frexp(x, &e);                                // |x| = m 2^e, m in [0.5, 1)
+  const int qexp = (e - 1 >= -14 ? e - 1 : -14) - 10;  // quantum: 2^-10 of the leading bit, or 2^-24
+  return (float)(nearbyint(ldexp(x, -qexp)) * ldexp(1.0, qexp));
+}
 
 // Kernel launchers (defined in the .hip files).  All enqueue on `st`.
 struct Dev {

@@ -166,14 +166,26 @@ def test_lloyd_fixed_point_and_separated_clusters():
     r = np.random.default_rng(14)
     centers = np.array([-3.0, -1.0, 0.5, 4.0])
     x = np.concatenate([c + 0.01 * r.standard_normal(1000) for c in centers])
-    cb = codebook.lloyd_codebook(x, 2)
+    cb = np.sort(codebook.lloyd_centroids(x, 2))
     np.testing.assert_allclose(cb, [x[i * 1000:(i + 1) * 1000].mean() for i in range(4)], atol=1e-6)
     # at convergence every centroid is the mean of the samples nearest to it
     y = r.standard_normal(20000)
-    cb = codebook.lloyd_codebook(y, 3, max_iter=1000).astype(np.float64)
+    cb = codebook.lloyd_centroids(y, 3, max_iter=1000)
     a = np.argmin(np.abs(y[:, None] - cb[None]), 1)
     for i in range(8):
         assert abs(y[a == i].mean() - cb[i]) < 1e-6
+
+
+def test_stored_codebook_is_the_fp16_rounding_of_the_centroids():
+    y = np.random.default_rng(15).standard_normal(20000) * 0.37
+    for bits in (2, 3, 4):
+        c = np.sort(codebook.lloyd_centroids(y, bits))
+        cb = codebook.lloyd_codebook(y, bits)
+        assert cb.dtype == np.float32 and np.all(np.diff(cb) >= 0)
+        # every entry is an fp16 value, within half an fp16 ulp of its centroid
+        assert np.array_equal(cb.astype(np.float16).astype(np.float32), cb)
+        ulp = np.spacing(np.abs(c).astype(np.float16)).astype(np.float64)
+        assert np.all(np.abs(cb.astype(np.float64) - c) <= ulp / 2)
 
 
 def test_kvq_sequence_dequant_error_is_bounded_by_the_codebook_gap():
