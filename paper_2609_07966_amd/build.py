@@ -25,6 +25,9 @@ def flags():
         # no packed fp32 instructions in device code; no implicit fused multiply-add (the
         # quantizer and approximate-score steps are specified in separately rounded float32)
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+        # matrix-core accumulators in ordinary VGPRs: the attention loop rescales them with VALU
+        # ops, which cannot read the accumulation registers
+        "-mllvm", "-amdgpu-mfma-vgpr-form",
         "-ffp-contract=off", "-Wall", "-Wno-unused-function", "-Wno-unknown-pragmas",
         "-I", os.path.join(ROOT, "include"), "-I", CSRC,
     ]

@@ -19,9 +19,9 @@ MKV_DEV int code_from_mid(float xhat, const float *mid, int nmid) {
   return c;
 }
 
-// Outlier entry: fp16 value in bits 16..31, the (clamped) code in bits 8..11, channel in 0..7.
-MKV_DEV uint32_t outlier_entry(uint32_t bits16, int code, int ch) {
-  return ((bits16 & 0xFFFFu) << 16) | ((uint32_t)code << 8) | (uint32_t)ch;
+// Outlier entry of token slot t (layout in outlier_pack): the (clamped) code stays in the entry.
+MKV_DEV uint32_t outlier_entry(uint32_t bits16, int t, int code, int ch) {
+  return outlier_pack(bits16 & 0xFFFFu, t, code, ch);
 }
 
 // Word w of a packed code row: code i sits at bits [bits*i, bits*i + bits) of the row (bit 0 =
@@ -107,9 +107,10 @@ MKV_DEV int kvq_value_token(const SeqDesc &sd, int h, int t, uint32_t vbits, con
   const bool outl = sd.bp > 0 && ax > s;
   int total;
   const int r = flag_rank<D>(outl, s_tmp, &total);
-  uint32_t *vo = reinterpret_cast<uint32_t *>(sd.vout) + h * stride_vout(sd) + (size_t)t * sd.nov_slots;
-  if (outl && r < sd.nov_slots) vo[r] = outlier_entry(vbits, code, c);
-  if (c >= total && c < sd.nov_slots) vo[c] = kNoOutlier;
+  // slot-major: entry r of token t at r * cap + t
+  uint32_t *vo = reinterpret_cast<uint32_t *>(sd.vout) + h * stride_vout(sd) + t;
+  if (outl && r < sd.nov_slots) vo[(size_t)r * sd.cap] = outlier_entry(vbits, t, code, c);
+  if (c >= total && c < sd.nov_slots) vo[(size_t)c * sd.cap] = kNoOutlier;
   if (c == 0) (reinterpret_cast<float *>(sd.vmeta) + h * stride_slots(sd))[t] = s;
   return code;
 }
@@ -245,7 +246,7 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
       const int r = flag_rank<D>(outl, s_tmp, &total);
       const int fill = st[ST_KOUT_FILL];
       uint32_t *ko = reinterpret_cast<uint32_t *>(sd.kout) + h * stride_kout(sd);
-      if (outl) ko[fill + r] = outlier_entry(kb, code, c);
+      if (outl) ko[fill + r] = outlier_entry(kb, count, code, c);
       const int vcode = kvq_value_token<D>(sd, h, count, vb, cbtab, s_abs, &s_scale, s_tmp);
       // the value code goes into its 4-token block: start from zero for the block's first token,
       // otherwise from the stored block
@@ -368,7 +369,7 @@ __global__ __launch_bounds__(128) void k_kvq_keys(const SeqDesc *__restrict__ se
   } else {
     int total;
     const int r = flag_rank<D>(outl, s_tmp, &total);
-    if (outl) (reinterpret_cast<uint32_t *>(sd.kout) + h * stride_kout(sd))[krow[t] + r] = outlier_entry(kb, code, c);
+    if (outl) (reinterpret_cast<uint32_t *>(sd.kout) + h * stride_kout(sd))[krow[t] + r] = outlier_entry(kb, t, code, c);
   }
 }
 

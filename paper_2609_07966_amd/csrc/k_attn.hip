@@ -10,12 +10,12 @@
 // v_mfma_f32_16x16x16_f16.  q.k is S^T = K Q^T (tokens x query heads; channels permuted so a
 // lane reads 32 contiguous channels of one token), and its result layout is exactly the operand
 // layout of P^T in O^T = V^T P^T (channels x query heads), so probabilities feed the second
-// product without moving.  KVQuant codes are turned into packed fp16 pairs by one LDS table
-// lookup per two codes; its key thresholds are folded into q and its value scales into p, and
-// outliers are applied as sparse corrections.  fp16 operands would cost KVQuant about 1e-3 of
-// the value RMS (codebook entries are not fp16 values), so codebook entries, q and p are split
-// into high and low fp16 parts: the low part of q or p rides in spare columns G..2G-1 of the
-// same product, and the low part of the codebook takes a second product.
+// product without moving.  KVQuant codes become packed fp16 pairs by one LDS table lookup per
+// two codes (codebook entries are fp16 values); its key thresholds are folded into q and its
+// value scales into p, both of which are fp32: their fp16 rounding residual rides in the spare
+// columns G..2G-1 of the same product and is added back after it.  Outliers are sparse
+// corrections: a batch's key outliers are loaded by the whole wave at once and scattered into
+// per-token logit terms in LDS; value outliers add to per-channel terms in LDS.
 //
 // Vector path (uniform 4-bit): D/8 lanes share a token (8 channels each) and reduce q.k with DPP
 // row ops; per-block key scales are folded into q once per 64-token block.
@@ -63,20 +63,17 @@ struct MG {
   static constexpr int NS = 2;        // 16-token steps per batch
 };
 
-// q.k operand B per MFMA.  fp16 rows: hi = q in columns 0..G-1.  KVQuant (q' = q tau):
-// hi = high part of q' in columns 0..G-1 and its low part in G..2G-1; lo = high part only,
-// multiplied by the low part of the codebook.
+// q.k operand B per MFMA: q of head lr in columns 0..G-1 (KVQuant: fp16 part of q' = q tau in
+// columns 0..G-1, its rounding residual in columns G..2G-1).
 template <int D>
 struct QB {
-  h4v hi[MG<D>::NM];
-  h4v lo[MG<D>::NM];
+  h4v b[MG<D>::NM];
 };
 
 // fp16 rows.  Gather: token t of the tile is the t-th selected slot (RocketKV).
 template <int D, int G, bool GATHER>
 struct MRows {
   static constexpr int NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
-  static constexpr bool kSplitQ = false, kQuant = false;
   const uint16_t *K, *V;
   const int32_t *sel;
   int lr, lq;
@@ -85,6 +82,7 @@ struct MRows {
     uint32_t vw[4][VPL / 2];
     int ks, vs[4];
   };
+  struct Batch {};
   MKV_DEV int slot_of(int t) const { return GATHER ? gld(sel + t) : t; }
   MKV_DEV void load_rows(Raw &r) const {
     const uint32_t *kp = reinterpret_cast<const uint32_t *>(K + (size_t)r.ks * D + CPL * lq);
@@ -106,16 +104,19 @@ struct MRows {
   MKV_DEV void fetch2(Raw &r) const {
     if (GATHER) load_rows(r);
   }
+  MKV_DEV void batch_fetch(int, int, Batch &) const {}
+  MKV_DEV void batch_fetch2(Batch &) const {}
+  MKV_DEV void batch_fix(const Batch &) const {}
   MKV_DEV int slot(const Raw &r, int j) const { return r.vs[j]; }
   MKV_DEV void qk(const Raw &r, const QB<D> &qb, f4v &S) const {
 #pragma unroll
-    for (int m = 0; m < NM; ++m) S = mfma16(mk_h4(r.kw[2 * m], r.kw[2 * m + 1]), qb.hi[m], S);
+    for (int m = 0; m < NM; ++m) S = mfma16(mk_h4(r.kw[2 * m], r.kw[2 * m + 1]), qb.b[m], S);
   }
-  MKV_DEV void kfix(const Raw &, float (&)[4]) const {}
+  MKV_DEV void kfix(int, float (&)[4]) const {}
   MKV_DEV void combine(float (&)[4]) const {}
   MKV_DEV float vscale(const Raw &, int) const { return 1.f; }
   MKV_DEV void vfix(const Raw &, const float (&)[4], const float (&)[4], int) const {}
-  MKV_DEV void rescale_fix(float) const {}
+  MKV_DEV void track_max(float) {}
   MKV_DEV void pv(const Raw &r, const float (&pp)[4], f4v (&O)[NM]) const {
     const h4v P = mk_h4(pk_f16(pp[0], pp[1]), pk_f16(pp[2], pp[3]));
 #pragma unroll
@@ -131,12 +132,10 @@ struct MRows {
 // KVQuant-style b-bit codes.  Key codes: code c of a row at bit b*c, so channels (2p, 2p+1)
 // form a 2b-bit field p.  Value codes: 4-token blocks with code (channel c, token j) at bit
 // b*(4c + j), so the tokens (0,1) and (2,3) of a channel form two 2b-bit fields.  A field
-// indexes a table of two packed fp16 pairs: high parts (cb[low code], cb[high code]) and the
-// low parts cb - high.
+// indexes a table of packed fp16 pairs (cb[first code], cb[second code]).
 template <int D, int G, int BITS>
 struct MKVQ {
   static constexpr int NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
-  static constexpr bool kSplitQ = true, kQuant = true;
   static constexpr int SEG = CPL * BITS;  // bits per lane segment (keys; values alike)
   // words per segment: a segment starts at bit SEG * lane_index, which is word aligned unless
   // SEG = 48 (d = 64, 3 bits), where it starts at bit 0 or 16 of a word and still spans 2 words
@@ -145,17 +144,25 @@ struct MKVQ {
   const uint8_t *kc, *vc;
   const uint32_t *krow, *kout, *vout;
   const float *vsc;
-  const uint2 *lutk, *lutv;       // LDS pair tables
+  const uint32_t *lutk, *lutv;    // LDS pair tables
   const float *cbk, *cbv;         // LDS codebooks
-  const float *q32, *qp32;        // LDS [G][D]: q and q * tau
-  float *vcorr;                   // LDS [G][D]: this wave's value-outlier corrections
-  int lr, lq, rowbytes, nov;
-  int prole;                      // p operand: 0 high part, 1 low part, 2 none (columns >= 2G)
+  const float *qq;                // LDS [D][2G]: q of heads 0..G-1, then q tau
+  float *vcorr;                   // LDS [G][D]: this wave's value-outlier terms, relative to vref
+  float *kcorr;                   // LDS [G][32]: this wave's key-outlier logit terms of the batch
+  int lr, lq, rowbytes, nov, cap;
+  int prole;                      // p operand: 0 fp16 part, 1 residual (columns G..2G-1), 2 zero
+  // The value-outlier terms of head lr are kept relative to a reference max vref <= m_run that
+  // moves only when m_run exceeds it by more than 8 (so the terms are rarely rescaled); a term
+  // computed against m_run is multiplied by vscl = 2^(m_run - vref) <= 2^8.
+  float vref, vscl;
   struct Raw {
     uint32_t kw[NW], vw[NW];
     float sv[4];
-    uint32_t ka[4], kb[4], e0[4], vo[4];
-    int t[4];
+    uint32_t vo[4];
+    int t0;
+  };
+  struct Batch {
+    uint32_t e0, e1, ent;
   };
   // load a segment and shift it to start at bit 0 of w[0]
   MKV_DEV void seg(const uint8_t *base, int bitoff, uint32_t (&w)[NW]) const {
@@ -181,91 +188,107 @@ struct MKVQ {
     // 32); past the end, the last block is re-read, whose slots all lie below the slot capacity
     // (a multiple of 4)
     const int t0 = min(base + 4 * lq, (b - 1) & ~3);
+    r.t0 = t0;
     seg(vc + (size_t)t0 * rowbytes, SEG * lr, r.vw);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      r.t[j] = t0 + j;
       r.sv[j] = gld(vsc + t0 + j);
-      r.ka[j] = gld(krow + t0 + j);
-      r.vo[j] = gld(vout + (size_t)(t0 + j) * nov);
-    }
-    uint32_t end = gld(krow + t0 + 4);
-    // slots at or past the count have no outlier range (their CSR words are not written)
-#pragma unroll
-    for (int j = 3; j >= 0; --j) {
-      const bool in = t0 + j < b;
-      r.kb[j] = in ? end : 0u;
-      end = r.ka[j];
-      r.ka[j] = in ? r.ka[j] : 0u;
+      r.vo[j] = gld(vout + t0 + j);  // entry 0 of each token (slot-major entries)
     }
   }
-  MKV_DEV void fetch2(Raw &r) const {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) r.e0[j] = r.ka[j] < r.kb[j] ? gld(kout + r.ka[j]) : kNoOutlier;
+  MKV_DEV void fetch2(Raw &) const {}
+  // The key outliers of the batch's slots [base, min(base + 32, b)) are one contiguous range of
+  // the pool: lane l takes entry l of it (CSR words past the count are never read).
+  MKV_DEV void batch_fetch(int base, int b, Batch &bt) const {
+    bt.e0 = gld(krow + base);
+    bt.e1 = gld(krow + min(base + 32, b));
   }
-  MKV_DEV int slot(const Raw &r, int j) const { return r.t[j]; }
+  MKV_DEV void batch_fetch2(Batch &bt) const {
+    const uint32_t e = bt.e0 + (threadIdx.x & 63);
+    bt.ent = e < bt.e1 ? gld(kout + e) : kNoOutlier;
+  }
+  // an outlier replaces its channel: add q x - q' cb[code] to the logit of (token, head)
+  MKV_DEV void kscatter(uint32_t ent) const {
+    if (ent == kNoOutlier) return;
+    const int ch = outlier_ch(ent), code = outlier_code(ent), tag = outlier_tag(ent);
+    const float x = h2f(ent >> 16), c = cbk[code];
+#pragma unroll
+    for (int g = 0; g < G; ++g) atomicAdd(&kcorr[g * 32 + tag], qq[ch * 2 * G + g] * x - qq[ch * 2 * G + G + g] * c);
+  }
+  MKV_DEV void batch_fix(const Batch &bt) const {
+    kscatter(bt.ent);
+    for (uint32_t off = 64; off < bt.e1 - bt.e0; off += 64) {  // more than 64 outliers: rare
+      const uint32_t e = bt.e0 + off + (threadIdx.x & 63);
+      kscatter(e < bt.e1 ? gld(kout + e) : kNoOutlier);
+    }
+  }
+  MKV_DEV int slot(const Raw &r, int j) const { return r.t0 + j; }
   MKV_DEV void qk(const Raw &r, const QB<D> &qb, f4v &S) const {
 #pragma unroll
-    for (int m = 0; m < NM; ++m) {
-      const uint2 e0 = lutk[field(r.kw, 2 * m)], e1 = lutk[field(r.kw, 2 * m + 1)];
-      S = mfma16(mk_h4(e0.x, e1.x), qb.hi[m], S);
-      S = mfma16(mk_h4(e0.y, e1.y), qb.lo[m], S);
-    }
+    for (int m = 0; m < NM; ++m)
+      S = mfma16(mk_h4(lutk[field(r.kw, 2 * m)], lutk[field(r.kw, 2 * m + 1)]), qb.b[m], S);
   }
-  // column g + G holds the low part of head g's logit
+  // step s of the batch: this lane's tokens 16 s + 4 lq + j, head lr; the terms are cleared
+  MKV_DEV void kfix(int s, float (&x)[4]) const {
+    if (lr >= G) return;
+    float4 *p = reinterpret_cast<float4 *>(kcorr + lr * 32 + 16 * s + 4 * lq);
+    const float4 c = *p;
+    x[0] += c.x;
+    x[1] += c.y;
+    x[2] += c.z;
+    x[3] += c.w;
+    *p = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  // column g + G holds the residual part of head g's logit
   MKV_DEV void combine(float (&x)[4]) const {
 #pragma unroll
     for (int j = 0; j < 4; ++j) x[j] += __shfl_xor(x[j], G);
   }
-  // key outliers replace their channel: add q x - q' cb16[code] to the raw logit
-  MKV_DEV void kfix_one(uint32_t ent, float &s) const {
-    const int ch = (int)(ent & 0xFFu), code = (int)((ent >> 8) & 15u);
-    s += q32[lr * D + ch] * h2f(ent >> 16) - qp32[lr * D + ch] * cbk[code];
-  }
-  MKV_DEV void kfix(const Raw &r, float (&s)[4]) const {
-    if (lr >= G) return;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (r.e0[j] == kNoOutlier) continue;
-      kfix_one(r.e0[j], s[j]);
-      for (uint32_t e = r.ka[j] + 1; e < r.kb[j]; ++e) kfix_one(gld(kout + e), s[j]);
-    }
-  }
   MKV_DEV float vscale(const Raw &r, int j) const { return r.sv[j]; }
-  // value outliers replace their channel: p x - p' cb16[code] accumulates in LDS per channel
+  // value outliers replace their channel: p x - p' cb[code] accumulates in LDS per channel
+  MKV_DEV void vadd(uint32_t ent, float p, float pp) const {
+    atomicAdd(&vcorr[lr * D + outlier_ch(ent)], (p * h2f(ent >> 16) - pp * cbv[outlier_code(ent)]) * vscl);
+  }
   MKV_DEV void vfix(const Raw &r, const float (&p)[4], const float (&pp)[4], int valid_mask) const {
     if (lr >= G) return;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (!((valid_mask >> j) & 1)) continue;
-      for (int i = 0; i < nov; ++i) {
-        const uint32_t ent = i == 0 ? r.vo[j] : gld(vout + (size_t)r.t[j] * nov + i);
-        if (ent == kNoOutlier) break;
-        const int ch = (int)(ent & 0xFFu), code = (int)((ent >> 8) & 15u);
-        atomicAdd(&vcorr[lr * D + ch], p[j] * h2f(ent >> 16) - pp[j] * cbv[code]);
+    for (int j = 0; j < 4; ++j)
+      if (((valid_mask >> j) & 1) && r.vo[j] != kNoOutlier) vadd(r.vo[j], p[j], pp[j]);
+    if (nov > 1) {  // further entries (outlier budgets above one per token)
+      for (int j = 0; j < 4; ++j) {
+        if (!((valid_mask >> j) & 1) || r.vo[j] == kNoOutlier) continue;
+        for (int i = 1; i < nov; ++i) {
+          const uint32_t ent = gld(vout + (size_t)i * cap + r.t0 + j);
+          if (ent == kNoOutlier) break;
+          vadd(ent, p[j], pp[j]);
+        }
       }
     }
   }
-  MKV_DEV void rescale_fix(float corr) const {
-    if (lr >= G || corr == 1.f) return;
-    for (int c = lq * (D / 4); c < (lq + 1) * (D / 4); ++c) vcorr[lr * D + c] *= corr;
+  MKV_DEV void track_max(float m_run) {
+    if (m_run - vref > 8.f) {
+      if (lr < G && vref != -INFINITY) {
+        const float f = fexp2(vref - m_run);
+        for (int c = lq * (D / 4); c < (lq + 1) * (D / 4); ++c) vcorr[lr * D + c] *= f;
+      }
+      vref = m_run;
+    }
+    vscl = fexp2(m_run - vref);
   }
+  // factor that brings the terms to the final m_run (0 when there are none)
+  MKV_DEV float vfactor(float m_run) const { return vref == -INFINITY ? 0.f : fexp2(vref - m_run); }
   MKV_DEV void pv(const Raw &r, const float (&pp)[4], f4v (&O)[NM]) const {
-    uint32_t w1[2], w2[2];
+    uint32_t w[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const float a = pp[2 * i], b = pp[2 * i + 1];
       const float ah = (float)(_Float16)a, bh = (float)(_Float16)b;
-      w1[i] = prole == 0 ? pk_f16(ah, bh) : prole == 1 ? pk_f16(a - ah, b - bh) : 0u;
-      w2[i] = prole == 0 ? pk_f16(ah, bh) : 0u;
+      w[i] = prole == 0 ? pk_f16(ah, bh) : prole == 1 ? pk_f16(a - ah, b - bh) : 0u;
     }
-    const h4v P1 = mk_h4(w1[0], w1[1]), P2 = mk_h4(w2[0], w2[1]);
+    const h4v P = mk_h4(w[0], w[1]);
 #pragma unroll
-    for (int m = 0; m < NM; ++m) {
-      const uint2 e0 = lutv[field(r.vw, 2 * m)], e1 = lutv[field(r.vw, 2 * m + 1)];
-      O[m] = mfma16(mk_h4(e0.x, e1.x), P1, O[m]);
-      O[m] = mfma16(mk_h4(e0.y, e1.y), P2, O[m]);
-    }
+    for (int m = 0; m < NM; ++m)
+      O[m] = mfma16(mk_h4(lutv[field(r.vw, 2 * m)], lutv[field(r.vw, 2 * m + 1)]), P, O[m]);
   }
 };
 
@@ -278,10 +301,14 @@ MKV_DEV void wave_mfma(L &ld, int a, int b, const QB<D> &qb, float qscale, float
   const int lane = threadIdx.x & 63, lr = lane & 15, lq = lane >> 4;
   for (int base = a; base < b; base += 16 * NS) {
     typename L::Raw raw[NS];
+    typename L::Batch bt;
 #pragma unroll
     for (int s = 0; s < NS; ++s) ld.fetch(base + 16 * s, b, raw[s]);
+    ld.batch_fetch(base, b, bt);
 #pragma unroll
     for (int s = 0; s < NS; ++s) ld.fetch2(raw[s]);
+    ld.batch_fetch2(bt);
+    ld.batch_fix(bt);
     float sc[NS][4];
     float mx = -INFINITY;
 #pragma unroll
@@ -289,7 +316,7 @@ MKV_DEV void wave_mfma(L &ld, int a, int b, const QB<D> &qb, float qscale, float
       f4v S = {0.f, 0.f, 0.f, 0.f};
       ld.qk(raw[s], qb, S);
       float x[4] = {S[0], S[1], S[2], S[3]};
-      ld.kfix(raw[s], x);
+      ld.kfix(s, x);
       ld.combine(x);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -312,8 +339,8 @@ MKV_DEV void wave_mfma(L &ld, int a, int b, const QB<D> &qb, float qscale, float
       l_part *= corr;
 #pragma unroll
       for (int m = 0; m < MG<D>::NM; ++m) O[m] *= corr;
-      ld.rescale_fix(corr);
       m_run = mx;
+      ld.track_max(m_run);
     }
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
@@ -507,9 +534,10 @@ MKV_DEV WaveRange wave_range(int t0, int t1, int wave, int nw) {
 }
 
 // Merge the waves' (max, sum, o) into the tile's partial; `vc` (or null) holds per-wave additive
-// terms of o that share each wave's max.
+// terms of o, to be multiplied by vf[wave][head] to share that wave's max.
 template <int D, int G, int NW>
-MKV_DEV void merge_waves(const float (*s_red)[G][D + 2], const float (*vc)[G][D], float *dst) {
+MKV_DEV void merge_waves(const float (*s_red)[G][D + 2], const float (*vc)[G][D], const float (*vf)[G],
+                         float *dst) {
   for (int e = threadIdx.x; e < G * (D + 2); e += kTileThreads) {
     const int g = e / (D + 2), c = e % (D + 2);
     float M = -INFINITY;
@@ -526,7 +554,7 @@ MKV_DEV void merge_waves(const float (*s_red)[G][D + 2], const float (*vc)[G][D]
       for (int w = 0; w < NW; ++w) {
         if (s_red[w][g][0] == -INFINITY) continue;
         float x = s_red[w][g][c];
-        if (vc != nullptr && c >= 2) x += vc[w][g][c - 2];
+        if (vc != nullptr && c >= 2) x += vc[w][g][c - 2] * vf[w][g];
         val += x * exp2f(s_red[w][g][0] - M);
       }
     }
@@ -542,9 +570,11 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   constexpr int NW = kTileThreads / 64, NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
   __shared__ float s_red[NW][G][D + 2];
   __shared__ float s_vc[NW][G][D];           // KVQuant value-outlier corrections, per wave
-  __shared__ float s_q[2][G][D];             // KVQuant: q and q * tau
-  __shared__ uint2 s_lut[2][256];            // KVQuant: key and value pair tables
+  __shared__ float s_q[D][2 * G];            // KVQuant: q of each head, then q * tau
+  __shared__ uint32_t s_lut[2][256];         // KVQuant: key and value pair tables
   __shared__ float s_cb[2][16];              // KVQuant: codebooks
+  __shared__ float s_kc[NW][G][32];          // KVQuant key-outlier logit terms, per wave
+  __shared__ float s_vf[NW][G];              // KVQuant: factor of each wave's s_vc
 
   const int tid = tile_base + blockIdx.x;
   const int4 tile = tiles[tid];
@@ -570,45 +600,42 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     for (int e = threadIdx.x; e < 2 * (1 << (2 * bits)); e += kTileThreads) {
       const int which = e >> (2 * bits), f = e & ((1 << (2 * bits)) - 1);
       const float *c = cb + which * nc;
-      const float x0 = c[f & (nc - 1)], x1 = c[f >> bits];  // first, second code of the field
-      const float h0 = (float)(_Float16)x0, h1 = (float)(_Float16)x1;
-      s_lut[which][f] = make_uint2(pk_f16(h0, h1), pk_f16(x0 - h0, x1 - h1));
+      s_lut[which][f] = pk_f16(c[f & (nc - 1)], c[f >> bits]);  // first, second code of the field
     }
     const float *tau = reinterpret_cast<const float *>(sd.kmeta) + (size_t)h * D * 2;
     for (int e = threadIdx.x; e < G * D; e += kTileThreads) {
       const int g = e / D, c = e % D;
       const float qx = h2f(qh[(size_t)g * D + c]);
-      s_q[0][g][c] = qx;
-      s_q[1][g][c] = qx * gld(tau + 2 * c);
+      s_q[c][g] = qx;
+      s_q[c][G + g] = qx * gld(tau + 2 * c);
     }
     for (int e = lane; e < G * D; e += 64) (&s_vc[wave][0][0])[e] = 0.f;
+    for (int e = lane; e < G * 32; e += 64) (&s_kc[wave][0][0])[e] = 0.f;
   }
   __syncthreads();
-  // q.k operand B: query head lr (KVQuant: columns G..2G-1 carry the low part of q' of head
-  // lr - G), channels CPL*lq + 4m .. +3
+  // q.k operand B: query head lr, channels CPL*lq + 4m .. +3 (KVQuant: fp16 part of q' in
+  // columns 0..G-1, its residual in columns G..2G-1)
   QB<D> qb;
 #pragma unroll
   for (int m = 0; m < NM; ++m) {
-    uint32_t hw[2] = {0u, 0u}, lw[2] = {0u, 0u};
+    uint32_t w[2] = {0u, 0u};
     const int c = CPL * lq + 4 * m;
     if (kvq) {
       if (lr < 2 * G) {
         const int g = lr < G ? lr : lr - G;
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          const float x0 = s_q[1][g][c + 2 * j], x1 = s_q[1][g][c + 2 * j + 1];
+          const float x0 = s_q[c + 2 * j][G + g], x1 = s_q[c + 2 * j + 1][G + g];
           const float h0 = (float)(_Float16)x0, h1 = (float)(_Float16)x1;
-          hw[j] = lr < G ? pk_f16(h0, h1) : pk_f16(x0 - h0, x1 - h1);
-          lw[j] = lr < G ? hw[j] : 0u;
+          w[j] = lr < G ? pk_f16(h0, h1) : pk_f16(x0 - h0, x1 - h1);
         }
       }
     } else if (lr < G) {
       const uint32_t *qp = reinterpret_cast<const uint32_t *>(qh + (size_t)lr * D + c);
-      hw[0] = gld(qp);
-      hw[1] = gld(qp + 1);
+      w[0] = gld(qp);
+      w[1] = gld(qp + 1);
     }
-    qb.hi[m] = mk_h4(hw[0], hw[1]);
-    qb.lo[m] = mk_h4(lw[0], lw[1]);
+    qb.b[m] = mk_h4(w[0], w[1]);
   }
   float m_run = -INFINITY, l_part = 0.f;
   f4v O[NM];
@@ -645,21 +672,25 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
       ld.lutv = s_lut[1];
       ld.cbk = s_cb[0];
       ld.cbv = s_cb[1];
-      ld.q32 = &s_q[0][0][0];
-      ld.qp32 = &s_q[1][0][0];
+      ld.qq = &s_q[0][0];
+      ld.kcorr = &s_kc[wave][0][0];
       ld.vcorr = &s_vc[wave][0][0];
       ld.lr = lr;
       ld.lq = lq;
       ld.rowbytes = sd.rowbytes;
       ld.nov = sd.nov_slots;
+      ld.cap = sd.cap;
       ld.prole = lr < G ? 0 : lr < 2 * G ? 1 : 2;
+      ld.vref = -INFINITY;
+      ld.vscl = 1.f;
       wave_mfma<D, G>(ld, wr.a, wr.b, qb, qscale, m_run, l_part, O, nullptr);
+      if (lr < G && lq == 0) s_vf[wave][lr] = ld.vfactor(m_run);
     };
     if (sd.bits == 4) run(std::integral_constant<int, 4>{});
     else if (sd.bits == 3) run(std::integral_constant<int, 3>{});
     else run(std::integral_constant<int, 2>{});
   }
-  // KVQuant: column lr + G holds the low-part products of head lr
+  // KVQuant: column lr + G holds the products of head lr's p residual
   if (kvq) {
 #pragma unroll
     for (int m = 0; m < NM; ++m)
@@ -680,7 +711,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     }
   }
   __syncthreads();
-  merge_waves<D, G, NW>(s_red, kvq ? s_vc : nullptr, partials + (size_t)tid * G * (D + 2));
+  merge_waves<D, G, NW>(s_red, kvq ? s_vc : nullptr, s_vf, partials + (size_t)tid * G * (D + 2));
 }
 
 template <int D, int G>
@@ -748,7 +779,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_uq(
     }
   }
   __syncthreads();
-  merge_waves<D, G, NW>(s_red, nullptr, partials + (size_t)tid * G * (D + 2));
+  merge_waves<D, G, NW>(s_red, nullptr, nullptr, partials + (size_t)tid * G * (D + 2));
 }
 
 // Log-sum-exp merge of one (sequence, kv head)'s tiles; H2O also adds every query head's

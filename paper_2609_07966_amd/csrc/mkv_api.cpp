@@ -681,15 +681,16 @@ extern "C" mkv_status mkv_export(mkv_cache *c, int32_t seq, int32_t h, int32_t w
         if ((st = dget(row, d.krow + (uint64_t)h * stride_krow(d) * 4, count + 1)) != MKV_OK) return st;
         if ((st = dget(pool, d.kout + (uint64_t)h * stride_kout(d) * 4, row[count])) != MKV_OK) return st;
         for (int t = 0; t < count; ++t)
-          for (uint32_t e2 = row[t]; e2 < row[t + 1]; ++e2) m[(size_t)t * D + (pool[e2] & 0xFF)] = (int32_t)(pool[e2] >> 16);
+          for (uint32_t e2 = row[t]; e2 < row[t + 1]; ++e2) m[(size_t)t * D + outlier_ch(pool[e2])] = (int32_t)(pool[e2] >> 16);
       } else {
         std::vector<uint32_t> vo;
-        if ((st = dget(vo, d.vout + (uint64_t)h * stride_vout(d) * 4, (size_t)count * d.nov_slots)) != MKV_OK) return st;
+        if ((st = dget(vo, d.vout + (uint64_t)h * stride_vout(d) * 4, (size_t)d.cap * d.nov_slots)) != MKV_OK)
+          return st;
         for (int t = 0; t < count; ++t)
           for (int j = 0; j < d.nov_slots; ++j) {
-            const uint32_t ent = vo[(size_t)t * d.nov_slots + j];
+            const uint32_t ent = vo[(size_t)j * d.cap + t];
             if (ent == kNoOutlier) break;
-            m[(size_t)t * D + (ent & 0xFF)] = (int32_t)(ent >> 16);
+            m[(size_t)t * D + outlier_ch(ent)] = (int32_t)(ent >> 16);
           }
       }
       put(m.data(), m.size() * 4);

@@ -24,7 +24,16 @@ enum StateWord : int32_t {
 
 constexpr int kTileThreads = 256;
 constexpr int kMaxG = 8;
-constexpr uint32_t kNoOutlier = 0xFFFFFFFFu;
+constexpr uint32_t kNoOutlier = 0xFFFFFFFFu;  // fp16 bits 0xFFFF (a NaN) never occur in an entry
+
+// KVQ outlier entry: the fp16 value in bits 16..31, the token's slot mod 32 in bits 11..15, the
+// code stored at the outlier's channel in bits 7..10, the channel (d <= 128) in bits 0..6.
+__host__ __device__ inline uint32_t outlier_pack(uint32_t bits16, int slot, int code, int ch) {
+  return (bits16 << 16) | ((uint32_t)(slot & 31) << 11) | ((uint32_t)code << 7) | (uint32_t)ch;
+}
+__host__ __device__ inline int outlier_ch(uint32_t e) { return (int)(e & 127u); }
+__host__ __device__ inline int outlier_code(uint32_t e) { return (int)((e >> 7) & 15u); }
+__host__ __device__ inline int outlier_tag(uint32_t e) { return (int)((e >> 11) & 31u); }
 
 // One sequence's configuration and region base pointers (kv head 0); every
 // region is [Hkv][...] with the per-head stride given by the helpers below.
@@ -40,7 +49,7 @@ struct SeqDesc {
   uint64_t kc, vc;          // packed codes [cap][rowbytes] (UQ / KVQ)
   uint64_t kmeta, vmeta;    // UQ: float2 [nblk][d], float2 [cap][d/64]; KVQ: float2 tau/inv [d], float [cap]
   uint64_t kres;            // UQ: fp16 [64][d] residual key block
-  uint64_t krow, kout, vout;// KVQ: u32 [cap+1] CSR, u32 [pool_cap], u32 [cap][nov_slots]
+  uint64_t krow, kout, vout;// KVQ: u32 [cap+1] CSR, u32 [pool_cap], u32 [nov_slots][cap]
   uint64_t pos, score;      // H2O / ROCKET: int32 [cap], float [cap]
   uint64_t logits;          // H2O: float [cap][G] log2-domain logits of the last attention
   uint64_t stage_k, stage_v;// H2O / ROCKET: fp16 [n0][d] prompt staging
