@@ -14,8 +14,10 @@
 // two codes (codebook entries are fp16 values); its key thresholds are folded into q and its
 // value scales into p, both of which are fp32: their fp16 rounding residual rides in the spare
 // columns G..2G-1 of the same product and is added back after it.  Outliers are sparse
-// corrections: a batch's key outliers are loaded by the whole wave at once and scattered into
-// per-token logit terms in LDS; value outliers add to per-channel terms in LDS.
+// corrections, applied without LDS atomics (which the LDS executes one lane at a time): a
+// batch's key outliers are loaded by the whole wave at once and gathered per token by lane
+// shuffles; value outliers accumulate in LDS rows private to each lane and are folded into the
+// output at the end.
 //
 // Vector path (uniform 4-bit): D/8 lanes share a token (8 channels each) and reduce q.k with DPP
 // row ops; per-block key scales are folded into q once per 64-token block.
@@ -55,6 +57,8 @@ MKV_DEV uint32_t pk_f16(float lo, float hi) { return f16bits(lo) | (f16bits(hi) 
 //   S              token rows 4*lq + j, query head lr
 //   p.v operand A  channel VPL*lr + m, tokens 4*lq + j
 //   O^T            channel VPL*(4*lq + i) + m, query head lr
+// Where q or p carry an fp16 rounding residual, the residual of head g sits in column 2G-1-g,
+// so one DPP mirror (quad, half-row or row) adds it to column g.
 template <int D>
 struct MG {
   static constexpr int NM = D / 16;   // MFMAs per 16-token step, for q.k and for p.v
@@ -63,8 +67,15 @@ struct MG {
   static constexpr int NS = 2;        // 16-token steps per batch
 };
 
-// q.k operand B per MFMA: q of head lr in columns 0..G-1 (KVQuant: fp16 part of q' = q tau in
-// columns 0..G-1, its rounding residual in columns G..2G-1).
+template <int G>
+MKV_DEV float mirror_cols(float x) {
+  if constexpr (G == 1) return dpp<0xB1>(x);        // quad_perm [1,0,3,2]
+  else if constexpr (G == 2) return dpp<0x1B>(x);   // quad_perm [3,2,1,0]
+  else if constexpr (G == 4) return dpp<0x141>(x);  // row_half_mirror
+  else return dpp<0x140>(x);                        // row_mirror
+}
+
+// q.k operand B per MFMA (see the kernel for its columns).
 template <int D>
 struct QB {
   h4v b[MG<D>::NM];
@@ -74,6 +85,8 @@ struct QB {
 template <int D, int G, bool GATHER>
 struct MRows {
   static constexpr int NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
+  static constexpr bool kSplit = false;   // q and p enter as single fp16 parts
+  static constexpr bool kScaled = false;  // logits still need the log2(e)/sqrt(d) factor
   const uint16_t *K, *V;
   const int32_t *sel;
   int lr, lq;
@@ -83,7 +96,21 @@ struct MRows {
     int ks, vs[4];
   };
   struct Batch {};
+  // Gather: the slots of the next batch, loaded one batch ahead so that row loads never wait
+  // for their index loads
+  struct Carry {
+    int ks[MG<D>::NS], vs[MG<D>::NS][4];
+  };
   MKV_DEV int slot_of(int t) const { return GATHER ? gld(sel + t) : t; }
+  MKV_DEV void carry(int base, int b, Carry &cy) const {
+    if (!GATHER) return;
+#pragma unroll
+    for (int s = 0; s < MG<D>::NS; ++s) {
+      cy.ks[s] = gld(sel + min(base + 16 * s + lr, b - 1));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) cy.vs[s][j] = gld(sel + min(base + 16 * s + 4 * lq + j, b - 1));
+    }
+  }
   MKV_DEV void load_rows(Raw &r) const {
     const uint32_t *kp = reinterpret_cast<const uint32_t *>(K + (size_t)r.ks * D + CPL * lq);
 #pragma unroll
@@ -95,17 +122,22 @@ struct MRows {
       for (int i = 0; i < VPL / 2; ++i) r.vw[j][i] = gld(vp + i);
     }
   }
-  MKV_DEV void fetch(int base, int b, Raw &r) const {
-    r.ks = slot_of(min(base + lr, b - 1));
+  // step s: FULL: all 16 tokens of the step exist; otherwise indices past the end re-read the
+  // last one
+  template <bool FULL>
+  MKV_DEV void fetch(int base, int b, int s, const Carry &cy, Raw &r) const {
+    if (GATHER) {
+      r.ks = cy.ks[s];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) r.vs[j] = slot_of(min(base + 4 * lq + j, b - 1));
-    if (!GATHER) load_rows(r);
+      for (int j = 0; j < 4; ++j) r.vs[j] = cy.vs[s][j];
+    } else {
+      r.ks = FULL ? base + lr : min(base + lr, b - 1);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) r.vs[j] = FULL ? base + 4 * lq + j : min(base + 4 * lq + j, b - 1);
+    }
+    load_rows(r);
   }
-  MKV_DEV void fetch2(Raw &r) const {
-    if (GATHER) load_rows(r);
-  }
-  MKV_DEV void batch_fetch(int, int, Batch &) const {}
-  MKV_DEV void batch_fetch2(Batch &) const {}
+  MKV_DEV void batch_fetch(const Carry &, Batch &) const {}
   MKV_DEV void batch_fix(const Batch &) const {}
   MKV_DEV int slot(const Raw &r, int j) const { return r.vs[j]; }
   MKV_DEV void qk(const Raw &r, const QB<D> &qb, f4v &S) const {
@@ -113,7 +145,6 @@ struct MRows {
     for (int m = 0; m < NM; ++m) S = mfma16(mk_h4(r.kw[2 * m], r.kw[2 * m + 1]), qb.b[m], S);
   }
   MKV_DEV void kfix(int, float (&)[4]) const {}
-  MKV_DEV void combine(float (&)[4]) const {}
   MKV_DEV float vscale(const Raw &, int) const { return 1.f; }
   MKV_DEV void vfix(const Raw &, const float (&)[4], const float (&)[4], int) const {}
   MKV_DEV void track_max(float) {}
@@ -136,6 +167,8 @@ struct MRows {
 template <int D, int G, int BITS>
 struct MKVQ {
   static constexpr int NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
+  static constexpr bool kSplit = true;   // fp16 residuals of q' and p in columns G..2G-1
+  static constexpr bool kScaled = true;  // q' carries log2(e)/sqrt(d)
   static constexpr int SEG = CPL * BITS;  // bits per lane segment (keys; values alike)
   // words per segment: a segment starts at bit SEG * lane_index, which is word aligned unless
   // SEG = 48 (d = 64, 3 bits), where it starts at bit 0 or 16 of a word and still spans 2 words
@@ -146,11 +179,11 @@ struct MKVQ {
   const float *vsc;
   const uint32_t *lutk, *lutv;    // LDS pair tables
   const float *cbk, *cbv;         // LDS codebooks
-  const float *qq;                // LDS [D][2G]: q of heads 0..G-1, then q tau
-  float *vcorr;                   // LDS [G][D]: this wave's value-outlier terms, relative to vref
+  const float *qq;                // LDS [D][2G]: scaled q of heads 0..G-1, then scaled q tau
+  float *vcorr;                   // LDS [D]: this lane's value-outlier terms (head lr), relative to vref
   float *kcorr;                   // LDS [G][32]: this wave's key-outlier logit terms of the batch
   int lr, lq, rowbytes, nov, cap;
-  int prole;                      // p operand: 0 fp16 part, 1 residual (columns G..2G-1), 2 zero
+  int prole;                      // p operand: 0 fp16 part, 1 residual, 2 zero
   // The value-outlier terms of head lr are kept relative to a reference max vref <= m_run that
   // moves only when m_run exceeds it by more than 8 (so the terms are rarely rescaled); a term
   // computed against m_run is multiplied by vscl = 2^(m_run - vref) <= 2^8.
@@ -162,8 +195,17 @@ struct MKVQ {
     int t0;
   };
   struct Batch {
-    uint32_t e0, e1, ent;
+    uint32_t kr, ent;
   };
+  // The key outliers of a batch's slots [base, min(base + 32, b)) are one contiguous range of
+  // the pool: lane l <= 32 holds the CSR word of slot base + l (clamped to b; CSR words past the
+  // count are never read), loaded one batch ahead.
+  struct Carry {
+    uint32_t kr;
+  };
+  MKV_DEV void carry(int base, int b, Carry &cy) const {
+    cy.kr = gld(krow + min(base + min((int)(threadIdx.x & 63), 32), b));
+  }
   // load a segment and shift it to start at bit 0 of w[0]
   MKV_DEV void seg(const uint8_t *base, int bitoff, uint32_t (&w)[NW]) const {
     const uint32_t *p = reinterpret_cast<const uint32_t *>(base) + (bitoff >> 5);
@@ -181,13 +223,14 @@ struct MKVQ {
     if (s + 2 * BITS <= 32) return (w[i] >> s) & FMASK;
     return __builtin_amdgcn_alignbit(w[i + 1], w[i], s) & FMASK;
   }
-  MKV_DEV void fetch(int base, int b, Raw &r) const {
-    const int tk = min(base + lr, b - 1);
+  // this lane's 4 tokens form one 4-token block (tile and wave ranges start at multiples of 32);
+  // past the end, the last block is re-read, whose slots all lie below the slot capacity (a
+  // multiple of 4)
+  template <bool FULL>
+  MKV_DEV void fetch(int base, int b, int, const Carry &, Raw &r) const {
+    const int tk = FULL ? base + lr : min(base + lr, b - 1);
     seg(kc + (size_t)tk * rowbytes, SEG * lq, r.kw);
-    // this lane's 4 tokens form one 4-token block (tile and wave ranges start at multiples of
-    // 32); past the end, the last block is re-read, whose slots all lie below the slot capacity
-    // (a multiple of 4)
-    const int t0 = min(base + 4 * lq, (b - 1) & ~3);
+    const int t0 = FULL ? base + 4 * lq : min(base + 4 * lq, (b - 1) & ~3);
     r.t0 = t0;
     seg(vc + (size_t)t0 * rowbytes, SEG * lr, r.vw);
 #pragma unroll
@@ -196,30 +239,39 @@ struct MKVQ {
       r.vo[j] = gld(vout + t0 + j);  // entry 0 of each token (slot-major entries)
     }
   }
-  MKV_DEV void fetch2(Raw &) const {}
-  // The key outliers of the batch's slots [base, min(base + 32, b)) are one contiguous range of
-  // the pool: lane l takes entry l of it (CSR words past the count are never read).
-  MKV_DEV void batch_fetch(int base, int b, Batch &bt) const {
-    bt.e0 = gld(krow + base);
-    bt.e1 = gld(krow + min(base + 32, b));
+  // lane l takes entry l of the batch's key-outlier range
+  MKV_DEV void batch_fetch(const Carry &cy, Batch &bt) const {
+    bt.kr = cy.kr;
+    const uint32_t e0 = __builtin_amdgcn_readlane(cy.kr, 0), e1 = __builtin_amdgcn_readlane(cy.kr, 32);
+    const uint32_t e = e0 + (threadIdx.x & 63);
+    bt.ent = e < e1 ? gld(kout + e) : kNoOutlier;
   }
-  MKV_DEV void batch_fetch2(Batch &bt) const {
-    const uint32_t e = bt.e0 + (threadIdx.x & 63);
-    bt.ent = e < bt.e1 ? gld(kout + e) : kNoOutlier;
-  }
-  // an outlier replaces its channel: add q x - q' cb[code] to the logit of (token, head)
-  MKV_DEV void kscatter(uint32_t ent) const {
-    if (ent == kNoOutlier) return;
-    const int ch = outlier_ch(ent), code = outlier_code(ent), tag = outlier_tag(ent);
-    const float x = h2f(ent >> 16), c = cbk[code];
-#pragma unroll
-    for (int g = 0; g < G; ++g) atomicAdd(&kcorr[g * 32 + tag], qq[ch * 2 * G + g] * x - qq[ch * 2 * G + G + g] * c);
-  }
+  // Lane t < 32 sums, per head, q x - q' cb[code] over the outliers of slot base + t (each
+  // replaces its channel) and writes the sums to kcorr[head][t].
   MKV_DEV void batch_fix(const Batch &bt) const {
-    kscatter(bt.ent);
-    for (uint32_t off = 64; off < bt.e1 - bt.e0; off += 64) {  // more than 64 outliers: rare
-      const uint32_t e = bt.e0 + off + (threadIdx.x & 63);
-      kscatter(e < bt.e1 ? gld(kout + e) : kNoOutlier);
+    const int lane = threadIdx.x & 63;
+    const uint32_t e0 = __builtin_amdgcn_readlane(bt.kr, 0);
+    const int k0 = (int)(bt.kr - e0);
+    const int k1 = (int)((uint32_t)__shfl_down((int)bt.kr, 1) - e0);
+    const int cnt = lane < 32 ? k1 - k0 : 0;
+    float acc[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) acc[g] = 0.f;
+    for (int i = 0; __any(i < cnt); ++i) {
+      const int src = k0 + i;
+      // entries past the 64 loaded by the wave (more than 64 in one batch) come from memory
+      uint32_t ent = (uint32_t)__shfl((int)bt.ent, min(src, 63));
+      if (i < cnt && src >= 64) ent = gld(kout + e0 + src);
+      if (i < cnt) {
+        const int ch = outlier_ch(ent);
+        const float x = h2f(ent >> 16), c = cbk[outlier_code(ent)];
+#pragma unroll
+        for (int g = 0; g < G; ++g) acc[g] += qq[ch * 2 * G + g] * x - qq[ch * 2 * G + G + g] * c;
+      }
+    }
+    if (lane < 32) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) kcorr[g * 32 + lane] = acc[g];
     }
   }
   MKV_DEV int slot(const Raw &r, int j) const { return r.t0 + j; }
@@ -228,39 +280,34 @@ struct MKVQ {
     for (int m = 0; m < NM; ++m)
       S = mfma16(mk_h4(lutk[field(r.kw, 2 * m)], lutk[field(r.kw, 2 * m + 1)]), qb.b[m], S);
   }
-  // step s of the batch: this lane's tokens 16 s + 4 lq + j, head lr; the terms are cleared
+  // step s of the batch: this lane's tokens 16 s + 4 lq + j, head lr
   MKV_DEV void kfix(int s, float (&x)[4]) const {
     if (lr >= G) return;
-    float4 *p = reinterpret_cast<float4 *>(kcorr + lr * 32 + 16 * s + 4 * lq);
-    const float4 c = *p;
+    const float4 c = *reinterpret_cast<const float4 *>(kcorr + lr * 32 + 16 * s + 4 * lq);
     x[0] += c.x;
     x[1] += c.y;
     x[2] += c.z;
     x[3] += c.w;
-    *p = make_float4(0.f, 0.f, 0.f, 0.f);
-  }
-  // column g + G holds the residual part of head g's logit
-  MKV_DEV void combine(float (&x)[4]) const {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) x[j] += __shfl_xor(x[j], G);
   }
   MKV_DEV float vscale(const Raw &r, int j) const { return r.sv[j]; }
-  // value outliers replace their channel: p x - p' cb[code] accumulates in LDS per channel
-  MKV_DEV void vadd(uint32_t ent, float p, float pp) const {
-    atomicAdd(&vcorr[lr * D + outlier_ch(ent)], (p * h2f(ent >> 16) - pp * cbv[outlier_code(ent)]) * vscl);
-  }
+  // value outliers replace their channel: p x - p' cb[code] accumulates in this lane's LDS row
+  // (an absent or masked entry adds 0 to channel 0)
   MKV_DEV void vfix(const Raw &r, const float (&p)[4], const float (&pp)[4], int valid_mask) const {
     if (lr >= G) return;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (((valid_mask >> j) & 1) && r.vo[j] != kNoOutlier) vadd(r.vo[j], p[j], pp[j]);
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t ent = r.vo[j];
+      const bool ok = ((valid_mask >> j) & 1) && ent != kNoOutlier;
+      const float val = (p[j] * h2f(ent >> 16) - pp[j] * cbv[outlier_code(ent)]) * vscl;
+      vcorr[ok ? outlier_ch(ent) : 0] += ok ? val : 0.f;
+    }
     if (nov > 1) {  // further entries (outlier budgets above one per token)
       for (int j = 0; j < 4; ++j) {
         if (!((valid_mask >> j) & 1) || r.vo[j] == kNoOutlier) continue;
         for (int i = 1; i < nov; ++i) {
           const uint32_t ent = gld(vout + (size_t)i * cap + r.t0 + j);
           if (ent == kNoOutlier) break;
-          vadd(ent, p[j], pp[j]);
+          vcorr[outlier_ch(ent)] += (p[j] * h2f(ent >> 16) - pp[j] * cbv[outlier_code(ent)]) * vscl;
         }
       }
     }
@@ -269,7 +316,15 @@ struct MKVQ {
     if (m_run - vref > 8.f) {
       if (lr < G && vref != -INFINITY) {
         const float f = fexp2(vref - m_run);
-        for (int c = lq * (D / 4); c < (lq + 1) * (D / 4); ++c) vcorr[lr * D + c] *= f;
+        float4 *row = reinterpret_cast<float4 *>(vcorr);
+        for (int c = 0; c < D / 4; ++c) {
+          float4 v = row[c];
+          v.x *= f;
+          v.y *= f;
+          v.z *= f;
+          v.w *= f;
+          row[c] = v;
+        }
       }
       vref = m_run;
     }
@@ -292,71 +347,92 @@ struct MKVQ {
   }
 };
 
-// One wave over tokens [a, b) of its tile, 32 tokens per batch.  m_run / l_part belong to this
-// lane's query head (lr); O holds this lane's part of O^T.
-template <int D, int G, class L>
-MKV_DEV void wave_mfma(L &ld, int a, int b, const QB<D> &qb, float qscale, float &m_run, float &l_part,
-                       f4v (&O)[MG<D>::NM], float *logit_out) {
+// One 32-token batch of a wave.  FULL: all 32 tokens exist (no clamping, no masks).
+template <bool FULL, int D, int G, class L>
+MKV_DEV void mfma_batch(L &ld, int base, int b, typename L::Carry &cy, const QB<D> &qb, float qscale,
+                        float &m_run, float &l_part, f4v (&O)[MG<D>::NM], float *logit_out) {
   constexpr int NS = MG<D>::NS;
   const int lane = threadIdx.x & 63, lr = lane & 15, lq = lane >> 4;
-  for (int base = a; base < b; base += 16 * NS) {
-    typename L::Raw raw[NS];
-    typename L::Batch bt;
+  typename L::Raw raw[NS];
+  typename L::Batch bt;
+  // issue order: loads that depend on the carried indices first, then this batch's rows or
+  // codes, then the next batch's indices
+  ld.batch_fetch(cy, bt);
 #pragma unroll
-    for (int s = 0; s < NS; ++s) ld.fetch(base + 16 * s, b, raw[s]);
-    ld.batch_fetch(base, b, bt);
+  for (int s = 0; s < NS; ++s) ld.template fetch<FULL>(base + 16 * s, b, s, cy, raw[s]);
+  ld.carry(base + 16 * NS, b, cy);
+  ld.batch_fix(bt);
+  float sc[NS][4];
+  float mx = -INFINITY;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) ld.fetch2(raw[s]);
-    ld.batch_fetch2(bt);
-    ld.batch_fix(bt);
-    float sc[NS][4];
-    float mx = -INFINITY;
+  for (int s = 0; s < NS; ++s) {
+    f4v S = {0.f, 0.f, 0.f, 0.f};
+    ld.qk(raw[s], qb, S);
+    float x[4] = {S[0], S[1], S[2], S[3]};
+    ld.kfix(s, x);
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      f4v S = {0.f, 0.f, 0.f, 0.f};
-      ld.qk(raw[s], qb, S);
-      float x[4] = {S[0], S[1], S[2], S[3]};
-      ld.kfix(s, x);
-      ld.combine(x);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const bool valid = base + 16 * s + 4 * lq + j < b;
-        sc[s][j] = valid ? x[j] * qscale : -INFINITY;
-        mx = fmaxf(mx, sc[s][j]);
-      }
+    for (int j = 0; j < 4; ++j) {
+      if (L::kSplit) x[j] += mirror_cols<G>(x[j]);
+      float v = L::kScaled ? x[j] : x[j] * qscale;
+      if (!FULL) v = base + 16 * s + 4 * lq + j < b ? v : -INFINITY;
+      sc[s][j] = v;
+      mx = fmaxf(mx, v);
     }
-    if (logit_out != nullptr && lr < G) {
+  }
+  if (logit_out != nullptr && lr < G) {
 #pragma unroll
-      for (int s = 0; s < NS; ++s)
+    for (int s = 0; s < NS; ++s)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (sc[s][j] != -INFINITY) gst(logit_out + (size_t)ld.slot(raw[s], j) * G + lr, sc[s][j]);
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    if (mx > m_run) {
-      const float corr = fexp2(m_run - mx);
-      l_part *= corr;
+      for (int j = 0; j < 4; ++j)
+        if (FULL || sc[s][j] != -INFINITY) gst(logit_out + (size_t)ld.slot(raw[s], j) * G + lr, sc[s][j]);
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const bool up = mx > m_run;
+  if (__any(up)) {  // wave-uniform: rescale with factor 1 for the heads whose max held
+    const float corr = up ? fexp2(m_run - mx) : 1.f;
+    l_part *= corr;
 #pragma unroll
-      for (int m = 0; m < MG<D>::NM; ++m) O[m] *= corr;
+    for (int m = 0; m < MG<D>::NM; ++m) O[m] *= corr;
+    if (up) {
       m_run = mx;
       ld.track_max(m_run);
     }
+  }
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      float p[4], pp[4];
-      int valid_mask = 0;
+  for (int s = 0; s < NS; ++s) {
+    float p[4], pp[4];
+    int valid_mask = 0xF;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        p[j] = sc[s][j] == -INFINITY ? 0.f : fexp2(sc[s][j] - m_run);
-        valid_mask |= (sc[s][j] != -INFINITY) << j;
-        l_part += p[j];
+    for (int j = 0; j < 4; ++j) {
+      p[j] = fexp2(sc[s][j] - m_run);  // 0 for a masked token
+      l_part += p[j];
+      pp[j] = p[j] * ld.vscale(raw[s], j);
+      if (!FULL) {
         // slots past the count may hold any bits: their scale must not reach the product
-        pp[j] = sc[s][j] == -INFINITY ? 0.f : p[j] * ld.vscale(raw[s], j);
+        const bool ok = sc[s][j] != -INFINITY;
+        pp[j] = ok ? pp[j] : 0.f;
+        valid_mask &= ~((ok ? 0 : 1) << j);
       }
-      ld.vfix(raw[s], p, pp, valid_mask);
-      ld.pv(raw[s], pp, O);
     }
+    ld.vfix(raw[s], p, pp, valid_mask);
+    ld.pv(raw[s], pp, O);
+  }
+}
+
+// One wave over tokens [a, b) of its tile.  m_run / l_part belong to this lane's query head
+// (column lr); O holds this lane's part of O^T.
+template <int D, int G, class L>
+MKV_DEV void wave_mfma(L &ld, int a, int b, const QB<D> &qb, float qscale, float &m_run, float &l_part,
+                       f4v (&O)[MG<D>::NM], float *logit_out) {
+  if (a >= b) return;
+  typename L::Carry cy;
+  ld.carry(a, b, cy);
+  for (int base = a; base < b; base += 16 * MG<D>::NS) {
+    if (base + 16 * MG<D>::NS <= b)
+      mfma_batch<true, D, G>(ld, base, b, cy, qb, qscale, m_run, l_part, O, logit_out);
+    else
+      mfma_batch<false, D, G>(ld, base, b, cy, qb, qscale, m_run, l_part, O, logit_out);
   }
 }
 
@@ -533,16 +609,16 @@ MKV_DEV WaveRange wave_range(int t0, int t1, int wave, int nw) {
   return {a, min(a + span, end)};
 }
 
-// Merge the waves' (max, sum, o) into the tile's partial; `vc` (or null) holds per-wave additive
-// terms of o, to be multiplied by vf[wave][head] to share that wave's max.
+// Merge the waves' (max, sum, o) into the tile's partial.  Wave w's values sit at
+// red + w * wstride as [G][D + 2].
 template <int D, int G, int NW>
-MKV_DEV void merge_waves(const float (*s_red)[G][D + 2], const float (*vc)[G][D], const float (*vf)[G],
-                         float *dst) {
+MKV_DEV void merge_waves(const float *red, int wstride, float *dst) {
+  auto at = [&](int w, int g, int c) { return red[w * wstride + g * (D + 2) + c]; };
   for (int e = threadIdx.x; e < G * (D + 2); e += kTileThreads) {
     const int g = e / (D + 2), c = e % (D + 2);
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, s_red[w][g][0]);
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, at(w, g, 0));
     float val;
     if (M == -INFINITY) {
       val = (c == 0) ? -INFINITY : 0.f;
@@ -552,10 +628,8 @@ MKV_DEV void merge_waves(const float (*s_red)[G][D + 2], const float (*vc)[G][D]
       val = 0.f;
 #pragma unroll
       for (int w = 0; w < NW; ++w) {
-        if (s_red[w][g][0] == -INFINITY) continue;
-        float x = s_red[w][g][c];
-        if (vc != nullptr && c >= 2) x += vc[w][g][c - 2] * vf[w][g];
-        val += x * exp2f(s_red[w][g][0] - M);
+        if (at(w, g, 0) == -INFINITY) continue;
+        val += at(w, g, c) * exp2f(at(w, g, 0) - M);
       }
     }
     dst[e] = val;
@@ -568,13 +642,15 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     const uint16_t *__restrict__ q, float *__restrict__ partials, const float *__restrict__ cbtab,
     int Hkv, float qscale, int tile_base) {
   constexpr int NW = kTileThreads / 64, NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
-  __shared__ float s_red[NW][G][D + 2];
-  __shared__ float s_vc[NW][G][D];           // KVQuant value-outlier corrections, per wave
-  __shared__ float s_q[D][2 * G];            // KVQuant: q of each head, then q * tau
+  // per wave: KVQuant value-outlier terms, one row of D per (lane quad, head) while the wave
+  // runs; then the wave's (max, sum, o) for the merge
+  constexpr int kWaveFloats = 4 * G * D;
+  static_assert(kWaveFloats >= G * (D + 2), "wave region too small");
+  __shared__ __attribute__((aligned(16))) float s_wave[NW][kWaveFloats];
+  __shared__ float s_q[D][2 * G];            // KVQuant: scaled q of each head, then scaled q * tau
   __shared__ uint32_t s_lut[2][256];         // KVQuant: key and value pair tables
   __shared__ float s_cb[2][16];              // KVQuant: codebooks
-  __shared__ float s_kc[NW][G][32];          // KVQuant key-outlier logit terms, per wave
-  __shared__ float s_vf[NW][G];              // KVQuant: factor of each wave's s_vc
+  __shared__ __attribute__((aligned(16))) float s_kc[NW][G][32];  // KVQuant key-outlier logit terms
 
   const int tid = tile_base + blockIdx.x;
   const int4 tile = tiles[tid];
@@ -605,16 +681,16 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     const float *tau = reinterpret_cast<const float *>(sd.kmeta) + (size_t)h * D * 2;
     for (int e = threadIdx.x; e < G * D; e += kTileThreads) {
       const int g = e / D, c = e % D;
-      const float qx = h2f(qh[(size_t)g * D + c]);
+      const float qx = h2f(qh[(size_t)g * D + c]) * qscale;
       s_q[c][g] = qx;
       s_q[c][G + g] = qx * gld(tau + 2 * c);
     }
-    for (int e = lane; e < G * D; e += 64) (&s_vc[wave][0][0])[e] = 0.f;
-    for (int e = lane; e < G * 32; e += 64) (&s_kc[wave][0][0])[e] = 0.f;
+    float4 *vz = reinterpret_cast<float4 *>(&s_wave[wave][0]);
+    for (int e = lane; e < kWaveFloats / 4; e += 64) vz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
   __syncthreads();
-  // q.k operand B: query head lr, channels CPL*lq + 4m .. +3 (KVQuant: fp16 part of q' in
-  // columns 0..G-1, its residual in columns G..2G-1)
+  // q.k operand B: query head lr, channels CPL*lq + 4m .. +3 (KVQuant: fp16 part of the scaled
+  // q' in columns g < G, its residual in columns 2G-1-g)
   QB<D> qb;
 #pragma unroll
   for (int m = 0; m < NM; ++m) {
@@ -622,7 +698,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     const int c = CPL * lq + 4 * m;
     if (kvq) {
       if (lr < 2 * G) {
-        const int g = lr < G ? lr : lr - G;
+        const int g = lr < G ? lr : 2 * G - 1 - lr;
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
           const float x0 = s_q[c + 2 * j][G + g], x1 = s_q[c + 2 * j + 1][G + g];
@@ -674,7 +750,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
       ld.cbv = s_cb[1];
       ld.qq = &s_q[0][0];
       ld.kcorr = &s_kc[wave][0][0];
-      ld.vcorr = &s_vc[wave][0][0];
+      ld.vcorr = &s_wave[wave][(lq * G + (lr < G ? lr : 0)) * D];
       ld.lr = lr;
       ld.lq = lq;
       ld.rowbytes = sd.rowbytes;
@@ -684,34 +760,51 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
       ld.vref = -INFINITY;
       ld.vscl = 1.f;
       wave_mfma<D, G>(ld, wr.a, wr.b, qb, qscale, m_run, l_part, O, nullptr);
-      if (lr < G && lq == 0) s_vf[wave][lr] = ld.vfactor(m_run);
+      // fold the value-outlier rows of head lr (one per lane quad) into this lane's channels
+      if (lr < G) {
+        const float f = ld.vfactor(m_run);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+          for (int m = 0; m < NM; ++m) {
+            const int c = VPL * (4 * lq + i) + m;
+            float v = 0.f;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) v += s_wave[wave][(k * G + lr) * D + c];
+            O[m][i] += v * f;
+          }
+        }
+      }
     };
     if (sd.bits == 4) run(std::integral_constant<int, 4>{});
     else if (sd.bits == 3) run(std::integral_constant<int, 3>{});
     else run(std::integral_constant<int, 2>{});
   }
-  // KVQuant: column lr + G holds the products of head lr's p residual
+  // KVQuant: column 2G-1-lr holds the products of head lr's p residual
   if (kvq) {
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) O[m][i] += __shfl_xor(O[m][i], G);
+      for (int i = 0; i < 4; ++i) O[m][i] += mirror_cols<G>(O[m][i]);
   }
   // the 4 quads of a query head hold disjoint tokens
   l_part += __shfl_xor(l_part, 16);
   l_part += __shfl_xor(l_part, 32);
+  // this wave's (max, sum, o) over its own region (the outlier rows were folded above; a wave's
+  // LDS accesses complete in order)
+  float(*red)[D + 2] = reinterpret_cast<float(*)[D + 2]>(&s_wave[wave][0]);
   if (lr < G) {
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) s_red[wave][lr][2 + VPL * (4 * lq + i) + m] = O[m][i];
+      for (int i = 0; i < 4; ++i) red[lr][2 + VPL * (4 * lq + i) + m] = O[m][i];
     if (lq == 0) {
-      s_red[wave][lr][0] = m_run;
-      s_red[wave][lr][1] = l_part;
+      red[lr][0] = m_run;
+      red[lr][1] = l_part;
     }
   }
   __syncthreads();
-  merge_waves<D, G, NW>(s_red, kvq ? s_vc : nullptr, s_vf, partials + (size_t)tid * G * (D + 2));
+  merge_waves<D, G, NW>(&s_wave[0][0], kWaveFloats, partials + (size_t)tid * G * (D + 2));
 }
 
 template <int D, int G>
@@ -779,7 +872,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_uq(
     }
   }
   __syncthreads();
-  merge_waves<D, G, NW>(s_red, nullptr, nullptr, partials + (size_t)tid * G * (D + 2));
+  merge_waves<D, G, NW>(&s_red[0][0][0], G * (D + 2), partials + (size_t)tid * G * (D + 2));
 }
 
 // Log-sum-exp merge of one (sequence, kv head)'s tiles; H2O also adds every query head's
