@@ -10,7 +10,7 @@ configurations (seeded).  It is the only workload whose step runs every hot-path
 ~0.7 GB of compressed KV per step exceeds the 256 MB Infinity Cache, so it reads HBM.
 
 Also reported per configuration (``per_config``): the Llama-3-8B-shaped layer (8 seqs, prompt
-4096) under FP16 and KVQuant 4/3/2-bit, H2O-20 at prompt 8192, RocketKV-4096 at prompt 32768.
+4096) under FP16, uniform 4-bit and KVQuant 4/3/2-bit, H2O-20 at prompt 8192, RocketKV-4096 at prompt 32768.
 Their working sets fit in the Infinity Cache, so each runs R independent cache replicas in
 round-robin, R x bytes >= 512 MiB, and each step reads cold data.
 
@@ -169,15 +169,22 @@ def run_gpu(wl, steps, warmup, replicas=1, label=""):
             ms += a_ms
         kinds[kind] = (n, ms)
     n_tiles, n_uq = caches[0].n_tiles()
-    bytes_steps = [launch_bytes(wl, warmup + i, n_tiles - n_uq) for i in range(steps)]
+    # the partial kernel that carries most of the bytes: the fp16-row / KVQuant instantiation,
+    # unless the batch holds only uniform 4-bit sequences
+    part = "partial" if kinds["partial"][0] else "partial_uq"
+    ptiles = n_tiles - n_uq if part == "partial" else n_uq
+    pbytes = "mx" if part == "partial" else "uq"
+    bytes_steps = [launch_bytes(wl, warmup + i, ptiles, pbytes) for i in range(steps)]
     avg_bytes = float(np.mean(bytes_steps))
-    n_part, ms_part = kinds["partial"]
+    all_bytes = float(np.mean([launch_bytes(wl, warmup + i, n_tiles - n_uq, "mx") +
+                               launch_bytes(wl, warmup + i, n_uq, "uq") for i in range(steps)]))
+    n_part, ms_part = kinds[part]
     avg_part_ms = ms_part / max(n_part, 1)
     res = {
         "steps": steps, "ms_per_step": elapsed / steps * 1e3, "steps_per_s": steps / elapsed,
-        "partial_ms": avg_part_ms, "partial_bytes": avg_bytes,
+        "partial_kernel": part, "partial_ms": avg_part_ms, "partial_bytes": avg_bytes,
         "partial_gbs": avg_bytes / (avg_part_ms * 1e-3) / 1e9,
-        "step_gbs": avg_bytes / (elapsed / steps) / 1e9,
+        "step_gbs": all_bytes / (elapsed / steps) / 1e9,
         "n_tiles": n_tiles, "n_tiles_uq": n_uq, "replicas": replicas,
         "kernel_ms": {k: (v[1] / max(v[0], 1)) for k, v in kinds.items() if v[0]},
     }
@@ -191,8 +198,8 @@ def run_gpu(wl, steps, warmup, replicas=1, label=""):
 def per_config_runs(args):
     from workloads import make_workload
     runs = []
-    cases = [("llama_layer", "FP16"), ("llama_layer", "KVQ4"), ("llama_layer", "KVQ3"), ("llama_layer", "KVQ2"),
-             ("h2o", "H2O-20"), ("rocket", "Rocket-4096")]
+    cases = [("llama_layer", "FP16"), ("llama_layer", "UQ4-g64"), ("llama_layer", "KVQ4"), ("llama_layer", "KVQ3"),
+             ("llama_layer", "KVQ2"), ("h2o", "H2O-20"), ("rocket", "Rocket-4096")]
     for name, cfg in cases:
         wl = make_workload(name, seed=args.seed, config_ids=cfg)
         b1 = launch_bytes(wl, 0, 0, "mx") + launch_bytes(wl, 0, 0, "uq")
@@ -303,7 +310,7 @@ def main():
         "pct_of_peak_attention": round(100 * head["partial_gbs"] / PEAK_HBM_GBS, 1),
         "roofline": {"bound": "hbm", "achieved": round(head["partial_gbs"], 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(head["partial_gbs"] / PEAK_HBM_GBS, 4), "traffic": None,
-                     "kernel": "k_attn_partial", "bytes_per_launch": round(head["partial_bytes"]),
+                     "kernel": "k_attn_partial_mx<128, 4, false>", "bytes_per_launch": round(head["partial_bytes"]),
                      "avg_launch_us": round(head["partial_ms"] * 1e3, 2)},
         "kernel_us": {k: round(v * 1e3, 2) for k, v in head["kernel_ms"].items()},
         "per_config": per_cfg,

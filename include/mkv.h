@@ -231,9 +231,10 @@ mkv_status mkv_fit_codebooks(const uint16_t *k, const uint16_t *v, int32_t n_tok
  * `cache` is bracketed by HIP events on its stream (at most `max_launches`
  * per kind, pre-created here).  mkv_profile_read waits for them and returns,
  * for kernel kind `kind`, the launch count and the summed device time in
- * milliseconds.  Kinds: 0 attention partial (every method but uniform 4-bit),
- * 1 attention combine, 2 append, 3 top-k select, 4 H2O eviction,
- * 5 attention partial of uniform 4-bit sequences (launched only when there are any).
+ * milliseconds.  Kinds: 0 attention partial (every method but uniform 4-bit;
+ * launched only when there are such sequences), 1 attention combine, 2 append,
+ * 3 top-k select, 4 H2O eviction, 5 attention partial of uniform 4-bit
+ * sequences (launched only when there are any).
  */
 mkv_status mkv_profile_enable(mkv_cache *cache, int32_t enable, int32_t max_launches);
 mkv_status mkv_profile_read(mkv_cache *cache, int32_t kind, int32_t *launches, double *total_ms);

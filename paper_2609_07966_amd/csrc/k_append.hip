@@ -135,9 +135,10 @@ MKV_DEV int kvq_key_code(const SeqDesc &sd, int h, int c, uint32_t kbits, const 
   return code_from_mid(xhat, mid, nc - 1);
 }
 
-// UQ value row of one token: 64-channel groups, one wave per group.
+// UQ value of one token: 64-channel groups, one wave per group; returns this thread's code
+// (the caller places it in the token's 4-token block) and writes the group's (min, step).
 template <int D>
-MKV_DEV void uq_value_token(const SeqDesc &sd, int h, int t, uint32_t vbits) {
+MKV_DEV int uq_value_token(const SeqDesc &sd, int h, int t, uint32_t vbits) {
   const int c = threadIdx.x;
   const float x = h2f(vbits);
   const float mn = wave_min(x), mx = wave_max(x);
@@ -145,12 +146,23 @@ MKV_DEV void uq_value_token(const SeqDesc &sd, int h, int t, uint32_t vbits) {
   const float inv = r > 0.f ? __fdiv_rn(15.0f, r) : 0.f;
   const float y = __fmul_rn(__fsub_rn(x, mn), inv);
   const int code = (int)fminf(fmaxf(rintf(y), 0.f), 15.f);
-  const int partner = __shfl_down(code, 1);
-  uint8_t *row = reinterpret_cast<uint8_t *>(sd.vc) + h * stride_codes(sd) + (size_t)t * (D / 2);
-  if ((c & 1) == 0) row[c / 2] = (uint8_t)(code | (partner << 4));
   if ((c & 63) == 0)
     (reinterpret_cast<float2 *>(sd.vmeta) + h * stride_uq_vmeta(sd, D))[(size_t)t * (D / 64) + c / 64] =
         make_float2(mn, __fdiv_rn(r, 15.0f));
+  return code;
+}
+
+// OR a UQ value code into an LDS image of its 4-token block (nibbles never straddle words).
+MKV_DEV void or_uq_code(uint32_t *s_blk, int ch, int j, int code, int D) {
+  const int bit = uq_vbit(ch, j, D);
+  atomicOr(&s_blk[bit >> 5], (uint32_t)code << (bit & 31));
+}
+
+// Write a 4-token block (D/2 words) from an LDS image; t0 is the block's first slot.
+MKV_DEV void store_block(uint8_t *codes, int h_stride_bytes, int h, int t0, int rowbytes, const uint32_t *s_blk,
+                         int words) {
+  uint32_t *dst = reinterpret_cast<uint32_t *>(codes + (size_t)h * h_stride_bytes + (size_t)(t0 / 4) * 4 * rowbytes);
+  for (int w = threadIdx.x; w < words; w += blockDim.x) gst(dst + w, s_blk[w]);
 }
 
 // UQ key block: thread c quantizes channel c over 64 tokens read through `get(t)`.
@@ -226,7 +238,17 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
       break;
     }
     case UQ: {
-      uq_value_token<D>(sd, h, count, vb);
+      const int vcode = uq_value_token<D>(sd, h, count, vb);
+      // the value code goes into its 4-token block: zero for the block's first token, otherwise
+      // the stored block
+      const int j = count & 3, words = D / 2;
+      const uint32_t *blk = reinterpret_cast<const uint32_t *>(reinterpret_cast<const uint8_t *>(sd.vc) +
+                                                               h * stride_codes(sd) + (size_t)(count / 4) * 4 * sd.rowbytes);
+      for (int w = c; w < words; w += D) s_blk[w] = j == 0 ? 0u : gld(blk + w);
+      __syncthreads();
+      or_uq_code(s_blk, c, j, vcode, D);
+      __syncthreads();
+      store_block(reinterpret_cast<uint8_t *>(sd.vc), (int)stride_codes(sd), h, count & ~3, sd.rowbytes, s_blk, words);
       uint16_t *res = reinterpret_cast<uint16_t *>(sd.kres) + (size_t)h * 64 * D;
       res[(size_t)(count & 63) * D + c] = (uint16_t)kb;
       if ((count & 63) == 63) {
@@ -290,12 +312,22 @@ __global__ void k_prefill_copy(const uint16_t *__restrict__ k, const uint16_t *_
   *reinterpret_cast<uint4 *>(dv + h * head_stride + t * D + ch * 8) = b;
 }
 
+// UQ prompt values: one workgroup per (4-token block, kv head).
 template <int D>
 __global__ __launch_bounds__(128) void k_prefill_uq_values(const SeqDesc *__restrict__ seqs, int seq,
-                                                          const uint16_t *__restrict__ v, int Hkv) {
+                                                          const uint16_t *__restrict__ v, int Hkv, int n0) {
+  __shared__ uint32_t s_blk[D / 2];
   const SeqDesc &sd = seqs[seq];
-  const int t = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
-  uq_value_token<D>(sd, h, t, v[((size_t)t * Hkv + h) * D + c]);
+  const int q = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
+  for (int w = c; w < D / 2; w += D) s_blk[w] = 0;
+  __syncthreads();
+  for (int j = 0; j < 4 && 4 * q + j < n0; ++j) {
+    const int t = 4 * q + j;
+    const int code = uq_value_token<D>(sd, h, t, v[((size_t)t * Hkv + h) * D + c]);
+    or_uq_code(s_blk, c, j, code, D);
+  }
+  __syncthreads();
+  store_block(reinterpret_cast<uint8_t *>(sd.vc), (int)stride_codes(sd), h, 4 * q, sd.rowbytes, s_blk, D / 2);
 }
 
 template <int D>
@@ -463,7 +495,7 @@ hipError_t prefill_impl(const Dev &dv, const Shape &sh, const SeqDesc &hs, int s
       break;
     }
     case UQ:
-      hipLaunchKernelGGL(k_prefill_uq_values<D>, dim3(n0, Hkv), dim3(D), 0, st, dv.seqs, seq, v, Hkv);
+      hipLaunchKernelGGL(k_prefill_uq_values<D>, dim3((n0 + 3) / 4, Hkv), dim3(D), 0, st, dv.seqs, seq, v, Hkv, n0);
       hipLaunchKernelGGL(k_prefill_uq_keys<D>, dim3(n0 / 64 + 1, Hkv), dim3(D), 0, st, dv.seqs, seq, k, Hkv, n0);
       break;
     case KVQ:

@@ -85,6 +85,7 @@ struct QB {
 template <int D, int G, bool GATHER>
 struct MRows {
   static constexpr int NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
+  static constexpr int NS = MG<D>::NS;
   static constexpr bool kSplit = false;   // q and p enter as single fp16 parts
   static constexpr bool kScaled = false;  // logits still need the log2(e)/sqrt(d) factor
   const uint16_t *K, *V;
@@ -93,7 +94,6 @@ struct MRows {
   struct Raw {
     uint32_t kw[CPL / 2];
     uint32_t vw[4][VPL / 2];
-    int ks, vs[4];
   };
   struct Batch {};
   // Gather: the slots of the next batch, loaded one batch ahead so that row loads never wait
@@ -111,13 +111,13 @@ struct MRows {
       for (int j = 0; j < 4; ++j) cy.vs[s][j] = gld(sel + min(base + 16 * s + 4 * lq + j, b - 1));
     }
   }
-  MKV_DEV void load_rows(Raw &r) const {
-    const uint32_t *kp = reinterpret_cast<const uint32_t *>(K + (size_t)r.ks * D + CPL * lq);
+  MKV_DEV void load_rows(int ks, const int (&vs)[4], Raw &r) const {
+    const uint32_t *kp = reinterpret_cast<const uint32_t *>(K + (size_t)ks * D + CPL * lq);
 #pragma unroll
     for (int i = 0; i < CPL / 2; ++i) r.kw[i] = gld(kp + i);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint32_t *vp = reinterpret_cast<const uint32_t *>(V + (size_t)r.vs[j] * D + VPL * lr);
+      const uint32_t *vp = reinterpret_cast<const uint32_t *>(V + (size_t)vs[j] * D + VPL * lr);
 #pragma unroll
       for (int i = 0; i < VPL / 2; ++i) r.vw[j][i] = gld(vp + i);
     }
@@ -126,20 +126,22 @@ struct MRows {
   // last one
   template <bool FULL>
   MKV_DEV void fetch(int base, int b, int s, const Carry &cy, Raw &r) const {
+    int ks, vs[4];
     if (GATHER) {
-      r.ks = cy.ks[s];
+      ks = cy.ks[s];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) r.vs[j] = cy.vs[s][j];
+      for (int j = 0; j < 4; ++j) vs[j] = cy.vs[s][j];
     } else {
-      r.ks = FULL ? base + lr : min(base + lr, b - 1);
+      ks = FULL ? base + lr : min(base + lr, b - 1);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) r.vs[j] = FULL ? base + 4 * lq + j : min(base + 4 * lq + j, b - 1);
+      for (int j = 0; j < 4; ++j) vs[j] = FULL ? base + 4 * lq + j : min(base + 4 * lq + j, b - 1);
     }
-    load_rows(r);
+    load_rows(ks, vs, r);
   }
   MKV_DEV void batch_fetch(const Carry &, Batch &) const {}
   MKV_DEV void batch_fix(const Batch &) const {}
-  MKV_DEV int slot(const Raw &r, int j) const { return r.vs[j]; }
+  // slot of this lane's token j of the step at `base` (rows only: the logit store of H2O)
+  MKV_DEV int slot(int base, const Raw &, int j) const { return base + 4 * lq + j; }
   MKV_DEV void qk(const Raw &r, const QB<D> &qb, f4v &S) const {
 #pragma unroll
     for (int m = 0; m < NM; ++m) S = mfma16(mk_h4(r.kw[2 * m], r.kw[2 * m + 1]), qb.b[m], S);
@@ -148,7 +150,9 @@ struct MRows {
   MKV_DEV float vscale(const Raw &, int) const { return 1.f; }
   MKV_DEV void vfix(const Raw &, const float (&)[4], const float (&)[4], int) const {}
   MKV_DEV void track_max(float) {}
-  MKV_DEV void pv(const Raw &r, const float (&pp)[4], f4v (&O)[NM]) const {
+  MKV_DEV void prep(int, QB<D> &) {}
+  MKV_DEV void rescale(float) {}
+  MKV_DEV void pv(const Raw &r, const float (&)[4], const float (&pp)[4], int, f4v (&O)[NM]) const {
     const h4v P = mk_h4(pk_f16(pp[0], pp[1]), pk_f16(pp[2], pp[3]));
 #pragma unroll
     for (int m = 0; m < NM; ++m) {
@@ -167,6 +171,7 @@ struct MRows {
 template <int D, int G, int BITS>
 struct MKVQ {
   static constexpr int NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
+  static constexpr int NS = 2;           // 32-token batches (the key-outlier gather assumes 32)
   static constexpr bool kSplit = true;   // fp16 residuals of q' and p in columns G..2G-1
   static constexpr bool kScaled = true;  // q' carries log2(e)/sqrt(d)
   static constexpr int SEG = CPL * BITS;  // bits per lane segment (keys; values alike)
@@ -274,7 +279,7 @@ struct MKVQ {
       for (int g = 0; g < G; ++g) kcorr[g * 32 + lane] = acc[g];
     }
   }
-  MKV_DEV int slot(const Raw &r, int j) const { return r.t0 + j; }
+  MKV_DEV int slot(int, const Raw &r, int j) const { return r.t0 + j; }
   MKV_DEV void qk(const Raw &r, const QB<D> &qb, f4v &S) const {
 #pragma unroll
     for (int m = 0; m < NM; ++m)
@@ -332,7 +337,9 @@ struct MKVQ {
   }
   // factor that brings the terms to the final m_run (0 when there are none)
   MKV_DEV float vfactor(float m_run) const { return vref == -INFINITY ? 0.f : fexp2(vref - m_run); }
-  MKV_DEV void pv(const Raw &r, const float (&pp)[4], f4v (&O)[NM]) const {
+  MKV_DEV void prep(int, QB<D> &) {}
+  MKV_DEV void rescale(float) {}
+  MKV_DEV void pv(const Raw &r, const float (&)[4], const float (&pp)[4], int, f4v (&O)[NM]) const {
     uint32_t w[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -347,14 +354,199 @@ struct MKVQ {
   }
 };
 
+// The fp16 pair of p (or of p times a scale) for operand column lr: 0 its fp16 part, 1 the
+// rounding residual, 2 zero.
+MKV_DEV uint32_t p_pair(float a, float b, int role) {
+  const float ah = (float)(_Float16)a, bh = (float)(_Float16)b;
+  return role == 0 ? pk_f16(ah, bh) : role == 1 ? pk_f16(a - ah, b - bh) : 0u;
+}
+// the 4-bit nibbles k and k + 4 of w as a packed pair of fp16 integers: each becomes the fp16
+// value 1024 + n by an and-or, then n by one packed fp16 subtraction (both exact)
+MKV_DEV uint32_t nib_pair(uint32_t w, int k) {
+  const h2v x = __builtin_bit_cast(h2v, ((w >> (4 * k)) & 0x000F000Fu) | 0x64006400u);
+  const h2v off = {(_Float16)1024.0f, (_Float16)1024.0f};
+  return __builtin_bit_cast(uint32_t, x - off);
+}
+
+// Uniform 4-bit (64-token key blocks with per-channel min and step; per-token value groups of
+// 64 channels with min and step).  Codes n enter the matrix cores as exact fp16 integers:
+// q.k = sum q'' n + sum q mn with q'' = q st, and p.v = sum p' n + sum p mn with p' = p st,
+// the second terms kept per head (keys: per block; values: per value group).  A lane's 8 key channels of one code
+// word enter in the order {0,4,1,5} and {2,6,3,7} (two nibble pairs per and-or); value codes
+// are stored in the operand order (uq_vbit).  RES: the current incomplete block, whose keys
+// are fp16 rows (same channel order, q'' = q).
+template <int D, int G, bool RES>
+struct MUQ {
+  static constexpr int NM = MG<D>::NM, CPL = MG<D>::CPL;
+  static constexpr int NGRP = D / 64;     // value groups
+  static constexpr int KW = RES ? CPL / 2 : CPL / 8;  // key words per lane and step
+  static constexpr int NS = RES ? 1 : 2;  // the fp16 block (at most 63 tokens) in 16-token batches
+  static constexpr bool kSplit = true;    // fp16 residuals of q'' and p' in columns G..2G-1
+  static constexpr bool kScaled = true;   // q'' carries log2(e)/sqrt(d)
+  const uint8_t *kc, *vc;
+  const float *kmeta, *vmeta;             // float2 pairs (min, step)
+  const uint16_t *kres;
+  const float *qs;                        // LDS [D][2G]: scaled q in columns 0..G-1
+  float2 *vm;                             // LDS [32 * NGRP]: this wave's batch of value (min, step)
+  float *km;                              // LDS [D][2]: this wave's key block (min, step) pairs
+  int lr, lq, prole, cur_blk;
+  float kbias;                            // sum q mn of head lr for the current block
+  float om[NGRP];                         // sum p mn of head lr per value group
+  struct Raw {
+    uint32_t kw[KW];
+    uint32_t vw[NM / 2];
+    int t0;  // first slot of this lane's 4-token value block
+  };
+  struct Batch {
+    float mn, st;
+  };
+  struct Carry {};
+  MKV_DEV void carry(int, int, Carry &) const {}
+  // the batch's value (min, step) pairs, one per lane (slot base + l / NGRP, group l % NGRP),
+  // staged in LDS for the p.v step (slots past the end re-read the last one)
+  int bbase, bend;
+  MKV_DEV void batch_fetch(const Carry &, Batch &bt) const {
+    const int l = threadIdx.x & 63;
+    const int t = min(bbase + l / NGRP, bend - 1);
+    const float *mp = vmeta + ((size_t)t * NGRP + l % NGRP) * 2;
+    bt.mn = l < 16 * NS * NGRP ? gld(mp) : 0.f;
+    bt.st = l < 16 * NS * NGRP ? gld(mp + 1) : 0.f;
+  }
+  MKV_DEV void batch_fix(const Batch &bt) const {
+    const int l = threadIdx.x & 63;
+    if (l < 16 * NS * NGRP) vm[l] = make_float2(bt.mn, bt.st);
+  }
+  MKV_DEV int slot(int, const Raw &, int) const { return 0; }
+  // offset, from the lane's first key channel CPL*lq, of element j of key operand m
+  static constexpr int kofs(int m, int j) { return 8 * (m >> 1) + ((m & 1) ? 2 : 0) + ((j & 1) ? 4 : 0) + (j >> 1); }
+  // rebuild the key operand B (and sum q mn) when the batch enters a new block
+  MKV_DEV void prep(int base, QB<D> &qb) {
+    bbase = base;
+    const int blk = RES ? -2 : base >> 6;
+    if (blk == cur_blk) return;
+    cur_blk = blk;
+    if (!RES) {
+      // stage the block's (min, step) pairs: lane l takes channels 2l and 2l + 1
+      const int l = threadIdx.x & 63;
+      if (l < D / 2) {
+        const U4 u = gld16u(kmeta + ((size_t)blk * D + 2 * l) * 2);
+        float4 *dst = reinterpret_cast<float4 *>(km + 4 * l);
+        *dst = make_float4(__builtin_bit_cast(float, u.x), __builtin_bit_cast(float, u.y),
+                           __builtin_bit_cast(float, u.z), __builtin_bit_cast(float, u.w));
+      }
+    }
+    // the head whose part this column carries (columns >= 2G: any head, the operand is zero)
+    const int g = lr < G ? lr : lr < 2 * G ? 2 * G - 1 - lr : 0;
+    const float *qrow = qs + CPL * lq * 2 * G + g;  // q of channel CPL*lq + d at qrow[d * 2G]
+    const float *krw = km + 2 * CPL * lq;           // (min, step) of that channel at krw[2d]
+    float bias = 0.f;
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      uint32_t w[2];
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        float hv[2], rv[2];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int d = kofs(m, 2 * h2 + e);
+          const float q = qrow[d * 2 * G];
+          float x = q;
+          if (!RES) {
+            x = q * krw[2 * d + 1];
+            bias += q * krw[2 * d];
+          }
+          hv[e] = (float)(_Float16)x;
+          rv[e] = (float)(_Float16)(x - hv[e]);
+        }
+        const uint32_t ph = pk_f16(hv[0], hv[1]), pr = pk_f16(rv[0], rv[1]);
+        w[h2] = prole == 0 ? ph : prole == 1 ? pr : 0u;
+      }
+      qb.b[m] = mk_h4(w[0], w[1]);
+    }
+    bias += __shfl_xor(bias, 16);
+    bias += __shfl_xor(bias, 32);
+    kbias = lr < G ? bias : 0.f;
+  }
+  template <bool FULL>
+  MKV_DEV void fetch(int base, int b, int, const Carry &, Raw &r) const {
+    const int tk = FULL ? base + lr : min(base + lr, b - 1);
+    if (RES) {
+      const uint32_t *kp = reinterpret_cast<const uint32_t *>(kres + (size_t)(tk & 63) * D + CPL * lq);
+#pragma unroll
+      for (int i = 0; i < KW; ++i) r.kw[i] = gld(kp + i);
+    } else {
+      const uint32_t *kp = reinterpret_cast<const uint32_t *>(kc + (size_t)tk * (D / 2) + CPL * lq / 2);
+#pragma unroll
+      for (int i = 0; i < KW; ++i) r.kw[i] = gld(kp + i);
+    }
+    // the 4-token value block of this lane's tokens (past the end: the last block, whose slots
+    // all lie below the capacity, a multiple of 4)
+    const int t0 = FULL ? base + 4 * lq : min(base + 4 * lq, (b - 1) & ~3);
+    r.t0 = t0;
+    const uint32_t *vp = reinterpret_cast<const uint32_t *>(vc + (size_t)t0 * (D / 2) + lr * (D / 8));
+#pragma unroll
+    for (int i = 0; i < NM / 2; ++i) r.vw[i] = gld(vp + i);
+  }
+  MKV_DEV void qk(const Raw &r, const QB<D> &qb, f4v &S) const {
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      h4v a;
+      if (RES) {
+        const int u = m >> 1, o = (m & 1) ? 1 : 0;
+        const uint32_t wa = r.kw[4 * u + o], wb = r.kw[4 * u + 2 + o];  // channel pairs (0|2, 1|3), (4|6, 5|7)
+        a = mk_h4(pk_lo(wa, wb), pk_hi(wa, wb));
+      } else {
+        const uint32_t w = r.kw[m >> 1];
+        a = (m & 1) ? mk_h4(nib_pair(w, 2), nib_pair(w, 3)) : mk_h4(nib_pair(w, 0), nib_pair(w, 1));
+      }
+      S = mfma16(a, qb.b[m], S);
+    }
+  }
+  MKV_DEV void kfix(int, float (&x)[4]) const {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) x[j] += kbias;
+  }
+  MKV_DEV float vscale(const Raw &, int) const { return 1.f; }
+  MKV_DEV void vfix(const Raw &, const float (&)[4], const float (&)[4], int) const {}
+  MKV_DEV void track_max(float) {}
+  MKV_DEV void rescale(float corr) {
+#pragma unroll
+    for (int gr = 0; gr < NGRP; ++gr) om[gr] *= corr;
+  }
+  MKV_DEV void pv(const Raw &r, const float (&p)[4], const float (&)[4], int valid_mask, f4v (&O)[NM]) {
+    // this lane's 4 slots r.t0 .. r.t0 + 3 within the staged batch (clamped like the loads)
+    const int k0 = min(r.t0 - bbase, 16 * NS - 4);
+#pragma unroll
+    for (int gr = 0; gr < NGRP; ++gr) {
+      float pp[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        // slots past the count may hold any bits: masked tokens contribute nothing
+        const bool ok = (valid_mask >> j) & 1;
+        const float2 ms = vm[(k0 + j) * NGRP + gr];
+        pp[j] = ok ? p[j] * ms.y : 0.f;
+        om[gr] += ok ? p[j] * ms.x : 0.f;
+      }
+      const h4v P = mk_h4(p_pair(pp[0], pp[1], prole), p_pair(pp[2], pp[3], prole));
+#pragma unroll
+      for (int m = 4 * gr; m < 4 * gr + 4 && m < NM; ++m) {
+        const uint32_t w = r.vw[m >> 1];
+        const h4v a = (m & 1) ? mk_h4(nib_pair(w, 2), nib_pair(w, 3)) : mk_h4(nib_pair(w, 0), nib_pair(w, 1));
+        O[m] = mfma16(a, P, O[m]);
+      }
+    }
+  }
+};
+
 // One 32-token batch of a wave.  FULL: all 32 tokens exist (no clamping, no masks).
 template <bool FULL, int D, int G, class L>
-MKV_DEV void mfma_batch(L &ld, int base, int b, typename L::Carry &cy, const QB<D> &qb, float qscale,
+MKV_DEV void mfma_batch(L &ld, int base, int b, typename L::Carry &cy, QB<D> &qb, float qscale,
                         float &m_run, float &l_part, f4v (&O)[MG<D>::NM], float *logit_out) {
-  constexpr int NS = MG<D>::NS;
+  constexpr int NS = L::NS;
   const int lane = threadIdx.x & 63, lr = lane & 15, lq = lane >> 4;
   typename L::Raw raw[NS];
   typename L::Batch bt;
+  ld.prep(base, qb);
   // issue order: loads that depend on the carried indices first, then this batch's rows or
   // codes, then the next batch's indices
   ld.batch_fetch(cy, bt);
@@ -384,7 +576,7 @@ MKV_DEV void mfma_batch(L &ld, int base, int b, typename L::Carry &cy, const QB<
     for (int s = 0; s < NS; ++s)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        if (FULL || sc[s][j] != -INFINITY) gst(logit_out + (size_t)ld.slot(raw[s], j) * G + lr, sc[s][j]);
+        if (FULL || sc[s][j] != -INFINITY) gst(logit_out + (size_t)ld.slot(base + 16 * s, raw[s], j) * G + lr, sc[s][j]);
   }
   mx = fmaxf(mx, __shfl_xor(mx, 16));
   mx = fmaxf(mx, __shfl_xor(mx, 32));
@@ -394,6 +586,7 @@ MKV_DEV void mfma_batch(L &ld, int base, int b, typename L::Carry &cy, const QB<
     l_part *= corr;
 #pragma unroll
     for (int m = 0; m < MG<D>::NM; ++m) O[m] *= corr;
+    ld.rescale(corr);
     if (up) {
       m_run = mx;
       ld.track_max(m_run);
@@ -416,20 +609,20 @@ MKV_DEV void mfma_batch(L &ld, int base, int b, typename L::Carry &cy, const QB<
       }
     }
     ld.vfix(raw[s], p, pp, valid_mask);
-    ld.pv(raw[s], pp, O);
+    ld.pv(raw[s], p, pp, valid_mask, O);
   }
 }
 
 // One wave over tokens [a, b) of its tile.  m_run / l_part belong to this lane's query head
 // (column lr); O holds this lane's part of O^T.
 template <int D, int G, class L>
-MKV_DEV void wave_mfma(L &ld, int a, int b, const QB<D> &qb, float qscale, float &m_run, float &l_part,
+MKV_DEV void wave_mfma(L &ld, int a, int b, QB<D> &qb, float qscale, float &m_run, float &l_part,
                        f4v (&O)[MG<D>::NM], float *logit_out) {
   if (a >= b) return;
   typename L::Carry cy;
   ld.carry(a, b, cy);
-  for (int base = a; base < b; base += 16 * MG<D>::NS) {
-    if (base + 16 * MG<D>::NS <= b)
+  for (int base = a; base < b; base += 16 * L::NS) {
+    if (base + 16 * L::NS <= b)
       mfma_batch<true, D, G>(ld, base, b, cy, qb, qscale, m_run, l_part, O, logit_out);
     else
       mfma_batch<false, D, G>(ld, base, b, cy, qb, qscale, m_run, l_part, O, logit_out);
@@ -437,166 +630,9 @@ MKV_DEV void wave_mfma(L &ld, int a, int b, const QB<D> &qb, float qscale, float
 }
 
 // ================================================================================================
-// Vector path (uniform 4-bit)
-// ================================================================================================
-template <int D, int G>
-struct Geo {
-  static constexpr int LPT = D / 8;      // lanes per token
-  static constexpr int TPW = 64 / LPT;   // tokens per wave load
-  static constexpr int BT = G > 4 ? 16 : 32;  // tokens per wave batch (all loads issued first)
-  static constexpr int U = BT / TPW;     // wave loads in flight per batch
-};
-
-template <int G>
-struct Qs {
-  uint32_t h[G][4];  // fp16 pairs of channels c0..c0+7, unscaled
-  float f[G][8];     // the same in fp32
-};
-
-// Uniform 4-bit: k = mn_c + code * st_c per (64-token block, channel), so q . k = sum q mn +
-// sum (q st) code with both per-block factors prepared once per block; v = mn_t + code * st_t
-// per (token, 64 channels), so p v = p mn + (p st) code, with sum p mn kept per head (`om`).
-template <int D, int G>
-struct LdUQ {
-  const uint8_t *kc, *vc;
-  const float2 *kmeta, *vmeta;
-  const uint16_t *kres;
-  int c0, full, cur_blk;
-  float qs[G][8], qm[G];
-  float om[G];  // sum over tokens of p * mn, rescaled with o and added to it at the end
-  struct Raw { uint32_t kw, vw, k0, k1, k2, k3; float vmn, vst; bool quant; };
-  MKV_DEV void rescale(int g, float corr) { om[g] *= corr; }
-  MKV_DEV void finish(float (&o)[G][8]) const {
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o[g][i] += om[g];
-  }
-  MKV_DEV void prep(int base, const Qs<G> &q) {
-    const int blk = base >> 6;
-    if (blk == cur_blk) return;
-    cur_blk = blk;
-    if (blk * 64 < full) {
-#pragma unroll
-      for (int g = 0; g < G; ++g) qm[g] = 0.f;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float *mp = reinterpret_cast<const float *>(kmeta + (size_t)blk * D + c0 + i);
-        const float mn = gld(mp), stp = gld(mp + 1);
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-          qs[g][i] = q.f[g][i] * stp;
-          qm[g] = fmaf(q.f[g][i], mn, qm[g]);
-        }
-      }
-    }
-  }
-  MKV_DEV void fetch(int t, Raw &r) const {
-    r.quant = t < full;
-    r.kw = 0;
-    r.k0 = r.k1 = r.k2 = r.k3 = 0;
-    if (r.quant) {
-      r.kw = gld(reinterpret_cast<const uint32_t *>(kc + (size_t)t * (D / 2) + c0 / 2));
-    } else {
-      const uint32_t *kr = reinterpret_cast<const uint32_t *>(kres + (size_t)(t & 63) * D + c0);
-      r.k0 = gld(kr);
-      r.k1 = gld(kr + 1);
-      r.k2 = gld(kr + 2);
-      r.k3 = gld(kr + 3);
-    }
-    r.vw = gld(reinterpret_cast<const uint32_t *>(vc + (size_t)t * (D / 2) + c0 / 2));
-    const float *mp = reinterpret_cast<const float *>(vmeta + (size_t)t * (D / 64) + c0 / 64);
-    r.vmn = gld(mp);
-    r.vst = gld(mp + 1);
-  }
-  MKV_DEV void dot(const Raw &r, const Qs<G> &q, float (&part)[G]) const {
-    if (r.quant) {
-      float cf[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) cf[i] = (float)((r.kw >> (4 * i)) & 15u);
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        float acc = qm[g];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc = fmaf(qs[g][i], cf[i], acc);
-        part[g] = acc;
-      }
-    } else {
-#pragma unroll
-      for (int g = 0; g < G; ++g)
-        part[g] = dot2(q.h[g][3], r.k3, dot2(q.h[g][2], r.k2, dot2(q.h[g][1], r.k1, dot2(q.h[g][0], r.k0, 0.f))));
-    }
-  }
-  MKV_DEV void pv(const Raw &r, const float (&p)[G], float (&o)[G][8]) {
-    float cf[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) cf[i] = (float)((r.vw >> (4 * i)) & 15u);
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      om[g] = fmaf(p[g], r.vmn, om[g]);
-      const float ps = p[g] * r.vst;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o[g][i] = fmaf(ps, cf[i], o[g][i]);
-    }
-  }
-};
-
-// Run one wave over tokens [a, b) of its tile.
-template <int D, int G, class L>
-MKV_DEV void wave_attend(L &ld, int a, int b, const Qs<G> &q, float qscale, float (&m_run)[G], float (&l)[G],
-                         float (&o)[G][8], int grp) {
-  constexpr int LPT = Geo<D, G>::LPT, TPW = Geo<D, G>::TPW, U = Geo<D, G>::U;
-  for (int base = a; base < b; base += U * TPW) {
-    ld.prep(base, q);
-    // every lane loads; a lane past the end of the range re-reads the range's last token, whose
-    // weight below is exactly 0 (no divergent branches around the loads)
-    typename L::Raw raw[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) ld.fetch(min(base + u * TPW + grp, b - 1), raw[u]);
-    float s[U][G];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const bool valid = base + u * TPW + grp < b;
-      float part[G];
-      ld.dot(raw[u], q, part);
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const float x = group_sum<LPT>(part[g]) * qscale;
-        s[u][g] = valid ? x : -INFINITY;
-      }
-    }
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      float mx = s[0][g];
-#pragma unroll
-      for (int u = 1; u < U; ++u) mx = fmaxf(mx, s[u][g]);
-#pragma unroll
-      for (int m = LPT; m < 64; m <<= 1) mx = fmaxf(mx, __shfl_xor(mx, m));
-      if (mx > m_run[g]) {
-        const float corr = fexp2(m_run[g] - mx);
-        l[g] *= corr;
-        ld.rescale(g, corr);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) o[g][i] *= corr;
-        m_run[g] = mx;
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      float p[G];
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        p[g] = s[u][g] == -INFINITY ? 0.f : fexp2(s[u][g] - m_run[g]);
-        l[g] += p[g];
-      }
-      ld.pv(raw[u], p, o);
-    }
-  }
-}
-
-// ================================================================================================
-// The partial kernels: one over the tiles of matrix-path sequences, one over the uniform 4-bit
-// ones (kept apart so that neither's register budget limits the other's occupancy).
+// The partial kernel, instantiated twice: UQK = false for fp16 rows, gathered rows and KVQuant,
+// UQK = true for uniform 4-bit tiles (kept apart so that neither's register budget limits the
+// other's occupancy).
 // ================================================================================================
 // Contiguous token range [a, b) of this wave within its tile, a multiple of 32 tokens.
 struct WaveRange {
@@ -636,7 +672,7 @@ MKV_DEV void merge_waves(const float *red, int wstride, float *dst) {
   }
 }
 
-template <int D, int G>
+template <int D, int G, bool UQK>
 __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     const SeqDesc *__restrict__ seqs, const int32_t *__restrict__ state, const int4 *__restrict__ tiles,
     const uint16_t *__restrict__ q, float *__restrict__ partials, const float *__restrict__ cbtab,
@@ -644,13 +680,15 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   constexpr int NW = kTileThreads / 64, NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
   // per wave: KVQuant value-outlier terms, one row of D per (lane quad, head) while the wave
   // runs; then the wave's (max, sum, o) for the merge
-  constexpr int kWaveFloats = 4 * G * D;
+  constexpr int kWaveFloats = UQK ? G * (D + 2) : 4 * G * D;
   static_assert(kWaveFloats >= G * (D + 2), "wave region too small");
   __shared__ __attribute__((aligned(16))) float s_wave[NW][kWaveFloats];
   __shared__ float s_q[D][2 * G];            // KVQuant: scaled q of each head, then scaled q * tau
   __shared__ uint32_t s_lut[2][256];         // KVQuant: key and value pair tables
   __shared__ float s_cb[2][16];              // KVQuant: codebooks
   __shared__ __attribute__((aligned(16))) float s_kc[NW][G][32];  // KVQuant key-outlier logit terms
+  __shared__ float2 s_vm[NW][64];            // uniform 4-bit: a batch's value (min, step) pairs
+  __shared__ __attribute__((aligned(16))) float s_km[NW][2 * D];  // uniform 4-bit: a key block's pairs
 
   const int tid = tile_base + blockIdx.x;
   const int4 tile = tiles[tid];
@@ -664,7 +702,14 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   const uint16_t *qh = q + ((size_t)seq * Hq + h * G) * D;
   const WaveRange wr = wave_range(tile.z, min(tile.w, n_act), wave, NW);
   const int lr = lane & 15, lq = lane >> 4;
-  const bool kvq = method == KVQ;
+  const bool kvq = !UQK && method == KVQ;
+  constexpr bool uq = UQK;
+  if constexpr (uq) {
+    for (int e = threadIdx.x; e < G * D; e += kTileThreads) {
+      const int g = e / D, c = e % D;
+      s_q[c][g] = h2f(qh[(size_t)g * D + c]) * qscale;
+    }
+  }
   if (kvq) {
     // codebook tables and q, q * tau for this kv head
     const int bits = sd.bits, nc = 1 << bits;
@@ -714,10 +759,52 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     qb.b[m] = mk_h4(w[0], w[1]);
   }
   float m_run = -INFINITY, l_part = 0.f;
+  float uq_om[D / 64];  // uniform 4-bit: sum p mn per value group (summed over the lane quads)
   f4v O[NM];
 #pragma unroll
   for (int m = 0; m < NM; ++m) O[m] = f4v{0.f, 0.f, 0.f, 0.f};
-  if (method == FP16 || method == H2O) {
+  auto run_uq = [&]() {
+    // the complete 64-token blocks, then the incomplete block's fp16 keys (a batch never spans
+    // both: ranges start at multiples of 32)
+    const int full = (st[ST_COUNT] / 64) * 64;
+    auto init = [&](auto &ld) {
+      ld.kc = reinterpret_cast<const uint8_t *>(sd.kc) + h * stride_codes(sd);
+      ld.vc = reinterpret_cast<const uint8_t *>(sd.vc) + h * stride_codes(sd);
+      ld.kmeta = reinterpret_cast<const float *>(sd.kmeta) + h * stride_uq_kmeta(sd, D) * 2;
+      ld.vmeta = reinterpret_cast<const float *>(sd.vmeta) + h * stride_uq_vmeta(sd, D) * 2;
+      ld.kres = reinterpret_cast<const uint16_t *>(sd.kres) + (size_t)h * 64 * D;
+      ld.qs = &s_q[0][0];
+      ld.vm = s_vm[wave];
+      ld.km = s_km[wave];
+      ld.lr = lr;
+      ld.lq = lq;
+      ld.prole = lr < G ? 0 : lr < 2 * G ? 1 : 2;
+      ld.cur_blk = -1;
+      ld.kbias = 0.f;
+    };
+    MUQ<D, G, false> lq_;
+    init(lq_);
+    lq_.bend = min(wr.b, full);
+#pragma unroll
+    for (int gr = 0; gr < D / 64; ++gr) lq_.om[gr] = 0.f;
+    wave_mfma<D, G>(lq_, wr.a, min(wr.b, full), qb, qscale, m_run, l_part, O, nullptr);
+    MUQ<D, G, true> lr_;
+    init(lr_);
+    lr_.bend = wr.b;
+#pragma unroll
+    for (int gr = 0; gr < D / 64; ++gr) lr_.om[gr] = lq_.om[gr];
+    wave_mfma<D, G>(lr_, max(wr.a, full), wr.b, qb, qscale, m_run, l_part, O, nullptr);
+#pragma unroll
+    for (int gr = 0; gr < D / 64; ++gr) {
+      float v = lr_.om[gr];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      uq_om[gr] = v;
+    }
+  };
+  if constexpr (UQK) {
+    run_uq();
+  } else if (method == FP16 || method == H2O) {
     MRows<D, G, false> ld;
     ld.K = reinterpret_cast<const uint16_t *>(sd.k) + h * stride_rows(sd, D);
     ld.V = reinterpret_cast<const uint16_t *>(sd.v) + h * stride_rows(sd, D);
@@ -780,12 +867,18 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     else if (sd.bits == 3) run(std::integral_constant<int, 3>{});
     else run(std::integral_constant<int, 2>{});
   }
-  // KVQuant: column 2G-1-lr holds the products of head lr's p residual
-  if (kvq) {
+  // KVQuant, uniform 4-bit: column 2G-1-lr holds the products of head lr's p residual
+  if (kvq || uq) {
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
       for (int i = 0; i < 4; ++i) O[m][i] += mirror_cols<G>(O[m][i]);
+  }
+  if constexpr (uq) {
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) O[m][i] += uq_om[m / 4];
   }
   // the 4 quads of a query head hold disjoint tokens
   l_part += __shfl_xor(l_part, 16);
@@ -794,10 +887,13 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   // LDS accesses complete in order)
   float(*red)[D + 2] = reinterpret_cast<float(*)[D + 2]>(&s_wave[wave][0]);
   if (lr < G) {
+    // O^T row 4 lq + i of operand m: channel VPL (4 lq + i) + m; uniform 4-bit values use the
+    // group-aligned order 64 (m / 4) + 4 (4 lq + i) + m % 4
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) red[lr][2 + VPL * (4 * lq + i) + m] = O[m][i];
+      for (int i = 0; i < 4; ++i)
+        red[lr][2 + (uq ? 64 * (m / 4) + 4 * (4 * lq + i) + (m & 3) : VPL * (4 * lq + i) + m)] = O[m][i];
     if (lq == 0) {
       red[lr][0] = m_run;
       red[lr][1] = l_part;
@@ -805,74 +901,6 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   }
   __syncthreads();
   merge_waves<D, G, NW>(&s_wave[0][0], kWaveFloats, partials + (size_t)tid * G * (D + 2));
-}
-
-template <int D, int G>
-__global__ __launch_bounds__(kTileThreads) void k_attn_partial_uq(
-    const SeqDesc *__restrict__ seqs, const int32_t *__restrict__ state, const int4 *__restrict__ tiles,
-    const uint16_t *__restrict__ q, float *__restrict__ partials, int Hkv, float qscale, int tile_base) {
-  constexpr int NW = kTileThreads / 64, LPT = Geo<D, G>::LPT;
-  __shared__ float s_red[NW][G][D + 2];
-  const int tid = tile_base + blockIdx.x;
-  const int4 tile = tiles[tid];
-  const int seq = tile.x, h = tile.y;
-  const SeqDesc &sd = seqs[seq];
-  const int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint16_t *qh = q + ((size_t)seq * Hkv * G + h * G) * D;
-  const WaveRange wr = wave_range(tile.z, min(tile.w, st[ST_COUNT]), wave, NW);
-  const int grp = lane / LPT, sub = lane % LPT, c0 = sub * 8;
-  Qs<G> qv;
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const U4 u = gld16u(qh + (size_t)g * D + c0);
-    qv.h[g][0] = u.x; qv.h[g][1] = u.y; qv.h[g][2] = u.z; qv.h[g][3] = u.w;
-    unpack8(u, qv.f[g]);
-  }
-  float m_run[G], l[G], o[G][8];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    m_run[g] = -INFINITY;
-    l[g] = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) o[g][i] = 0.f;
-  }
-  LdUQ<D, G> ld;
-  ld.kc = reinterpret_cast<const uint8_t *>(sd.kc) + h * stride_codes(sd);
-  ld.vc = reinterpret_cast<const uint8_t *>(sd.vc) + h * stride_codes(sd);
-  ld.kmeta = reinterpret_cast<const float2 *>(sd.kmeta) + h * stride_uq_kmeta(sd, D);
-  ld.vmeta = reinterpret_cast<const float2 *>(sd.vmeta) + h * stride_uq_vmeta(sd, D);
-  ld.kres = reinterpret_cast<const uint16_t *>(sd.kres) + (size_t)h * 64 * D;
-  ld.c0 = c0;
-  ld.full = (st[ST_COUNT] / 64) * 64;
-  ld.cur_blk = -1;
-#pragma unroll
-  for (int g = 0; g < G; ++g) ld.om[g] = 0.f;
-  wave_attend<D, G>(ld, wr.a, wr.b, qv, qscale, m_run, l, o, grp);
-  ld.finish(o);
-  // reduce over the lane groups of the wave (they share m_run)
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-#pragma unroll
-    for (int m = LPT; m < 64; m <<= 1) {
-      l[g] += __shfl_xor(l[g], m);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o[g][i] += __shfl_xor(o[g][i], m);
-    }
-  }
-  if (grp == 0) {
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) s_red[wave][g][2 + c0 + i] = o[g][i];
-      if (sub == 0) {
-        s_red[wave][g][0] = m_run[g];
-        s_red[wave][g][1] = l[g];
-      }
-    }
-  }
-  __syncthreads();
-  merge_waves<D, G, NW>(&s_red[0][0][0], G * (D + 2), partials + (size_t)tid * G * (D + 2));
 }
 
 // Log-sum-exp merge of one (sequence, kv head)'s tiles; H2O also adds every query head's
@@ -975,11 +1003,11 @@ hipError_t partial_impl(const Dev &dv, const Shape &sh, const uint16_t *q, int p
   const float qscale = kLog2e / sqrtf((float)D);
   const int n_mx = dv.n_tiles - dv.n_tiles_uq;
   if (part == 0 && n_mx > 0)
-    hipLaunchKernelGGL((k_attn_partial_mx<D, G>), dim3(n_mx), dim3(kTileThreads), 0, st, dv.seqs, dv.state,
-                       dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale, 0);
+    hipLaunchKernelGGL((k_attn_partial_mx<D, G, false>), dim3(n_mx), dim3(kTileThreads), 0, st, dv.seqs,
+                       dv.state, dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale, 0);
   if (part == 1 && dv.n_tiles_uq > 0)
-    hipLaunchKernelGGL((k_attn_partial_uq<D, G>), dim3(dv.n_tiles_uq), dim3(kTileThreads), 0, st, dv.seqs,
-                       dv.state, dv.tiles, q, dv.partials, sh.Hkv, qscale, n_mx);
+    hipLaunchKernelGGL((k_attn_partial_mx<D, G, true>), dim3(dv.n_tiles_uq), dim3(kTileThreads), 0, st,
+                       dv.seqs, dv.state, dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale, n_mx);
   return hipGetLastError();
 }
 

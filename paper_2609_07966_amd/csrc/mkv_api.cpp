@@ -142,7 +142,7 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
         d.v = take(H * d.cap * D * 2);
         break;
       case UQ:
-        d.cap = n0 + mn;
+        d.cap = (n0 + mn + 3) & ~3;  // value codes are stored in 4-token blocks
         d.rowbytes = D / 2;
         d.nblk = d.cap / 64;
         d.kc = take(H * d.cap * d.rowbytes);
@@ -502,10 +502,13 @@ mkv_status mkv_decode_attention(mkv_cache *c, const uint16_t *q, float *out, voi
   if (!(c->phase == PH_SELECTED || (c->phase == PH_APPENDED && !c->any_rocket)))
     return fail(MKV_ESTATE, "attention must follow the decode append (and top-k selection)");
   hipStream_t hst = static_cast<hipStream_t>(stream);
-  prof_mark(c, 0, 0, hst);
-  hipError_t e = launch_attention_partial(c->dv, c->sh, q, 0, hst);
-  prof_mark(c, 0, 1, hst);
-  if (e != hipSuccess) return hip_fail(e, "attention partial");
+  hipError_t e = hipSuccess;
+  if (c->dv.n_tiles > c->dv.n_tiles_uq) {
+    prof_mark(c, 0, 0, hst);
+    e = launch_attention_partial(c->dv, c->sh, q, 0, hst);
+    prof_mark(c, 0, 1, hst);
+    if (e != hipSuccess) return hip_fail(e, "attention partial");
+  }
   if (c->dv.n_tiles_uq > 0) {
     prof_mark(c, 5, 0, hst);
     e = launch_attention_partial(c->dv, c->sh, q, 1, hst);
@@ -657,17 +660,19 @@ extern "C" mkv_status mkv_export(mkv_cache *c, int32_t seq, int32_t h, int32_t w
       const bool isk = what == MKV_EXPORT_CODES_K;
       const int n = (d.method == UQ && isk) ? (count / 64) * 64 : count;
       const int bits = d.method == UQ ? 4 : d.bits;
-      // KVQ values sit in 4-token blocks (code of channel c, token j at bit bits*(4c + j));
-      // every other code row is one token
-      const bool quad = d.method == KVQ && !isk;
+      // values sit in 4-token blocks: KVQ code of channel c, token j at bit bits*(4c + j); UQ as
+      // laid out by uq_vbit; key code rows are one token each
+      const bool quad = !isk;
       const size_t nbytes = (size_t)(quad ? (n + 3) & ~3 : n) * d.rowbytes;
       std::vector<uint8_t> raw;
       if ((st = dget(raw, (isk ? d.kc : d.vc) + (uint64_t)h * stride_codes(d), nbytes)) != MKV_OK) return st;
       for (int t = 0; t < n; ++t)
         for (int ch = 0; ch < D; ++ch) {
-          const uint8_t code = quad ? (uint8_t)unpack_bits(raw.data() + (size_t)(t / 4) * 4 * d.rowbytes,
-                                                           4 * ch + (t & 3), bits)
-                                    : (uint8_t)unpack_bits(raw.data() + (size_t)t * d.rowbytes, ch, bits);
+          const uint8_t *blk = raw.data() + (size_t)(t / 4) * 4 * d.rowbytes;
+          uint8_t code;
+          if (!quad) code = (uint8_t)unpack_bits(raw.data() + (size_t)t * d.rowbytes, ch, bits);
+          else if (d.method == KVQ) code = (uint8_t)unpack_bits(blk, 4 * ch + (t & 3), bits);
+          else code = (uint8_t)((blk[uq_vbit(ch, t & 3, D) >> 3] >> (uq_vbit(ch, t & 3, D) & 7)) & 15u);
           put(&code, 1);
         }
       break;

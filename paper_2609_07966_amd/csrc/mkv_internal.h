@@ -77,6 +77,17 @@ __host__ __device__ inline int64_t stride_stage(const SeqDesc &s, int D) { retur
 __host__ __device__ inline int64_t stride_sel(const SeqDesc &s) { return (int64_t)(s.topk > 0 ? s.topk : 1); }
 __host__ __device__ inline int64_t stride_kcm(const SeqDesc &s, int D) { return (int64_t)s.cstride * D; }
 
+// UQ value codes sit in 4-token blocks of 2*D bytes laid out for the attention's matrix
+// operands: 16 segments (one per operand row r) of D/16 codes x 4 tokens, 4 bits each.  Channel
+// ch belongs to row r = (ch % 64) / 4 and operand m = 4 * (ch / 64) + ch % 4; within the segment
+// operand m uses nibbles 2*(m%2) + {0, 4, 1, 5} of word m/2 for tokens 0..3 of the block.
+// Returns the bit offset of (ch, token j of the block) within the block.
+__host__ __device__ inline int uq_vbit(int ch, int j, int D) {
+  const int r = (ch & 63) >> 2, m = 4 * (ch >> 6) + (ch & 3);
+  const int nib = 2 * (m & 1) + ((j & 1) ? 4 : 0) + ((j >> 1) & 1);
+  return r * D + (m >> 1) * 32 + 4 * nib;  // a segment holds D bits
+}
+
 // Codebook table: for b = 2, 3, 4: cbK[2^b], cbV[2^b], midK[2^b-1], midV[2^b-1].
 __host__ __device__ inline int cb_offset(int bits) {
   // sizes: b=2: 4+4+3+3 = 14; b=3: 8+8+7+7 = 30; b=4: 16+16+15+15 = 62
