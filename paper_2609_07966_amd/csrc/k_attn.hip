@@ -904,51 +904,63 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
 }
 
 // Log-sum-exp merge of one (sequence, kv head)'s tiles; H2O also adds every query head's
-// probability to each retained token's accumulated score.
+// probability to each retained token's accumulated score.  One workgroup of 1024 threads per
+// pair: a wave per query head reduces the tile maxima and sums, a thread per output element
+// merges its tiles, and all threads share the score pass over the retained slots.
 constexpr int kMaxTilesPerPair = 64;
+constexpr int kCombineThreads = 1024;
 
 template <int D, int G>
-__global__ __launch_bounds__(256) void k_attn_combine(const SeqDesc *__restrict__ seqs,
-                                                      int32_t *__restrict__ state,
-                                                      const float *__restrict__ partials,
-                                                      float *__restrict__ out, int Hkv) {
+__global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc *__restrict__ seqs,
+                                                                  int32_t *__restrict__ state,
+                                                                  const float *__restrict__ partials,
+                                                                  float *__restrict__ out, int Hkv) {
+  static_assert(G * D <= kCombineThreads && G * 64 <= kCombineThreads, "one thread per output element");
+  constexpr int NWC = kCombineThreads / 64;
   __shared__ float sm[kMaxTilesPerPair][G];
   __shared__ float sl[kMaxTilesPerPair][G];
   __shared__ float sM[G], sL[G];
+  __shared__ unsigned long long s_best[NWC];
   const int seq = blockIdx.x / Hkv, h = blockIdx.x % Hkv;
   const SeqDesc &sd = seqs[seq];
   const int first = sd.tile_first + h * sd.tile_count, nt = sd.tile_count;
   const float *P = partials + (size_t)first * G * (D + 2);
-  for (int e = threadIdx.x; e < nt * G; e += 256) {
-    const int t = e / G, g = e % G;
+  const int wv = threadIdx.x >> 6, ln = threadIdx.x & 63;
+  if (threadIdx.x < nt * G) {
+    const int t = threadIdx.x / G, g = threadIdx.x % G;
     sm[t][g] = P[((size_t)t * G + g) * (D + 2)];
     sl[t][g] = P[((size_t)t * G + g) * (D + 2) + 1];
   }
   __syncthreads();
-  if (threadIdx.x < G) {
-    const int g = threadIdx.x;
-    float M = -INFINITY;
-    for (int t = 0; t < nt; ++t) M = fmaxf(M, sm[t][g]);
-    float L = 0.f;
-    for (int t = 0; t < nt; ++t)
-      if (sm[t][g] != -INFINITY) L += sl[t][g] * exp2f(sm[t][g] - M);
-    sM[g] = M;
-    sL[g] = L;
+  if (wv < G) {  // wave g: lane t takes tile t
+    const float m = ln < nt ? sm[ln][wv] : -INFINITY;
+    const float M = wave_max(m);
+    const float L = wave_sum(ln < nt && m != -INFINITY ? sl[ln][wv] * exp2f(m - M) : 0.f);
+    if (ln == 0) {
+      sM[wv] = M;
+      sL[wv] = L;
+    }
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < nt * G; e += 256) {
-    const int t = e / G, g = e % G;
+  if (threadIdx.x < nt * G) {
+    const int t = threadIdx.x / G, g = threadIdx.x % G;
     sm[t][g] = sm[t][g] == -INFINITY ? 0.f : exp2f(sm[t][g] - sM[g]) / sL[g];
   }
   __syncthreads();
   const int Hq = Hkv * G;
-  for (int e = threadIdx.x; e < G * D; e += 256) {
-    const int g = e / D, c = e % D;
-    float acc = 0.f;
+  if (threadIdx.x < G * D) {
+    const int g = threadIdx.x / D, c = threadIdx.x % D;
     const float *pp = P + (size_t)g * (D + 2) + 2 + c;
-#pragma unroll 8
-    for (int t = 0; t < nt; ++t) acc = fmaf(pp[(size_t)t * G * (D + 2)], sm[t][g], acc);
-    out[((size_t)seq * Hq + h * G + g) * D + c] = acc;
+    // 8 independent partial sums keep 8 tile loads in flight
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    int t = 0;
+    for (; t + 8 <= nt; t += 8) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc[u] = fmaf(pp[(size_t)(t + u) * G * (D + 2)], sm[t + u][g], acc[u]);
+    }
+    for (; t < nt; ++t) acc[0] = fmaf(pp[(size_t)t * G * (D + 2)], sm[t][g], acc[0]);
+    out[((size_t)seq * Hq + h * G + g) * D + c] =
+        ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
   }
   if (sd.method == H2O) {
     // accumulate, and find the eviction candidate (lowest score among positions older than the
@@ -967,7 +979,7 @@ __global__ __launch_bounds__(256) void k_attn_combine(const SeqDesc *__restrict_
     }
     unsigned long long best = ~0ull;
     int best_slot = -1;
-    for (int j = threadIdx.x; j < count; j += 256) {
+    for (int j = threadIdx.x; j < count; j += kCombineThreads) {
       float acc = 0.f;
 #pragma unroll
       for (int g = 0; g < G; ++g) acc += exp2f(gld(lg + (size_t)j * G + g) - M[g]) * invL[g];
@@ -982,17 +994,16 @@ __global__ __launch_bounds__(256) void k_attn_combine(const SeqDesc *__restrict_
       }
     }
     if (count > sd.B) {
-      __shared__ unsigned long long s_best[4];
       unsigned long long wb = best;
 #pragma unroll
       for (int m = 32; m >= 1; m >>= 1) {
         const unsigned long long x = __shfl_xor(wb, m);
         wb = x < wb ? x : wb;
       }
-      if ((threadIdx.x & 63) == 0) s_best[threadIdx.x >> 6] = wb;
+      if (ln == 0) s_best[wv] = wb;
       __syncthreads();
       unsigned long long all = s_best[0];
-      for (int w = 1; w < 4; ++w) all = s_best[w] < all ? s_best[w] : all;
+      for (int w = 1; w < NWC; ++w) all = s_best[w] < all ? s_best[w] : all;
       if (best_slot >= 0 && best == all) st[ST_VICTIM] = best_slot;
     }
   }
@@ -1013,7 +1024,7 @@ hipError_t partial_impl(const Dev &dv, const Shape &sh, const uint16_t *q, int p
 
 template <int D, int G>
 hipError_t combine_impl(const Dev &dv, const Shape &sh, float *out, hipStream_t st) {
-  hipLaunchKernelGGL((k_attn_combine<D, G>), dim3(sh.S * sh.Hkv), dim3(256), 0, st, dv.seqs, dv.state,
+  hipLaunchKernelGGL((k_attn_combine<D, G>), dim3(sh.S * sh.Hkv), dim3(kCombineThreads), 0, st, dv.seqs, dv.state,
                      dv.partials, out, sh.Hkv);
   return hipGetLastError();
 }

@@ -36,16 +36,19 @@ MKV_DEV int compact_ascending(int n, Flag flag, IsEq is_eq, Emit emit, int *s_tm
 }
 
 // ---- RocketKV decode top-k ---------------------------------------------------------------------
+// One workgroup of 1024 threads per (sequence, kv head): a kept set of up to a few thousand
+// tokens is scored with ~4 tokens per thread and selected by radix passes over LDS keys.
+constexpr int kTopkThreads = 1024;
 template <int D, int G>
-__global__ __launch_bounds__(NT) void k_topk(const SeqDesc *__restrict__ seqs, int32_t *state,
+__global__ __launch_bounds__(kTopkThreads) void k_topk(const SeqDesc *__restrict__ seqs, int32_t *state,
                                              const uint16_t *__restrict__ q, int32_t *pos_out, int topk_max,
                                              int Hkv) {
   __shared__ float s_a[D];
   __shared__ float s_qb[D];
   __shared__ int s_ch[D];
-  __shared__ int whist[NT / 64][256];
+  __shared__ int whist[kTopkThreads / 64][256];
   __shared__ int s3[3];
-  __shared__ int s_tmp[NT / 64];
+  __shared__ int s_tmp[kTopkThreads / 64];
   __shared__ uint32_t s_keys[kTopkLdsKeys];
   const int seq = blockIdx.x / Hkv, h = blockIdx.x % Hkv;
   const SeqDesc &sd = seqs[seq];
@@ -60,7 +63,7 @@ __global__ __launch_bounds__(NT) void k_topk(const SeqDesc *__restrict__ seqs, i
   const uint16_t *qh = q + ((size_t)seq * Hq + h * G) * D;
 
   // channel magnitudes and head sums, float32 in ascending head order
-  for (int c = threadIdx.x; c < D; c += NT) {
+  for (int c = threadIdx.x; c < D; c += kTopkThreads) {
     float a = 0.f, qb = 0.f;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -74,7 +77,7 @@ __global__ __launch_bounds__(NT) void k_topk(const SeqDesc *__restrict__ seqs, i
   __syncthreads();
   const int nch = min(sd.nch, D);
   // channel c is selected iff fewer than nch channels beat it (larger a, or equal a and lower index)
-  for (int c = threadIdx.x; c < D; c += NT) {
+  for (int c = threadIdx.x; c < D; c += kTopkThreads) {
     const float a = s_a[c];
     int beats = 0;
     for (int c2 = 0; c2 < D; ++c2) {
@@ -86,22 +89,29 @@ __global__ __launch_bounds__(NT) void k_topk(const SeqDesc *__restrict__ seqs, i
   __syncthreads();
   __shared__ int s_sel_ch[D];
   __shared__ float s_sel_qb[D];
-  if (threadIdx.x == 0) {
-    int m = 0;
-    for (int c = 0; c < D; ++c)
-      if (s_ch[c]) {
-        s_sel_ch[m] = c;
-        s_sel_qb[m] = s_qb[c];
-        ++m;
-      }
+  __shared__ int s_wcnt[(D + 63) / 64];
+  // ascending compaction of the selected channels: rank = selected channels below c
+  {
+    const int c = threadIdx.x;
+    const bool f = c < D && s_ch[c] != 0;
+    const uint64_t m = __ballot(f);
+    const int lane = c & 63, w = c >> 6;
+    if (c < D && lane == 0) s_wcnt[w] = __popcll(m);
+    __syncthreads();
+    if (f) {
+      int r = __popcll(m & ((lane == 0) ? 0ull : (~0ull >> (64 - lane))));
+      for (int i = 0; i < w; ++i) r += s_wcnt[i];
+      s_sel_ch[r] = c;
+      s_sel_qb[r] = s_qb[c];
+    }
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < nch; i += NT) chan_out[i] = s_sel_ch[i];
+  for (int i = threadIdx.x; i < nch; i += kTopkThreads) chan_out[i] = s_sel_ch[i];
 
   if (k >= n) {
-    for (int j = threadIdx.x; j < n; j += NT) sel[j] = j;
+    for (int j = threadIdx.x; j < n; j += kTopkThreads) sel[j] = j;
     if (pos_out != nullptr)
-      for (int i = threadIdx.x; i < topk_max; i += NT)
+      for (int i = threadIdx.x; i < topk_max; i += kTopkThreads)
         pos_out[((size_t)seq * Hkv + h) * topk_max + i] = i < n ? pos[i] : -1;
     if (threadIdx.x == 0) st[ST_SEL_COUNT] = n;
     return;
@@ -117,7 +127,7 @@ __global__ __launch_bounds__(NT) void k_topk(const SeqDesc *__restrict__ seqs, i
   // each lane scores 4 consecutive tokens from one 8-byte load per channel; the loads of 16
   // channels are issued before any is used (rows are padded to 8 tokens, so the load never
   // leaves the row)
-  for (int j0 = 4 * (int)threadIdx.x; j0 < n; j0 += 4 * NT) {
+  for (int j0 = 4 * (int)threadIdx.x; j0 < n; j0 += 4 * kTopkThreads) {
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
     for (int i0 = 0; i0 < nch; i0 += 16) {
       uint32_t lo[16], hi[16];
@@ -152,10 +162,10 @@ __global__ __launch_bounds__(NT) void k_topk(const SeqDesc *__restrict__ seqs, i
   auto getk = [&](int i) { return in_lds ? s_keys[i] : gld(akeys + i); };
   uint32_t kth;
   int n_eq, need;
-  radix_select_kth_waves<NT>(n, k, getk, whist, s3, s_tmp, &kth, &n_eq, &need);
+  radix_select_kth_waves<kTopkThreads>(n, k, getk, whist, s3, s_tmp, &kth, &n_eq, &need);
   // each thread takes a contiguous run of tokens; counts of keys above and equal to the
   // threshold before its run place its selected tokens in ascending order
-  const int per = (n + NT - 1) / NT;
+  const int per = (n + kTopkThreads - 1) / kTopkThreads;
   const int ja = min(n, (int)threadIdx.x * per), jb = min(n, ja + per);
   int gt = 0, eq = 0;
   for (int j = ja; j < jb; ++j) {
@@ -164,8 +174,8 @@ __global__ __launch_bounds__(NT) void k_topk(const SeqDesc *__restrict__ seqs, i
     eq += kk == kth ? 1 : 0;
   }
   int tot;
-  const int gt_before = block_exclusive_scan<NT>(gt, s_tmp, &tot);
-  int eq_run = block_exclusive_scan<NT>(eq, s_tmp, &tot);
+  const int gt_before = block_exclusive_scan<kTopkThreads>(gt, s_tmp, &tot);
+  int eq_run = block_exclusive_scan<kTopkThreads>(eq, s_tmp, &tot);
   int slot = gt_before + min(eq_run, need);
   for (int j = ja; j < jb; ++j) {
     const uint32_t kk = getk(j);
@@ -176,7 +186,7 @@ __global__ __launch_bounds__(NT) void k_topk(const SeqDesc *__restrict__ seqs, i
   }
   __syncthreads();
   if (pos_out != nullptr)
-    for (int i = threadIdx.x; i < topk_max; i += NT)
+    for (int i = threadIdx.x; i < topk_max; i += kTopkThreads)
       pos_out[((size_t)seq * Hkv + h) * topk_max + i] = i < k ? gld(pos + gld(sel + i)) : -1;
   if (threadIdx.x == 0) st[ST_SEL_COUNT] = k;
 }
@@ -567,7 +577,7 @@ __global__ __launch_bounds__(NT) void k_snap_keep(const SeqDesc *__restrict__ se
 template <int D, int G>
 hipError_t topk_impl(const Dev &dv, const Shape &sh, const uint16_t *q, int32_t *pos_out, int topk_max,
                      hipStream_t st) {
-  hipLaunchKernelGGL((k_topk<D, G>), dim3(sh.S * sh.Hkv), dim3(NT), 0, st, dv.seqs, dv.state, q, pos_out,
+  hipLaunchKernelGGL((k_topk<D, G>), dim3(sh.S * sh.Hkv), dim3(kTopkThreads), 0, st, dv.seqs, dv.state, q, pos_out,
                      topk_max, sh.Hkv);
   return hipGetLastError();
 }

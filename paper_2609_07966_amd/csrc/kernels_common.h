@@ -179,27 +179,29 @@ MKV_DEV void radix_select_kth(int n, int k, Get get, int *hist, int *shared3, ui
 template <int NT, typename Get>
 MKV_DEV void radix_select_kth_waves(int n, int k, Get get, int (*whist)[256], int *shared3, int *s_tmp,
                                     uint32_t *kth, int *n_equal, int *need) {
-  static_assert(NT == 256, "one thread per digit");
+  static_assert(NT >= 256 && NT % 64 == 0, "threads 0..255 own one digit each");
   const int wid = threadIdx.x >> 6;
   uint32_t prefix = 0, mask = 0;
   int remaining = k;
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
-    for (int w = 0; w < NT / 64; ++w) whist[w][threadIdx.x] = 0;
+    for (int e = threadIdx.x; e < (NT / 64) * 256; e += NT) (&whist[0][0])[e] = 0;
     __syncthreads();
     for (int i = threadIdx.x; i < n; i += NT) {
       const uint32_t key = get(i);
       if ((key & mask) == prefix) atomicAdd(&whist[wid][(key >> shift) & 255u], 1);
     }
     __syncthreads();
-    // thread b owns digit 255 - b, so the exclusive scan gives the count of larger digits
+    // thread b < 256 owns digit 255 - b, so the exclusive scan gives the count of larger digits
     const int dgt = 255 - (int)threadIdx.x;
     int cnt = 0;
+    if (threadIdx.x < 256) {
 #pragma unroll
-    for (int w = 0; w < NT / 64; ++w) cnt += whist[w][dgt];
+      for (int w = 0; w < NT / 64; ++w) cnt += whist[w][dgt];
+    }
     int tot;
     const int above = block_exclusive_scan<NT>(cnt, s_tmp, &tot);
-    if (above < remaining && remaining <= above + cnt) {
+    if (threadIdx.x < 256 && above < remaining && remaining <= above + cnt) {
       shared3[0] = dgt;
       shared3[1] = remaining - above;
       shared3[2] = cnt;
