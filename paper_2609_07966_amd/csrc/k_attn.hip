@@ -52,7 +52,9 @@ MKV_DEV uint32_t pk_f16(float lo, float hi) { return f16bits(lo) | (f16bits(hi) 
 // Matrix path
 // ================================================================================================
 // Lane roles (lr = lane % 16, lq = lane / 16):
-//   q.k operand A  token row lr, channels CPL*lq + 4m + j (m = MFMA index, j = element)
+//   q.k operand A  token row lr, channels CPL*lq + 4m + j (m = MFMA index, j = element); fp16
+//                  rows instead take channels 32*(m/2) + 8*lq + 4*(m%2) + j, so that the four
+//                  lanes of a row read one contiguous 64-byte piece per load
 //   q.k operand B  query head lr, same channels
 //   S              token rows 4*lq + j, query head lr
 //   p.v operand A  channel VPL*lr + m, tokens 4*lq + j
@@ -112,9 +114,12 @@ struct MRows {
     }
   }
   MKV_DEV void load_rows(int ks, const int (&vs)[4], Raw &r) const {
-    const uint32_t *kp = reinterpret_cast<const uint32_t *>(K + (size_t)ks * D + CPL * lq);
+    // 16-byte pieces at channels 32 i + 8 lq (i < D / 32)
+    const uint32_t *kp = reinterpret_cast<const uint32_t *>(K + (size_t)ks * D + 8 * lq);
 #pragma unroll
-    for (int i = 0; i < CPL / 2; ++i) r.kw[i] = gld(kp + i);
+    for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+      for (int w = 0; w < 4; ++w) r.kw[4 * i + w] = gld(kp + 16 * i + w);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const uint32_t *vp = reinterpret_cast<const uint32_t *>(V + (size_t)vs[j] * D + VPL * lr);
@@ -186,7 +191,8 @@ struct MKVQ {
   const float *cbk, *cbv;         // LDS codebooks
   const float *qq;                // LDS [D][2G]: scaled q of heads 0..G-1, then scaled q tau
   float *vcorr;                   // LDS [D]: this lane's value-outlier terms (head lr), relative to vref
-  float *kcorr;                   // LDS [G][32]: this wave's key-outlier logit terms of the batch
+  float *kcorr;                   // LDS [G + 1][32]: this wave's key-outlier logit terms of the
+                                  // batch (row G stays zero)
   int lr, lq, rowbytes, nov, cap;
   int prole;                      // p operand: 0 fp16 part, 1 residual, 2 zero
   // The value-outlier terms of head lr are kept relative to a reference max vref <= m_run that
@@ -264,15 +270,17 @@ struct MKVQ {
     for (int g = 0; g < G; ++g) acc[g] = 0.f;
     for (int i = 0; __any(i < cnt); ++i) {
       const int src = k0 + i;
-      // entries past the 64 loaded by the wave (more than 64 in one batch) come from memory
+      const bool on = i < cnt;
       uint32_t ent = (uint32_t)__shfl((int)bt.ent, min(src, 63));
-      if (i < cnt && src >= 64) ent = gld(kout + e0 + src);
-      if (i < cnt) {
-        const int ch = outlier_ch(ent);
-        const float x = h2f(ent >> 16), c = cbk[outlier_code(ent)];
-#pragma unroll
-        for (int g = 0; g < G; ++g) acc[g] += qq[ch * 2 * G + g] * x - qq[ch * 2 * G + G + g] * c;
+      // entries past the 64 loaded by the wave (more than 64 in one batch) come from memory
+      if (__any(on && src >= 64)) {
+        if (on && src >= 64) ent = gld(kout + e0 + src);
       }
+      // lanes without an entry this round read channel 0 and add nothing
+      const int ch = on ? min(outlier_ch(ent), D - 1) : 0;
+      const float x = on ? h2f(ent >> 16) : 0.f, c = on ? cbk[outlier_code(ent)] : 0.f;
+#pragma unroll
+      for (int g = 0; g < G; ++g) acc[g] += qq[ch * 2 * G + g] * x - qq[ch * 2 * G + G + g] * c;
     }
     if (lane < 32) {
 #pragma unroll
@@ -285,10 +293,10 @@ struct MKVQ {
     for (int m = 0; m < NM; ++m)
       S = mfma16(mk_h4(lutk[field(r.kw, 2 * m)], lutk[field(r.kw, 2 * m + 1)]), qb.b[m], S);
   }
-  // step s of the batch: this lane's tokens 16 s + 4 lq + j, head lr
+  // step s of the batch: this lane's tokens 16 s + 4 lq + j, head lr (columns lr >= G read the
+  // zero row)
   MKV_DEV void kfix(int s, float (&x)[4]) const {
-    if (lr >= G) return;
-    const float4 c = *reinterpret_cast<const float4 *>(kcorr + lr * 32 + 16 * s + 4 * lq);
+    const float4 c = *reinterpret_cast<const float4 *>(kcorr + min(lr, G) * 32 + 16 * s + 4 * lq);
     x[0] += c.x;
     x[1] += c.y;
     x[2] += c.z;
@@ -686,7 +694,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   __shared__ float s_q[D][2 * G];            // KVQuant: scaled q of each head, then scaled q * tau
   __shared__ uint32_t s_lut[2][256];         // KVQuant: key and value pair tables
   __shared__ float s_cb[2][16];              // KVQuant: codebooks
-  __shared__ __attribute__((aligned(16))) float s_kc[NW][G][32];  // KVQuant key-outlier logit terms
+  __shared__ __attribute__((aligned(16))) float s_kc[NW][G + 1][32];  // KVQuant key-outlier logit terms
   __shared__ float2 s_vm[NW][64];            // uniform 4-bit: a batch's value (min, step) pairs
   __shared__ __attribute__((aligned(16))) float s_km[NW][2 * D];  // uniform 4-bit: a key block's pairs
 
@@ -732,6 +740,8 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     }
     float4 *vz = reinterpret_cast<float4 *>(&s_wave[wave][0]);
     for (int e = lane; e < kWaveFloats / 4; e += 64) vz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 *kz = reinterpret_cast<float4 *>(&s_kc[wave][0][0]);
+    for (int e = lane; e < (G + 1) * 32 / 4; e += 64) kz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
   __syncthreads();
   // q.k operand B: query head lr, channels CPL*lq + 4m .. +3 (KVQuant: fp16 part of the scaled
@@ -740,7 +750,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
 #pragma unroll
   for (int m = 0; m < NM; ++m) {
     uint32_t w[2] = {0u, 0u};
-    const int c = CPL * lq + 4 * m;
+    const int c = kvq ? CPL * lq + 4 * m : 32 * (m / 2) + 8 * lq + 4 * (m % 2);
     if (kvq) {
       if (lr < 2 * G) {
         const int g = lr < G ? lr : 2 * G - 1 - lr;
