@@ -73,13 +73,16 @@ def token_bytes(cfg, n0, step, D, G):
     return n * (D * b // 4 + 4 + 4 + 4 * nov + 4 * k_out)
 
 
+PART_OF = {"uq": "uq", "rocket": "rk"}
+
+
 def launch_bytes(wl, step, n_tiles, part="mx"):
-    """Algorithmic bytes of one launch of a partial kernel: "mx" (every method but uniform
-    4-bit) or "uq" (uniform 4-bit sequences); `n_tiles` is that kernel's workgroup count."""
+    """Algorithmic bytes of one partial launch: "mx" (fp16, H2O and KVQuant sequences), "rk"
+    (RocketKV) or "uq" (uniform 4-bit); `n_tiles` is that launch's workgroup count."""
     D, G, Hkv = wl.head_dim, wl.group, wl.n_kv_heads
     tot = 0.0
     for s in range(wl.n_seqs):
-        if (wl.cfg(s)["method"] == "uq") != (part == "uq"):
+        if PART_OF.get(wl.cfg(s)["method"], "mx") != part:
             continue
         tot += Hkv * token_bytes(wl.cfg(s), wl.prompt_lens[s], step, D, G)
         tot += wl.n_q_heads * D * 2                     # q
@@ -161,23 +164,24 @@ def run_gpu(wl, steps, warmup, replicas=1, label=""):
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - a
     kinds = {}
-    for kind in ("partial", "partial_uq", "combine", "append", "topk", "evict"):
+    for kind in ("partial", "partial_uq", "partial_rocket", "combine", "append", "topk", "evict"):
         n, ms = 0, 0.0
         for c in caches:
             a_n, a_ms = _lib.mkv_profile_read(c.h, kind)
             n += a_n
             ms += a_ms
         kinds[kind] = (n, ms)
-    n_tiles, n_uq = caches[0].n_tiles()
-    # the partial kernel that carries most of the bytes: the fp16-row / KVQuant instantiation,
-    # unless the batch holds only uniform 4-bit sequences
-    part = "partial" if kinds["partial"][0] else "partial_uq"
-    ptiles = n_tiles - n_uq if part == "partial" else n_uq
-    pbytes = "mx" if part == "partial" else "uq"
-    bytes_steps = [launch_bytes(wl, warmup + i, ptiles, pbytes) for i in range(steps)]
+    n_tiles, n_uq, n_rk = caches[0].n_tiles()
+    tiles_of = {"mx": n_tiles - n_uq - n_rk, "rk": n_rk, "uq": n_uq}
+    kind_of = {"mx": "partial", "rk": "partial_rocket", "uq": "partial_uq"}
+    # the partial launch that carries most of the bytes (the fp16-row / KVQuant one when the
+    # batch has such sequences)
+    part = max(("mx", "rk", "uq"), key=lambda p: launch_bytes(wl, warmup, tiles_of[p], p) if tiles_of[p] else -1)
+    bytes_steps = [launch_bytes(wl, warmup + i, tiles_of[part], part) for i in range(steps)]
     avg_bytes = float(np.mean(bytes_steps))
-    all_bytes = float(np.mean([launch_bytes(wl, warmup + i, n_tiles - n_uq, "mx") +
-                               launch_bytes(wl, warmup + i, n_uq, "uq") for i in range(steps)]))
+    all_bytes = float(np.mean([sum(launch_bytes(wl, warmup + i, tiles_of[p], p) for p in tiles_of)
+                               for i in range(steps)]))
+    part = kind_of[part]
     n_part, ms_part = kinds[part]
     avg_part_ms = ms_part / max(n_part, 1)
     res = {
@@ -185,7 +189,7 @@ def run_gpu(wl, steps, warmup, replicas=1, label=""):
         "partial_kernel": part, "partial_ms": avg_part_ms, "partial_bytes": avg_bytes,
         "partial_gbs": avg_bytes / (avg_part_ms * 1e-3) / 1e9,
         "step_gbs": all_bytes / (elapsed / steps) / 1e9,
-        "n_tiles": n_tiles, "n_tiles_uq": n_uq, "replicas": replicas,
+        "n_tiles": n_tiles, "n_tiles_uq": n_uq, "n_tiles_rocket": n_rk, "replicas": replicas,
         "kernel_ms": {k: (v[1] / max(v[0], 1)) for k, v in kinds.items() if v[0]},
     }
     for c in caches:
@@ -202,7 +206,7 @@ def per_config_runs(args):
              ("llama_layer", "KVQ2"), ("h2o", "H2O-20"), ("rocket", "Rocket-4096")]
     for name, cfg in cases:
         wl = make_workload(name, seed=args.seed, config_ids=cfg)
-        b1 = launch_bytes(wl, 0, 0, "mx") + launch_bytes(wl, 0, 0, "uq")
+        b1 = sum(launch_bytes(wl, 0, 0, p) for p in ("mx", "rk", "uq"))
         reps = max(1, math.ceil(2 * MALL_BYTES / b1))
         r = run_gpu(wl, args.cfg_steps, 2, replicas=reps, label=f"{name}/{cfg}")
         runs.append({"workload": name, "config": cfg, "steps_per_s": round(r["steps_per_s"], 1),
@@ -303,7 +307,7 @@ def main():
         "dtype": "f16 storage (fp16 / packed 2-4 bit codes), f32 compute",
         "data": "synthetic (seeded; workloads.gen)",
         "config": {"workload": "mixed: 64 seqs, 32q/8kv x 128, prompts log-uniform [1024, 32768], "
-                               "11 configs assigned uniformly (seed 0), one ragged launch per stage",
+                               "11 configs assigned uniformly (seed 0); per step: append, top-k, attention, eviction, with independent launches overlapped on 3 streams",
                    "n_seqs": wl.n_seqs, "prompt_tokens": int(sum(wl.prompt_lens)), "configs": counts,
                    "parallelism": "single GPU"},
         "hbm_TBs_attention": round(head["partial_gbs"] / 1e3, 3),

@@ -16,7 +16,13 @@
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     Calls validate on the host, enqueue on `stream` and return without
  *     synchronising (mkv_export and mkv_fit_codebooks are synchronous).
- *     Inputs must stay live until the stream has consumed them.
+ *     Inputs must stay live until the stream has consumed them.  Work that
+ *     does not depend on the rest runs on two streams the handle owns
+ *     (default priority), forked from `stream` and joined back into it: the
+ *     top-k selection and RocketKV attention, and uniform 4-bit attention.
+ *     mkv_decode_attention's output, and mkv_topk_select's pos_out when
+ *     given, are ordered on `stream`; use one stream for the decode calls of
+ *     a step.
  *   - A call that fails validation returns an error, enqueues nothing and
  *     leaves the handle unchanged; mkv_last_error() then describes it.
  *   - One host thread at a time per handle; distinct handles are independent.
@@ -231,10 +237,10 @@ mkv_status mkv_fit_codebooks(const uint16_t *k, const uint16_t *v, int32_t n_tok
  * `cache` is bracketed by HIP events on its stream (at most `max_launches`
  * per kind, pre-created here).  mkv_profile_read waits for them and returns,
  * for kernel kind `kind`, the launch count and the summed device time in
- * milliseconds.  Kinds: 0 attention partial (every method but uniform 4-bit;
- * launched only when there are such sequences), 1 attention combine, 2 append,
- * 3 top-k select, 4 H2O eviction, 5 attention partial of uniform 4-bit
- * sequences (launched only when there are any).
+ * milliseconds.  Kinds: 0 attention partial of fp16, H2O and KVQ sequences,
+ * 1 attention combine, 2 append, 3 top-k select, 4 H2O eviction, 5 attention
+ * partial of uniform 4-bit sequences, 6 attention partial of RocketKV
+ * sequences (each partial launch happens only when it has sequences).
  */
 mkv_status mkv_profile_enable(mkv_cache *cache, int32_t enable, int32_t max_launches);
 mkv_status mkv_profile_read(mkv_cache *cache, int32_t kind, int32_t *launches, double *total_ms);
@@ -242,9 +248,11 @@ mkv_status mkv_profile_read(mkv_cache *cache, int32_t kind, int32_t *launches, d
 /*
  * Workgroups of the attention partial kernels per decode step: `n_tiles` in
  * all, of which `n_tiles_uq` (may be NULL) belong to uniform 4-bit sequences
- * and run in the second partial kernel.
+ * and `n_tiles_rocket` (may be NULL) to RocketKV sequences; each group runs in
+ * a launch of its own.
  */
-mkv_status mkv_attention_tiles(mkv_cache *cache, int32_t *n_tiles, int32_t *n_tiles_uq);
+mkv_status mkv_attention_tiles(mkv_cache *cache, int32_t *n_tiles, int32_t *n_tiles_uq,
+                               int32_t *n_tiles_rocket);
 
 #ifdef __cplusplus
 }

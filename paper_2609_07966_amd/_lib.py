@@ -17,7 +17,8 @@ EXPORT = {
     "scales_k": 6, "scales_v": 7, "scores": 8, "topk": 9, "channels": 10,
 }
 
-PROFILE_KINDS = {"partial": 0, "combine": 1, "append": 2, "topk": 3, "evict": 4, "partial_uq": 5}
+PROFILE_KINDS = {"partial": 0, "combine": 1, "append": 2, "topk": 3, "evict": 4, "partial_uq": 5,
+                 "partial_rocket": 6}
 
 
 class mkv_config(ctypes.Structure):
@@ -59,7 +60,7 @@ _SIGS = {
                                ctypes.POINTER(ctypes.c_float)]),
     "mkv_profile_enable": (_I, [_P, _I, _I]),
     "mkv_profile_read": (_I, [_P, _I, ctypes.POINTER(_I), ctypes.POINTER(ctypes.c_double)]),
-    "mkv_attention_tiles": (_I, [_P, ctypes.POINTER(_I), ctypes.POINTER(_I)]),
+    "mkv_attention_tiles": (_I, [_P, ctypes.POINTER(_I), ctypes.POINTER(_I), ctypes.POINTER(_I)]),
 }
 SYMBOLS = tuple(_SIGS)
 
@@ -188,7 +189,7 @@ def mkv_profile_read(h, kind):
 
 
 def mkv_attention_tiles(h):
-    """-> (all partial tiles, tiles of uniform 4-bit sequences)."""
-    n, n_uq = _I(), _I()
-    _check(lib().mkv_attention_tiles(h, ctypes.byref(n), ctypes.byref(n_uq)))
-    return n.value, n_uq.value
+    """-> (all partial tiles, tiles of uniform 4-bit sequences, tiles of RocketKV sequences)."""
+    n, n_uq, n_rk = _I(), _I(), _I()
+    _check(lib().mkv_attention_tiles(h, ctypes.byref(n), ctypes.byref(n_uq), ctypes.byref(n_rk)))
+    return n.value, n_uq.value, n_rk.value

@@ -93,5 +93,5 @@ class KVCache:
         return struct.unpack("4i", L.mkv_export(self.h, seq, kv_head, "counts"))
 
     def n_tiles(self):
-        """-> (all attention tiles, tiles of uniform 4-bit sequences)."""
+        """-> (all attention tiles, tiles of uniform 4-bit sequences, tiles of RocketKV sequences)."""
         return L.mkv_attention_tiles(self.h)

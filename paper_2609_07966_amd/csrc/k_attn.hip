@@ -1022,13 +1022,18 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
 template <int D, int G>
 hipError_t partial_impl(const Dev &dv, const Shape &sh, const uint16_t *q, int part, hipStream_t st) {
   const float qscale = kLog2e / sqrtf((float)D);
-  const int n_mx = dv.n_tiles - dv.n_tiles_uq;
-  if (part == 0 && n_mx > 0)
-    hipLaunchKernelGGL((k_attn_partial_mx<D, G, false>), dim3(n_mx), dim3(kTileThreads), 0, st, dv.seqs,
+  // tile groups: [fp16-row and KVQuant][RocketKV][uniform 4-bit]
+  const int n_main = dv.n_tiles - dv.n_tiles_uq - dv.n_tiles_rk;
+  if (part == 0 && n_main > 0)
+    hipLaunchKernelGGL((k_attn_partial_mx<D, G, false>), dim3(n_main), dim3(kTileThreads), 0, st, dv.seqs,
                        dv.state, dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale, 0);
+  if (part == 2 && dv.n_tiles_rk > 0)
+    hipLaunchKernelGGL((k_attn_partial_mx<D, G, false>), dim3(dv.n_tiles_rk), dim3(kTileThreads), 0, st,
+                       dv.seqs, dv.state, dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale, n_main);
   if (part == 1 && dv.n_tiles_uq > 0)
     hipLaunchKernelGGL((k_attn_partial_mx<D, G, true>), dim3(dv.n_tiles_uq), dim3(kTileThreads), 0, st,
-                       dv.seqs, dv.state, dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale, n_mx);
+                       dv.seqs, dv.state, dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale,
+                       n_main + dv.n_tiles_rk);
   return hipGetLastError();
 }
 
