@@ -127,6 +127,12 @@ struct MRows {
       for (int i = 0; i < VPL / 2; ++i) r.vw[j][i] = gld(vp + i);
     }
   }
+  // slots of the step at `base` (indices past the end re-read the last token)
+  MKV_DEV void index(int base, int b, int &ks, int (&vs)[4]) const {
+    ks = slot_of(min(base + lr, b - 1));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) vs[j] = slot_of(min(base + 4 * lq + j, b - 1));
+  }
   // step s: FULL: all 16 tokens of the step exist; otherwise indices past the end re-read the
   // last one
   template <bool FULL>
@@ -546,6 +552,73 @@ struct MUQ {
   }
 };
 
+// One 16-token step of fp16 rows (the loads of the next step are already in flight).
+template <int D, int G, bool GATHER>
+MKV_DEV void rows_step(const MRows<D, G, GATHER> &ld, const typename MRows<D, G, GATHER>::Raw &r, int base, int b,
+                       const QB<D> &qb, float qscale, float &m_run, float &l_part, f4v (&O)[MG<D>::NM],
+                       float *logit_out) {
+  const int lane = threadIdx.x & 63, lr = lane & 15, lq = lane >> 4;
+  f4v S = {0.f, 0.f, 0.f, 0.f};
+  ld.qk(r, qb, S);
+  float sc[4];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    sc[j] = base + 4 * lq + j < b ? S[j] * qscale : -INFINITY;
+    mx = fmaxf(mx, sc[j]);
+  }
+  if (logit_out != nullptr && lr < G) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (sc[j] != -INFINITY) gst(logit_out + (size_t)(base + 4 * lq + j) * G + lr, sc[j]);
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const bool up = mx > m_run;
+  if (__any(up)) {  // wave-uniform: rescale with factor 1 for the heads whose max held
+    const float corr = up ? fexp2(m_run - mx) : 1.f;
+    l_part *= corr;
+#pragma unroll
+    for (int m = 0; m < MG<D>::NM; ++m) O[m] *= corr;
+    if (up) m_run = mx;
+  }
+  float pp[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    pp[j] = fexp2(sc[j] - m_run);  // 0 for a masked token
+    l_part += pp[j];
+  }
+  ld.pv(r, pp, pp, 0xF, O);
+}
+
+// fp16 rows (FP16, H2O; gathered for RocketKV) over tokens [a, b) in 16-token steps, the row
+// loads of step i + 1 issued before step i is computed (and, when gathering, the slot indices
+// one step further ahead).
+template <int D, int G, bool GATHER>
+MKV_DEV void wave_rows(const MRows<D, G, GATHER> &ld, int a, int b, const QB<D> &qb, float qscale, float &m_run,
+                       float &l_part, f4v (&O)[MG<D>::NM], float *logit_out) {
+  if (a >= b) return;
+  typename MRows<D, G, GATHER>::Raw r0, r1;
+  int ks, vs[4];
+  ld.index(a, b, ks, vs);
+  ld.load_rows(ks, vs, r0);
+  ld.index(a + 16, b, ks, vs);
+  for (int base = a; base < b; base += 32) {
+    const bool more1 = base + 16 < b;
+    if (more1) {
+      ld.load_rows(ks, vs, r1);
+      ld.index(base + 32, b, ks, vs);
+    }
+    rows_step(ld, r0, base, b, qb, qscale, m_run, l_part, O, logit_out);
+    if (!more1) break;
+    if (base + 32 < b) {
+      ld.load_rows(ks, vs, r0);
+      ld.index(base + 48, b, ks, vs);
+    }
+    rows_step(ld, r1, base + 16, b, qb, qscale, m_run, l_part, O, logit_out);
+  }
+}
+
 // One 32-token batch of a wave.  FULL: all 32 tokens exist (no clamping, no masks).
 template <bool FULL, int D, int G, class L>
 MKV_DEV void mfma_batch(L &ld, int base, int b, typename L::Carry &cy, QB<D> &qb, float qscale,
@@ -822,7 +895,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     ld.lr = lr;
     ld.lq = lq;
     float *lg = (method == H2O) ? reinterpret_cast<float *>(sd.logits) + h * stride_logits(sd, G) : nullptr;
-    wave_mfma<D, G>(ld, wr.a, wr.b, qb, qscale, m_run, l_part, O, lg);
+    wave_rows<D, G, false>(ld, wr.a, wr.b, qb, qscale, m_run, l_part, O, lg);
   } else if (method == ROCKET) {
     MRows<D, G, true> ld;
     ld.K = reinterpret_cast<const uint16_t *>(sd.k) + h * stride_rows(sd, D);
@@ -830,7 +903,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     ld.sel = reinterpret_cast<const int32_t *>(sd.sel) + h * stride_sel(sd);
     ld.lr = lr;
     ld.lq = lq;
-    wave_mfma<D, G>(ld, wr.a, wr.b, qb, qscale, m_run, l_part, O, nullptr);
+    wave_rows<D, G, true>(ld, wr.a, wr.b, qb, qscale, m_run, l_part, O, nullptr);
   } else if (kvq) {
     auto run = [&](auto bits_tag) {
       constexpr int BITS = decltype(bits_tag)::value;
