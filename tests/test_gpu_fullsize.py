@@ -1,0 +1,360 @@
+"""GPU parity at the full sizes of the benchmark workloads, on sampled outputs.
+
+Each workload runs through the C ABI at its full size and in the launch configuration the
+benchmark times (one cache holding every sequence, the whole decode step per call).  At a few
+sampled steps the GPU output of sampled sequences is checked against the CPU oracle computed
+from scratch for that step (FP16, uniform 4-bit, KVQuant, RocketKV: the cache contents at step t
+follow from the inputs alone), to the same tolerance as the small-size lock-step tests; KVQuant
+codes and RocketKV selections are checked bit for bit.  H2O's retained set depends on the whole
+eviction history, so at full size it is checked through properties that hold at any size: the
+budget, the protected recent window, attention equal to exact attention over the exported
+retained set, and each eviction taking the lowest accumulated score among the eligible tokens.
+"""
+import numpy as np
+import pytest
+
+from oracle import kvquant, rocketkv, snapkv, uniform
+from oracle.attention import softmax_attention
+from oracle.h2o import budget
+from workloads import make_workload, prompt_kv, prompt_q, step_inputs
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-3
+TIE_BAND = 1e-5
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import os
+    import sys
+    sys.path.insert(0, os.path.dirname(__file__))
+    from paper_2609_07966_amd import _lib
+    _lib.lib()
+
+
+def _log(*a):
+    print(*a, flush=True)
+
+
+class FullRun:
+    """The workload's cache on the GPU; decode steps with outputs kept at sampled steps."""
+
+    def __init__(self, wl, steps, device="cuda"):
+        import torch
+        from gpu_harness import oracle_codebooks
+        from paper_2609_07966_amd.cache import KVCache
+        self.torch, self.wl, self.steps = torch, wl, steps
+        S = wl.n_seqs
+        self.cfgs = [wl.cfg(s) for s in range(S)]
+        need_cb = any(c["method"] == "kvq" for c in self.cfgs)
+        self.cbs, flat = oracle_codebooks(wl) if need_cb else (None, None)
+        self.cache = KVCache((S, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, steps), self.cfgs, wl.prompt_lens,
+                             codebooks=None if flat is None else list(flat), device=device)
+        self.dev = device
+        self.prompts = [prompt_kv(wl, s) for s in range(S)]
+        self._steps = {}
+
+    def step_inputs(self, t):
+        if t not in self._steps:
+            self._steps[t] = step_inputs(self.wl, t)
+        return self._steps[t]
+
+    def h(self, x):
+        return self.torch.from_numpy(np.ascontiguousarray(x)).to(self.dev)
+
+    def prefill(self):
+        wl, c = self.wl, self.cache
+        c.append_prompt(self.h(np.concatenate([p[0] for p in self.prompts])),
+                        self.h(np.concatenate([p[1] for p in self.prompts])))
+        h2o = [s for s in range(wl.n_seqs) if self.cfgs[s]["method"] == "h2o"]
+        if h2o:
+            c.h2o_prefill(self.h(np.concatenate([prompt_q(wl, s) for s in h2o])))
+        rk = [s for s in range(wl.n_seqs) if self.cfgs[s]["method"] == "rocket"]
+        if rk:
+            blocks = []
+            for s in rk:
+                w = self.cfgs[s].get("window", 32)
+                q = prompt_q(wl, s, last=w)
+                if q.shape[0] < w:
+                    q = np.concatenate([np.zeros((w - q.shape[0],) + q.shape[1:], np.float16), q])
+                blocks.append(q)
+            c.snap_prefill(self.h(np.concatenate(blocks)))
+        self.sync()
+
+    def sync(self):
+        if self.dev != "cpu":
+            self.torch.cuda.synchronize()
+
+    def run(self, sample_steps, watches=()):
+        """Decode every step; returns {t: GPU output} at the sampled steps.  At each sampled step
+        every watch's attended(t) runs after attention and evicted(t) after the eviction."""
+        wl, c, torch = self.wl, self.cache, self.torch
+        outs = {}
+        out = torch.empty((wl.n_seqs, wl.n_q_heads, wl.head_dim), dtype=torch.float32, device=self.dev)
+        for t in range(self.steps):
+            kn, vn, q = self.step_inputs(t)
+            c.append(self.h(kn), self.h(vn))
+            c.topk(self.h(q))
+            c.attention(self.h(q), out)
+            if t in sample_steps:
+                outs[t] = out.cpu().numpy().copy()
+                for w in watches:
+                    w.attended(t)
+            c.evict()
+            if t in sample_steps:
+                for w in watches:
+                    w.evicted(t)
+            if t % 32 == 31:
+                _log(f"[full]   step {t + 1}/{self.steps}")
+        self.sync()
+        return outs
+
+    def tokens(self, s, t):
+        """fp16 K and V rows [n0 + t + 1][Hkv][d] of sequence s after step t's append."""
+        kp, vp = self.prompts[s]
+        ks, vs = [kp], [vp]
+        for u in range(t + 1):
+            kn, vn, _ = self.step_inputs(u)
+            ks.append(kn[s][None])
+            vs.append(vn[s][None])
+        return np.concatenate(ks), np.concatenate(vs)
+
+
+def _check_out(gout, ref, v_eff, what):
+    rms = float(np.sqrt(np.mean(np.asarray(v_eff, np.float64) ** 2)))
+    err = float(np.abs(gout - ref).max() / max(rms, 1e-30))
+    assert err <= TOL, f"{what}: error {err:.3e} > {TOL}"
+    return err
+
+
+def _oracle_dense(run, s, t, q, gout):
+    """Check sequence s (FP16, uniform 4-bit or KVQuant) at step t against attention over its
+    whole history, dequantized from scratch."""
+    wl, c = run.wl, run.cfgs[s]
+    K, V = run.tokens(s, t)
+    n0 = run.prompts[s][0].shape[0]
+    G, worst = wl.group, 0.0
+    for h in range(wl.n_kv_heads):
+        if c["method"] == "fp16":
+            kk, vv = K[:, h].astype(np.float64), V[:, h].astype(np.float64)
+        elif c["method"] == "uq":
+            kk = uniform.effective_keys(K[:, h], 4, 64)
+            vv = uniform.effective_values(V[:, h], 4, 64)
+        else:
+            b, bp = c["bits"], c.get("outlier_bp", 100)
+            cbk, cbv = run.cbs[b]
+            tau, inv = kvquant.calibrate_keys(K[:n0, h], bp)
+            ck, ok = kvquant.quantize_keys(K[:, h], tau, inv, cbk, bp)
+            cv, sv, ov = kvquant.quantize_values(V[:, h], cbv, bp)
+            kk = kvquant.dequantize_keys(K[:, h], ck, ok, tau, cbk)
+            vv = kvquant.dequantize_values(V[:, h], cv, ov, sv, cbv)
+            n = K.shape[0]
+            np.testing.assert_array_equal(run.cache.export(s, h, "codes_k").reshape(-1, wl.head_dim)[:n], ck)
+            np.testing.assert_array_equal(run.cache.export(s, h, "codes_v").reshape(-1, wl.head_dim)[:n], cv)
+        ref, _ = softmax_attention(q[s, h * G:(h + 1) * G].astype(np.float64), kk, vv)
+        worst = max(worst, _check_out(gout[s, h * G:(h + 1) * G], ref, vv, f"seq {s} ({c['name']}) head {h} step {t}"))
+    return worst
+
+
+class TopkWatch:
+    """The GPU's top-k selection of RocketKV sequences at sampled steps."""
+
+    def __init__(self, run, seqs):
+        self.run, self.seqs, self.sel = run, seqs, {}
+
+    def attended(self, t):
+        for s in self.seqs:
+            for h in range(self.run.wl.n_kv_heads):
+                self.sel[(t, s, h)] = np.asarray(self.run.cache.export(s, h, "topk"), np.int64)
+
+    def evicted(self, t):
+        pass
+
+
+def _oracle_rocket(run, s, t, q, gout, keeps, topk):
+    """Check RocketKV sequence s at step t: top-k positions exactly, output to tolerance."""
+    wl, c = run.wl, run.cfgs[s]
+    K, V = run.tokens(s, t)
+    n0 = run.prompts[s][0].shape[0]
+    G, worst = wl.group, 0.0
+    T = int(c["keep_tokens"])
+    k = rocketkv.default_topk(T, c.get("topk", 0))
+    for h in range(wl.n_kv_heads):
+        rows = np.concatenate([keeps[h], np.arange(n0, K.shape[0])])
+        qh = q[s, h * G:(h + 1) * G]
+        ch = rocketkv.select_channels(qh, int(c.get("n_channels", 32)))
+        sel = rocketkv.topk_indices(rocketkv.approx_scores(qh, K[rows, h], ch), k)
+        np.testing.assert_array_equal(topk.sel[(t, s, h)], rows[sel],
+                                      err_msg=f"top-k seq {s} head {h} step {t}")
+        kk, vv = K[rows[sel], h].astype(np.float64), V[rows[sel], h].astype(np.float64)
+        ref, _ = softmax_attention(qh.astype(np.float64), kk, vv)
+        worst = max(worst, _check_out(gout[s, h * G:(h + 1) * G], ref, vv, f"seq {s} (rocket) head {h} step {t}"))
+    return worst
+
+
+def _rocket_keeps(run, s):
+    """SnapKV keep-sets of sequence s: the GPU's, checked against the oracle's (tie band)."""
+    from gpu_harness import _keep_set_tie_ok
+    wl, c = run.wl, run.cfgs[s]
+    kp = run.prompts[s][0]
+    n0, G = kp.shape[0], wl.group
+    T, w, pool = int(c["keep_tokens"]), int(c.get("window", 32)), int(c.get("pool", 7))
+    qw = prompt_q(wl, s, last=w)
+    keeps = []
+    for h in range(wl.n_kv_heads):
+        gk = np.asarray(run.cache.export(s, h, "positions"), np.int64)[:min(T, n0)]
+        if T >= n0:
+            assert list(gk) == list(range(n0))
+        else:
+            ok_keep = snapkv.snap_keep(qw[:, h * G:(h + 1) * G], kp[:, h], T, w, pool)
+            u = snapkv.pooled_votes(qw[:, h * G:(h + 1) * G], kp[:, h], w, pool)
+            u_full = np.concatenate([u, np.full(min(w, n0), np.inf)])
+            ok, _ = _keep_set_tie_ok(u_full, gk, ok_keep, set(range(n0 - min(w, n0), n0)))
+            assert ok, f"SnapKV keep-set of seq {s} head {h} differs beyond the tie band"
+        keeps.append(np.sort(gk))
+    return keeps
+
+
+class H2OWatch:
+    """Property checks of H2O sequences at sampled steps (taken after attention, before the
+    eviction that follows it)."""
+
+    def __init__(self, run, seqs):
+        self.run, self.seqs, self.before, self.after = run, seqs, {}, {}
+
+    def attended(self, t):
+        run, wl = self.run, self.run.wl
+        for s in self.seqs:
+            for h in range(wl.n_kv_heads):
+                pos = np.asarray(run.cache.export(s, h, "positions"), np.int64)
+                sc = np.asarray(run.cache.export(s, h, "scores"), np.float64)
+                self.before[(t, s, h)] = (pos, sc)
+
+    def evicted(self, t):
+        for s in self.seqs:
+            for h in range(self.run.wl.n_kv_heads):
+                self.after[(t, s, h)] = set(np.asarray(self.run.cache.export(s, h, "positions"), np.int64).tolist())
+
+    def check(self, t, q, gout):
+        run, wl = self.run, self.run.wl
+        G = wl.group
+        for s in self.seqs:
+            c = run.cfgs[s]
+            n0 = run.prompts[s][0].shape[0]
+            B, R = budget(c["budget_pct"], n0)
+            K, V = run.tokens(s, t)
+            for h in range(wl.n_kv_heads):
+                pos, sc = self.before[(t, s, h)]
+                nxt = n0 + t + 1
+                assert len(pos) == min(B, n0) + min(t + 1, B + 1 - min(B, n0)) or len(pos) == B + 1, \
+                    f"H2O seq {s} head {h} step {t}: {len(pos)} retained"
+                assert len(set(pos.tolist())) == len(pos) and pos.max() < nxt
+                recent = set(range(max(0, nxt - R), nxt))
+                assert recent <= set(pos.tolist()), f"H2O seq {s} head {h} step {t}: a recent token is gone"
+                kk, vv = K[pos, h].astype(np.float64), V[pos, h].astype(np.float64)
+                ref, _ = softmax_attention(q[s, h * G:(h + 1) * G].astype(np.float64), kk, vv)
+                _check_out(gout[s, h * G:(h + 1) * G], ref, vv, f"seq {s} (h2o) head {h} step {t}")
+                after = self.after[(t, s, h)]
+                assert after <= set(pos.tolist()), f"H2O seq {s} head {h} step {t}: a token appeared"
+                gone = set(pos.tolist()) - after
+                if len(pos) <= B:
+                    assert not gone, f"H2O seq {s} head {h} step {t}: eviction under budget"
+                    continue
+                assert len(gone) == 1, f"H2O seq {s} head {h} step {t}: {len(gone)} evicted"
+                ev = gone.pop()
+                elig = pos < nxt - R
+                keys = np.where(elig, sc, np.inf)
+                best = int(np.argmin(np.where(keys == keys.min(), pos, np.iinfo(np.int64).max)))
+                if int(pos[best]) != ev:
+                    i = int(np.nonzero(pos == ev)[0][0])
+                    assert elig[i] and abs(sc[i] - sc[best]) <= TIE_BAND * max(abs(sc[best]), 1e-30), \
+                        f"H2O seq {s} head {h} step {t}: evicted {ev} (score {sc[i]}) vs {pos[best]} ({sc[best]})"
+
+
+def test_fullsize_llama_layer_fp16_uq_kvquant():
+    """8 sequences x 4096-token prompts, 32q/8kv x 128, 128 steps: two sequences each of FP16,
+    uniform 4-bit, KVQuant 4-bit and KVQuant 2-bit; sampled steps 0, 63 and 127."""
+    wl = make_workload("llama_layer", seed=0,
+                       config_ids=["FP16", "UQ4-g64", "KVQ4", "KVQ2", "FP16", "UQ4-g64", "KVQ4", "KVQ2"])
+    _log(f"[full] llama layer: {wl.n_seqs} x {wl.prompt_lens[0]}, cfgs {wl.config_ids}, 128 steps")
+    run = FullRun(wl, 128)
+    run.prefill()
+    samples = (0, 63, 127)
+    outs = run.run(set(samples))
+    worst = 0.0
+    for t in samples:
+        _, _, q = run.step_inputs(t)
+        for s in (0, 1, 2, 7):
+            worst = max(worst, _oracle_dense(run, s, t, q, outs[t]))
+    _log(f"[full]   max normalised error {worst:.2e}")
+    run.cache.close()
+
+
+def test_fullsize_h2o_properties():
+    """8 sequences x 8192-token prompts, H2O-20, 256 steps (budget reached immediately)."""
+    wl = make_workload("h2o", seed=0, config_ids="H2O-20")
+    _log(f"[full] h2o: {wl.n_seqs} x {wl.prompt_lens[0]}, 256 steps")
+    run = FullRun(wl, 256)
+    run.prefill()
+    watch = H2OWatch(run, (0, 5))
+    samples = (0, 100, 255)
+    outs = run.run(set(samples), watches=[watch])
+    for t in samples:
+        _, _, q = run.step_inputs(t)
+        watch.check(t, q, outs[t])
+    run.cache.close()
+
+
+def test_fullsize_rocket():
+    """4 sequences x 32768-token prompts, SnapKV keeps 4096, top-2048 of 32 channels, 256 steps."""
+    wl = make_workload("rocket", seed=0, config_ids="Rocket-4096")
+    _log(f"[full] rocket: {wl.n_seqs} x {wl.prompt_lens[0]}, 256 steps")
+    run = FullRun(wl, 256)
+    run.prefill()
+    keeps = {s: _rocket_keeps(run, s) for s in (0, 3)}
+    topk = TopkWatch(run, (0, 3))
+    samples = (0, 255)
+    outs = run.run(set(samples), watches=[topk])
+    worst = 0.0
+    for t in samples:
+        _, _, q = run.step_inputs(t)
+        for s in (0, 3):
+            worst = max(worst, _oracle_rocket(run, s, t, q, outs[t], keeps[s], topk))
+    _log(f"[full]   max normalised error {worst:.2e}")
+    run.cache.close()
+
+
+def test_fullsize_mixed_batch():
+    """The benchmark's mixed batch (64 sequences, prompts log-uniform in [1024, 32768], all 11
+    configurations): 6 decode steps in the benchmark's launch configuration, sampled sequences
+    of every method checked at the last step."""
+    wl = make_workload("mixed", seed=0)
+    steps = 6
+    _log(f"[full] mixed: {wl.n_seqs} seqs, {sum(wl.prompt_lens)} prompt tokens, {steps} steps")
+    run = FullRun(wl, steps)
+    run.prefill()
+    by = {}
+    for s in range(wl.n_seqs):
+        by.setdefault(run.cfgs[s]["method"], []).append(s)
+    pick = {m: sorted(v, key=lambda s: wl.prompt_lens[s])[-1:] + sorted(v, key=lambda s: wl.prompt_lens[s])[:1]
+            for m, v in by.items()}
+    keeps = {s: _rocket_keeps(run, s) for s in pick.get("rocket", [])}
+    watch = H2OWatch(run, pick.get("h2o", []))
+    topk = TopkWatch(run, pick.get("rocket", []))
+    t = steps - 1
+    outs = run.run({t}, watches=[watch, topk])
+    _, _, q = run.step_inputs(t)
+    worst = 0.0
+    for m, seqs in pick.items():
+        for s in seqs:
+            if m == "rocket":
+                worst = max(worst, _oracle_rocket(run, s, t, q, outs[t], keeps[s], topk))
+            elif m != "h2o":
+                worst = max(worst, _oracle_dense(run, s, t, q, outs[t]))
+    watch.check(t, q, outs[t])
+    _log(f"[full]   max normalised error {worst:.2e} over {sum(len(v) for v in pick.values())} sequences")
+    run.cache.close()
