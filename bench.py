@@ -30,6 +30,11 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
 MALL_BYTES = 256 << 20
+ROOFLINE_KERNEL = "k_attn_partial_mx<128, 4, false>"
+# the sources the attention partial kernel is compiled from, and the committed counter record
+KERNEL_SOURCES = ("paper_2609_07966_amd/csrc/k_attn.hip", "paper_2609_07966_amd/csrc/kernels_common.h",
+                  "paper_2609_07966_amd/csrc/mkv_internal.h")
+TRAFFIC_RECORD = "profiles/attn_partial_mx_mixed64_traffic.md"
 
 
 def log(*a):
@@ -90,6 +95,64 @@ def launch_bytes(wl, step, n_tiles, part="mx"):
     return tot
 
 
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic():
+    """HBM bytes per launch of the roofline kernel from the committed counter record, or None when
+    the record is missing or was taken from other kernel sources."""
+    path = os.path.join(ROOT, TRAFFIC_RECORD)
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and line.startswith("- "):
+                k, v = line[2:].split(":", 1)
+                rec[k.strip()] = v.strip().strip("`")
+    if rec.get("source_sha256") != kernel_source_hash():
+        return None
+    try:
+        return float(rec["fetch_bytes_per_launch"]) + float(rec["write_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_probe(mib, reps=3):
+    """A plain copy of known size (float32, `mib` MiB read and `mib` MiB written per launch), for
+    scaling the memory counters of a profiled run."""
+    import torch
+    n = (mib << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        torch.add(src, 0.0, out=dst)
+    torch.cuda.synchronize()
+    log(f"[bench] copy probe: {reps} launches, {mib} MiB read + {mib} MiB written each")
+    del src, dst
+
+
+def read_ceiling_gbs(gib=4, reps=5):
+    """Read bandwidth a plain streaming kernel reaches on this GPU (the library's read probe over
+    `gib` GiB, best of `reps` passes)."""
+    import torch
+    from paper_2609_07966_amd import _lib
+    x = torch.ones((gib << 30) // 2, dtype=torch.float16, device="cuda")
+    sink = torch.zeros(256, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    g = _lib.mkv_probe_read_bandwidth(x.data_ptr(), x.numel() * 2, sink.data_ptr(), reps,
+                                      torch.cuda.current_stream().cuda_stream)
+    del x, sink
+    torch.cuda.empty_cache()
+    return g
+
+
 # ---- GPU leg ----------------------------------------------------------------------------------
 
 def product_codebooks(wl, tokens=1024):
@@ -103,14 +166,20 @@ def product_codebooks(wl, tokens=1024):
     return flat
 
 
-def run_gpu(wl, steps, warmup, replicas=1, label=""):
+KIND_BITS = {"partial": 0, "combine": 1, "append": 2, "topk": 3, "evict": 4, "partial_uq": 5, "partial_rocket": 6}
+
+
+def run_gpu(wl, steps, warmup, replicas=1, label="", prof_steps=24):
+    """Prefill, `warmup` untimed steps, `steps` timed steps (HIP events around the launches of the
+    partial kernel that carries the most bytes, and nothing else), then `prof_steps` steps with
+    every kernel kind timed (for the per-kernel breakdown only)."""
     import torch
     from paper_2609_07966_amd import _lib
     from paper_2609_07966_amd.cache import KVCache
     from workloads import prompt_kv, prompt_q, step_inputs
     S, Hq, Hkv, D = wl.n_seqs, wl.n_q_heads, wl.n_kv_heads, wl.head_dim
     cfgs = [wl.cfg(s) for s in range(S)]
-    total_steps = warmup + steps
+    total_steps = warmup + steps + prof_steps
     per_rep = math.ceil(total_steps / replicas)
     t0 = time.time()
     cb = product_codebooks(wl) if any(c["method"] == "kvq" for c in cfgs) else None
@@ -154,8 +223,27 @@ def run_gpu(wl, steps, warmup, replicas=1, label=""):
     for t in range(warmup):
         caches[t % replicas].step(kn[t], vn[t], qn[t], out)
     torch.cuda.synchronize()
+    n_tiles, n_uq, n_rk = caches[0].n_tiles()
+    tiles_of = {"mx": n_tiles - n_uq - n_rk, "rk": n_rk, "uq": n_uq}
+    kind_of = {"mx": "partial", "rk": "partial_rocket", "uq": "partial_uq"}
+    # the partial launch that carries most of the bytes (the fp16-row / KVQuant one when the
+    # batch has such sequences)
+    part = max(("mx", "rk", "uq"), key=lambda p: launch_bytes(wl, warmup, tiles_of[p], p) if tiles_of[p] else -1)
+    kind = kind_of[part]
+
+    def read_kinds(names):
+        out = {}
+        for k in names:
+            n, ms = 0, 0.0
+            for c in caches:
+                a_n, a_ms = _lib.mkv_profile_read(c.h, k)
+                n += a_n
+                ms += a_ms
+            out[k] = (n, ms)
+        return out
+
     for c in caches:
-        _lib.mkv_profile_enable(c.h, 1, per_rep + 1)
+        _lib.mkv_profile_enable(c.h, 1 << KIND_BITS[kind], per_rep + 1)
     torch.cuda.synchronize()
     a = time.perf_counter()
     for i in range(steps):
@@ -163,26 +251,22 @@ def run_gpu(wl, steps, warmup, replicas=1, label=""):
         caches[t % replicas].step(kn[t], vn[t], qn[t], out)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - a
-    kinds = {}
-    for kind in ("partial", "partial_uq", "partial_rocket", "combine", "append", "topk", "evict"):
-        n, ms = 0, 0.0
-        for c in caches:
-            a_n, a_ms = _lib.mkv_profile_read(c.h, kind)
-            n += a_n
-            ms += a_ms
-        kinds[kind] = (n, ms)
-    n_tiles, n_uq, n_rk = caches[0].n_tiles()
-    tiles_of = {"mx": n_tiles - n_uq - n_rk, "rk": n_rk, "uq": n_uq}
-    kind_of = {"mx": "partial", "rk": "partial_rocket", "uq": "partial_uq"}
-    # the partial launch that carries most of the bytes (the fp16-row / KVQuant one when the
-    # batch has such sequences)
-    part = max(("mx", "rk", "uq"), key=lambda p: launch_bytes(wl, warmup, tiles_of[p], p) if tiles_of[p] else -1)
+    n_part, ms_part = read_kinds([kind])[kind]
+    # per-kernel breakdown, outside the timed region
+    for c in caches:
+        _lib.mkv_profile_enable(c.h, (1 << len(KIND_BITS)) - 1, per_rep + 1)
+    for i in range(prof_steps):
+        t = warmup + steps + i
+        caches[t % replicas].step(kn[t], vn[t], qn[t], out)
+    torch.cuda.synchronize()
+    kinds = read_kinds(KIND_BITS)
+    for c in caches:
+        _lib.mkv_profile_enable(c.h, 0, 0)
     bytes_steps = [launch_bytes(wl, warmup + i, tiles_of[part], part) for i in range(steps)]
     avg_bytes = float(np.mean(bytes_steps))
     all_bytes = float(np.mean([sum(launch_bytes(wl, warmup + i, tiles_of[p], p) for p in tiles_of)
                                for i in range(steps)]))
-    part = kind_of[part]
-    n_part, ms_part = kinds[part]
+    part = kind
     avg_part_ms = ms_part / max(n_part, 1)
     res = {
         "steps": steps, "ms_per_step": elapsed / steps * 1e3, "steps_per_s": steps / elapsed,
@@ -275,6 +359,8 @@ def main():
     ap.add_argument("--cpu-steps", type=int, default=2)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-per-config", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MiB",
+                    help="after the run, launch a plain copy of this size (for memory-counter scaling)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the decode path shards by "
@@ -292,8 +378,12 @@ def main():
     from workloads import make_workload
     wl = make_workload("mixed", seed=args.seed, steps=args.warmup + args.steps)
     head = run_gpu(wl, args.steps, args.warmup, label="mixed")
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+    ceiling = None if args.no_per_config else read_ceiling_gbs()
     per_cfg = [] if args.no_per_config else per_config_runs(args)
     cpu = None if args.no_cpu else cpu_baseline(wl, args.cpu_steps)
+    traffic = recorded_traffic() if head["partial_kernel"] == "partial" else None
     counts = {}
     for s in range(wl.n_seqs):
         counts[wl.cfg(s)["name"]] = counts.get(wl.cfg(s)["name"], 0) + 1
@@ -313,9 +403,12 @@ def main():
         "hbm_TBs_attention": round(head["partial_gbs"] / 1e3, 3),
         "pct_of_peak_attention": round(100 * head["partial_gbs"] / PEAK_HBM_GBS, 1),
         "roofline": {"bound": "hbm", "achieved": round(head["partial_gbs"], 1), "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s", "frac": round(head["partial_gbs"] / PEAK_HBM_GBS, 4), "traffic": None,
-                     "kernel": "k_attn_partial_mx<128, 4, false>", "bytes_per_launch": round(head["partial_bytes"]),
+                     "unit": "GB/s", "frac": round(head["partial_gbs"] / PEAK_HBM_GBS, 4),
+                     "traffic": None if traffic is None else round(traffic),
+                     "kernel": ROOFLINE_KERNEL, "bytes_per_launch": round(head["partial_bytes"]),
                      "avg_launch_us": round(head["partial_ms"] * 1e3, 2)},
+        "read_ceiling_GBs": None if ceiling is None else round(ceiling, 1),
+        "attention_frac_of_read_ceiling": None if ceiling is None else round(head["partial_gbs"] / ceiling, 4),
         "kernel_us": {k: round(v * 1e3, 2) for k, v in head["kernel_ms"].items()},
         "per_config": per_cfg,
         "cpu_baseline": cpu,

@@ -233,14 +233,17 @@ mkv_status mkv_fit_codebooks(const uint16_t *k, const uint16_t *v, int32_t n_tok
                              int32_t outlier_bp, float *cb_k, float *cb_v);
 
 /*
- * Kernel timing.  When enabled, every kernel the library launches on behalf of
- * `cache` is bracketed by HIP events on its stream (at most `max_launches`
- * per kind, pre-created here).  mkv_profile_read waits for them and returns,
- * for kernel kind `kind`, the launch count and the summed device time in
- * milliseconds.  Kinds: 0 attention partial of fp16, H2O and KVQ sequences,
- * 1 attention combine, 2 append, 3 top-k select, 4 H2O eviction, 5 attention
- * partial of uniform 4-bit sequences, 6 attention partial of RocketKV
- * sequences (each partial launch happens only when it has sequences).
+ * Kernel timing.  `enable` is a mask of kernel kinds (bit k = kind k; 0
+ * turns timing off).  Every launch of a selected kind that the library makes
+ * on behalf of `cache` is bracketed by HIP events on its stream (at most
+ * `max_launches` per kind, pre-created here); each event costs a few
+ * microseconds of device time, so time a step's rate with the fewest kinds
+ * selected.  mkv_profile_read waits for them and returns, for kind `kind`,
+ * the launch count and the summed device time in milliseconds.  Kinds:
+ * 0 attention partial of fp16, H2O and KVQ sequences, 1 attention combine,
+ * 2 append, 3 top-k select, 4 H2O eviction, 5 attention partial of uniform
+ * 4-bit sequences, 6 attention partial of RocketKV sequences (each partial
+ * launch happens only when it has sequences).
  */
 mkv_status mkv_profile_enable(mkv_cache *cache, int32_t enable, int32_t max_launches);
 mkv_status mkv_profile_read(mkv_cache *cache, int32_t kind, int32_t *launches, double *total_ms);
@@ -253,6 +256,19 @@ mkv_status mkv_profile_read(mkv_cache *cache, int32_t kind, int32_t *launches, d
  */
 mkv_status mkv_attention_tiles(mkv_cache *cache, int32_t *n_tiles, int32_t *n_tiles_uq,
                                int32_t *n_tiles_rocket);
+
+/*
+ * Measurement utility (no part of any method): the read bandwidth a plain
+ * streaming kernel reaches on this GPU, for comparison with the attention
+ * kernels' achieved bandwidth.  Reads the device buffer `buf` of `bytes`
+ * bytes (a positive multiple of 256 KiB) once untimed and then `reps` times
+ * between two HIP events on `stream`, waits, and stores the best single-pass
+ * rate in GB/s (1e9 bytes/s) in *gbs.  `sink` is a device uint32 [256] that
+ * the kernel may write (only to keep its loads from being optimised away).
+ * Synchronous; allocates nothing on the device.
+ */
+mkv_status mkv_probe_read_bandwidth(const void *buf, size_t bytes, uint32_t *sink, int32_t reps,
+                                    double *gbs, void *stream);
 
 #ifdef __cplusplus
 }

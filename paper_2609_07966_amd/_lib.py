@@ -61,6 +61,7 @@ _SIGS = {
     "mkv_profile_enable": (_I, [_P, _I, _I]),
     "mkv_profile_read": (_I, [_P, _I, ctypes.POINTER(_I), ctypes.POINTER(ctypes.c_double)]),
     "mkv_attention_tiles": (_I, [_P, ctypes.POINTER(_I), ctypes.POINTER(_I), ctypes.POINTER(_I)]),
+    "mkv_probe_read_bandwidth": (_I, [_P, ctypes.c_size_t, _P, _I, ctypes.POINTER(ctypes.c_double), _P]),
 }
 SYMBOLS = tuple(_SIGS)
 
@@ -179,6 +180,7 @@ def mkv_fit_codebooks(k_bytes, v_bytes, n_tokens, n_kv_heads, head_dim, bits, ou
 
 
 def mkv_profile_enable(h, enable, max_launches):
+    """enable: mask of PROFILE_KINDS values to time (bit k = kind k), 0 = off."""
     _check(lib().mkv_profile_enable(h, int(enable), int(max_launches)))
 
 
@@ -186,6 +188,13 @@ def mkv_profile_read(h, kind):
     n, ms = _I(), ctypes.c_double()
     _check(lib().mkv_profile_read(h, PROFILE_KINDS.get(kind, kind), ctypes.byref(n), ctypes.byref(ms)))
     return n.value, ms.value
+
+
+def mkv_probe_read_bandwidth(buf_ptr, nbytes, sink_ptr, reps, stream=0):
+    """Best single-pass read rate (GB/s) of a plain streaming kernel over a device buffer."""
+    g = ctypes.c_double()
+    _check(lib().mkv_probe_read_bandwidth(buf_ptr, nbytes, sink_ptr, reps, ctypes.byref(g), stream))
+    return g.value
 
 
 def mkv_attention_tiles(h):

@@ -19,11 +19,13 @@
 // shuffles; value outliers accumulate in LDS rows private to each lane and are folded into the
 // output at the end.
 //
-// Vector path (uniform 4-bit): D/8 lanes share a token (8 channels each) and reduce q.k with DPP
-// row ops; per-block key scales are folded into q once per 64-token block.
+// Uniform 4-bit tiles run the same matrix loop in an instantiation of their own: 4-bit codes
+// become exact fp16 integers, each 64-token block's key steps are folded into q, each token's
+// value steps into p, and the minima enter as per-head bias terms.
 //
-// Logits use the base-2 exponent (scaled by log2(e)/sqrt(d) after the dot product); each lane
-// group issues the loads of 32 tokens per wave before computing any of them.
+// Logits use the base-2 exponent (scaled by log2(e)/sqrt(d)).  fp16-row tiles keep the loads of
+// the next 16 tokens in flight while computing the current 16; the other paths issue the loads
+// of a 32-token batch before computing any of it.
 #include "kernels_common.h"
 
 namespace mkv {

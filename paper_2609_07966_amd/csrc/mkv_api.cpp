@@ -263,7 +263,7 @@ struct mkv_cache {
   hipEvent_t ev_fork = nullptr, ev_sel = nullptr, ev_done[2] = {nullptr, nullptr};
   bool sel_pending = false;  // top-k work on aux[0] not yet joined into a caller stream
   // profiling
-  bool prof = false;
+  int prof_mask = 0;  // bit k: launches of kind k are timed
   int prof_cap = 0;
   std::vector<hipEvent_t> ev[kProfKinds][2];
   int prof_n[kProfKinds] = {};
@@ -272,7 +272,7 @@ struct mkv_cache {
 namespace {
 
 void prof_mark(mkv_cache *c, int kind, int which, hipStream_t st) {
-  if (!c->prof) return;
+  if (!(c->prof_mask >> kind & 1)) return;
   const int i = c->prof_n[kind];
   if (i >= c->prof_cap) return;
   hipEventRecord(c->ev[kind][which][i], st);
@@ -600,8 +600,38 @@ mkv_status mkv_attention_tiles(mkv_cache *c, int32_t *n_tiles, int32_t *n_tiles_
   return MKV_OK;
 }
 
+mkv_status mkv_probe_read_bandwidth(const void *buf, size_t bytes, uint32_t *sink, int32_t reps, double *gbs,
+                                    void *stream) {
+  constexpr size_t kChunk = 256 << 10;
+  if (!buf || !sink || !gbs) return fail(MKV_EINVAL, "NULL argument");
+  if (bytes == 0 || bytes % kChunk != 0) return fail(MKV_EINVAL, "bytes must be a positive multiple of 256 KiB");
+  if (bytes / kChunk > 0x7FFFFFFFu) return fail(MKV_EINVAL, "buffer too large");
+  if (reps < 1) return fail(MKV_EINVAL, "reps must be >= 1");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipEvent_t a = nullptr, b = nullptr;
+  hipError_t e = hipEventCreate(&a);
+  if (e == hipSuccess) e = hipEventCreate(&b);
+  if (e == hipSuccess) e = launch_probe_read(buf, bytes, kChunk, sink, st);
+  float best = 0.f;
+  for (int r = 0; r < reps && e == hipSuccess; ++r) {
+    e = hipEventRecord(a, st);
+    if (e == hipSuccess) e = launch_probe_read(buf, bytes, kChunk, sink, st);
+    if (e == hipSuccess) e = hipEventRecord(b, st);
+    if (e == hipSuccess) e = hipEventSynchronize(b);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+    if (e == hipSuccess && (best == 0.f || ms < best)) best = ms;
+  }
+  if (a) (void)hipEventDestroy(a);
+  if (b) (void)hipEventDestroy(b);
+  if (e != hipSuccess) return hip_fail(e, "read probe");
+  *gbs = best > 0.f ? (double)bytes / (best * 1e-3) / 1e9 : 0.0;
+  return MKV_OK;
+}
+
 mkv_status mkv_profile_enable(mkv_cache *c, int32_t enable, int32_t max_launches) {
   if (!c) return fail(MKV_EINVAL, "cache is NULL");
+  if (enable < 0 || enable >= (1 << kProfKinds)) return fail(MKV_EINVAL, "enable must be a mask of kinds 0..%d", kProfKinds - 1);
   if (enable && max_launches < 1) return fail(MKV_EINVAL, "max_launches must be >= 1");
   hipError_t e = hipDeviceSynchronize();
   if (e != hipSuccess) return hip_fail(e, "profile enable");
@@ -609,7 +639,7 @@ mkv_status mkv_profile_enable(mkv_cache *c, int32_t enable, int32_t max_launches
     for (int w = 0; w < 2; ++w) {
       for (hipEvent_t ev : c->ev[k][w]) hipEventDestroy(ev);
       c->ev[k][w].clear();
-      if (enable)
+      if (enable >> k & 1)
         for (int i = 0; i < max_launches; ++i) {
           hipEvent_t ev;
           if ((e = hipEventCreate(&ev)) != hipSuccess) return hip_fail(e, "hipEventCreate");
@@ -618,7 +648,7 @@ mkv_status mkv_profile_enable(mkv_cache *c, int32_t enable, int32_t max_launches
     }
     c->prof_n[k] = 0;
   }
-  c->prof = enable != 0;
+  c->prof_mask = enable;
   c->prof_cap = enable ? max_launches : 0;
   return MKV_OK;
 }

@@ -131,5 +131,8 @@ hipError_t launch_h2o_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc 
 hipError_t launch_snap_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
                                    const uint16_t *q_window, hipStream_t st);
 hipError_t launch_init_state(const Dev &dv, const Shape &sh, hipStream_t st);
+// Streaming read of `bytes` (a multiple of `chunk`, itself a multiple of 16 KiB); sink: device
+// uint32 [256], written only in the (practically never taken) branch that keeps the loads alive.
+hipError_t launch_probe_read(const void *buf, size_t bytes, size_t chunk, uint32_t *sink, hipStream_t st);
 
 }  // namespace mkv

@@ -89,6 +89,20 @@ def test_arena_grows_with_context_and_steps(L):
     assert h > 0 and f > 0
 
 
+@pytest.mark.parametrize("buf,nbytes,sink,reps", [
+    (0, 1 << 18, 4096, 1),          # NULL buffer
+    (4096, 1 << 18, 0, 1),          # NULL sink
+    (4096, (1 << 18) + 16, 4096, 1),  # not a multiple of 256 KiB
+    (4096, 0, 4096, 1),             # empty
+    (4096, 1 << 18, 4096, 0),       # no timed pass
+])
+def test_read_probe_validation(L, buf, nbytes, sink, reps):
+    # rejected on the host before any device work (the pointers are never dereferenced)
+    with pytest.raises(L.MkvError) as e:
+        L.mkv_probe_read_bandwidth(buf, nbytes, sink, reps)
+    assert e.value.status == 1
+
+
 def test_status_strings(L):
     for s in range(7):
         assert L.lib().mkv_status_str(s)

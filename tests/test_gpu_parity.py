@@ -98,3 +98,65 @@ def test_edge_cases():
             {"id": 5, "name": "H2O-dense", "method": "h2o", "budget_pct": 1000}]
     wl.cfg = lambda s: dict(cfgs[s])
     _run(wl, 12)
+
+
+def test_batch_invariance():
+    """Every sequence of a mixed batch gets exactly (bit for bit) the outputs, codes, selections
+    and evictions of its solo run: the ragged launch shares no arithmetic between sequences."""
+    import torch
+    from gpu_harness import log, oracle_codebooks
+    from paper_2609_07966_amd.cache import KVCache
+    from workloads import prompt_kv, prompt_q, step_inputs
+    wl = make_workload("custom", seed=11, n_seqs=6, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                       prompt_lens=[1500, 700, 2100, 1300, 1800, 900], steps=6,
+                       config_ids=["FP16", "UQ4-g64", "KVQ3", "H2O-20", "Rocket-1024", "KVQ2"])
+    steps, S, Hkv = 6, wl.n_seqs, wl.n_kv_heads
+    _, flat = oracle_codebooks(wl)
+    cfgs = [wl.cfg(s) for s in range(S)]
+    prompts = [prompt_kv(wl, s) for s in range(S)]
+    ins = [step_inputs(wl, t) for t in range(steps)]
+
+    def h(x):
+        return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+    def run(seqs):
+        log(f"[parity] batch invariance: sequences {seqs}")
+        c = KVCache((len(seqs), wl.n_q_heads, Hkv, wl.head_dim, steps), [cfgs[s] for s in seqs],
+                    [wl.prompt_lens[s] for s in seqs], codebooks=list(flat))
+        c.append_prompt(h(np.concatenate([prompts[s][0] for s in seqs])),
+                        h(np.concatenate([prompts[s][1] for s in seqs])))
+        hq = [prompt_q(wl, s) for s in seqs if cfgs[s]["method"] == "h2o"]
+        if hq:
+            c.h2o_prefill(h(np.concatenate(hq)))
+        rq = [prompt_q(wl, s, last=32) for s in seqs if cfgs[s]["method"] == "rocket"]
+        if rq:
+            c.snap_prefill(h(np.concatenate(rq)))
+        out = torch.empty((len(seqs), wl.n_q_heads, wl.head_dim), dtype=torch.float32, device="cuda")
+        res = {s: {"out": []} for s in seqs}
+        for t in range(steps):
+            kn, vn, q = ins[t]
+            c.append(h(kn[seqs]), h(vn[seqs]))
+            c.topk(h(q[seqs]))
+            c.attention(h(q[seqs]), out)
+            o = out.cpu().numpy()
+            for i, s in enumerate(seqs):
+                res[s]["out"].append(o[i].copy())
+                if cfgs[s]["method"] == "rocket":
+                    res[s][("topk", t)] = [c.export(i, hh, "topk") for hh in range(Hkv)]
+            c.evict()
+        for i, s in enumerate(seqs):
+            for what in ("positions", "codes_k", "codes_v", "scores"):
+                if what == "scores" and cfgs[s]["method"] != "h2o":
+                    continue
+                if what.startswith("codes") and cfgs[s]["method"] not in ("kvq", "uq"):
+                    continue
+                res[s][what] = [c.export(i, hh, what) for hh in range(Hkv)]
+        c.close()
+        return res
+
+    batch = run(list(range(S)))
+    for s in range(S):
+        solo = run([s])[s]
+        for key, val in solo.items():
+            for a, b in zip(batch[s][key], val):
+                np.testing.assert_array_equal(a, b, err_msg=f"sequence {s} ({cfgs[s]['name']}): {key}")
