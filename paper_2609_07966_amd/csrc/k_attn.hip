@@ -14,10 +14,10 @@
 // two codes (codebook entries are fp16 values); its key thresholds are folded into q and its
 // value scales into p, both of which are fp32: their fp16 rounding residual rides in the spare
 // columns G..2G-1 of the same product and is added back after it.  Outliers are sparse
-// corrections, applied without LDS atomics (which the LDS executes one lane at a time): a
-// batch's key outliers are loaded by the whole wave at once and gathered per token by lane
-// shuffles; value outliers accumulate in LDS rows private to each lane and are folded into the
-// output at the end.
+// corrections, applied without LDS atomics (measured slower here than plain read-modify-write):
+// the terms of a batch's key outliers are computed by the whole wave at once, one entry per
+// lane, and summed per token from LDS; value outliers accumulate in LDS rows private to each
+// lane and are folded into the output at the end.
 //
 // Uniform 4-bit tiles run the same matrix loop in an instantiation of their own: 4-bit codes
 // become exact fp16 integers, each 64-token block's key steps are folded into q, each token's
@@ -199,6 +199,7 @@ struct MKVQ {
   const float *cbk, *cbv;         // LDS codebooks
   const float *qq;                // LDS [D][2G]: scaled q of heads 0..G-1, then scaled q tau
   float *vcorr;                   // LDS [D]: this lane's value-outlier terms (head lr), relative to vref
+  float *kterm;                   // LDS [64][G]: this wave's per-entry key-outlier logit terms
   float *kcorr;                   // LDS [G + 1][32]: this wave's key-outlier logit terms of the
                                   // batch (row G stays zero)
   int lr, lq, rowbytes, nov, cap;
@@ -265,30 +266,43 @@ struct MKVQ {
     const uint32_t e = e0 + (threadIdx.x & 63);
     bt.ent = e < e1 ? gld(kout + e) : kNoOutlier;
   }
-  // Lane t < 32 sums, per head, q x - q' cb[code] over the outliers of slot base + t (each
-  // replaces its channel) and writes the sums to kcorr[head][t].
+  // Per head, the logit correction q x - q' cb[code] of every key outlier of the batch (each
+  // replaces its channel), summed per slot: lane e computes the terms of entry e of the batch's
+  // range (64 entries per round) into LDS, then lane t < 32 adds those of its slot's entries
+  // [k0, k1) and writes the sums to kcorr[head][t].
   MKV_DEV void batch_fix(const Batch &bt) const {
     const int lane = threadIdx.x & 63;
-    const uint32_t e0 = __builtin_amdgcn_readlane(bt.kr, 0);
+    const uint32_t e0 = __builtin_amdgcn_readlane(bt.kr, 0), e1 = __builtin_amdgcn_readlane(bt.kr, 32);
+    const int total = (int)(e1 - e0);  // wave-uniform
     const int k0 = (int)(bt.kr - e0);
-    const int k1 = (int)((uint32_t)__shfl_down((int)bt.kr, 1) - e0);
-    const int cnt = lane < 32 ? k1 - k0 : 0;
+    // every lane takes part in the shuffle (lane 31 reads lane 32); lanes >= 32 sum nothing
+    const int next = (int)((uint32_t)__shfl_down((int)bt.kr, 1) - e0);
+    const int k1 = lane < 32 ? next : k0;
     float acc[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) acc[g] = 0.f;
-    for (int i = 0; __any(i < cnt); ++i) {
-      const int src = k0 + i;
-      const bool on = i < cnt;
-      uint32_t ent = (uint32_t)__shfl((int)bt.ent, min(src, 63));
-      // entries past the 64 loaded by the wave (more than 64 in one batch) come from memory
-      if (__any(on && src >= 64)) {
-        if (on && src >= 64) ent = gld(kout + e0 + src);
-      }
-      // lanes without an entry this round read channel 0 and add nothing
+    for (int r0 = 0; r0 < total; r0 += 64) {
+      const bool on = r0 + lane < total;
+      uint32_t ent = bt.ent;
+      if (r0 > 0) ent = on ? gld(kout + e0 + r0 + lane) : kNoOutlier;  // more than 64 in one batch
+      // lanes without an entry compute with channel 0 and x = c = 0
       const int ch = on ? min(outlier_ch(ent), D - 1) : 0;
       const float x = on ? h2f(ent >> 16) : 0.f, c = on ? cbk[outlier_code(ent)] : 0.f;
 #pragma unroll
-      for (int g = 0; g < G; ++g) acc[g] += qq[ch * 2 * G + g] * x - qq[ch * 2 * G + G + g] * c;
+      for (int g = 0; g < G; ++g) kterm[lane * G + g] = qq[ch * 2 * G + g] * x - qq[ch * 2 * G + G + g] * c;
+      // this round's entries of slot t, four loads in flight per pass
+      const int a = max(k0 - r0, 0), b = min(k1 - r0, 64);
+      for (int i = a; i < b; i += 4) {
+        float t[4][G];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int g = 0; g < G; ++g) t[u][g] = kterm[min(i + u, 63) * G + g];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int g = 0; g < G; ++g) acc[g] += i + u < b ? t[u][g] : 0.f;
+      }
     }
     if (lane < 32) {
 #pragma unroll
@@ -770,6 +784,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   __shared__ uint32_t s_lut[2][256];         // KVQuant: key and value pair tables
   __shared__ float s_cb[2][16];              // KVQuant: codebooks
   __shared__ __attribute__((aligned(16))) float s_kc[NW][G + 1][32];  // KVQuant key-outlier logit terms
+  __shared__ __attribute__((aligned(16))) float s_kt[NW][64 * G];      // KVQuant per-entry key-outlier terms
   __shared__ float2 s_vm[NW][64];            // uniform 4-bit: a batch's value (min, step) pairs
   __shared__ __attribute__((aligned(16))) float s_km[NW][2 * D];  // uniform 4-bit: a key block's pairs
 
@@ -922,6 +937,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
       ld.cbv = s_cb[1];
       ld.qq = &s_q[0][0];
       ld.kcorr = &s_kc[wave][0][0];
+      ld.kterm = s_kt[wave];
       ld.vcorr = &s_wave[wave][(lq * G + (lr < G ? lr : 0)) * D];
       ld.lr = lr;
       ld.lq = lq;
