@@ -30,7 +30,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
 MALL_BYTES = 256 << 20
-ROOFLINE_KERNEL = "k_attn_partial_mx<128, 4, false>"
+ROOFLINE_KERNEL = "k_attn_partial_mx<128, 4>"
 # the sources the attention partial kernel is compiled from, and the committed counter record
 KERNEL_SOURCES = ("paper_2609_07966_amd/csrc/k_attn.hip", "paper_2609_07966_amd/csrc/kernels_common.h",
                   "paper_2609_07966_amd/csrc/mkv_internal.h")
@@ -78,17 +78,12 @@ def token_bytes(cfg, n0, step, D, G):
     return n * (D * b // 4 + 4 + 4 + 4 * nov + 4 * k_out)
 
 
-PART_OF = {"uq": "uq", "rocket": "rk"}
-
-
-def launch_bytes(wl, step, n_tiles, part="mx"):
-    """Algorithmic bytes of one partial launch: "mx" (fp16, H2O and KVQuant sequences), "rk"
-    (RocketKV) or "uq" (uniform 4-bit); `n_tiles` is that launch's workgroup count."""
+def launch_bytes(wl, step, n_tiles):
+    """Algorithmic bytes of one attention partial launch (all sequences' tiles; `n_tiles` is its
+    workgroup count)."""
     D, G, Hkv = wl.head_dim, wl.group, wl.n_kv_heads
     tot = 0.0
     for s in range(wl.n_seqs):
-        if PART_OF.get(wl.cfg(s)["method"], "mx") != part:
-            continue
         tot += Hkv * token_bytes(wl.cfg(s), wl.prompt_lens[s], step, D, G)
         tot += wl.n_q_heads * D * 2                     # q
     tot += n_tiles * G * (D + 2) * 4                    # partial (m, l, o) writes
@@ -166,13 +161,13 @@ def product_codebooks(wl, tokens=1024):
     return flat
 
 
-KIND_BITS = {"partial": 0, "combine": 1, "append": 2, "topk": 3, "evict": 4, "partial_uq": 5, "partial_rocket": 6}
+KIND_BITS = {"partial": 0, "combine": 1, "append": 2, "topk": 3, "evict": 4}
 
 
 def run_gpu(wl, steps, warmup, replicas=1, label="", prof_steps=24):
-    """Prefill, `warmup` untimed steps, `steps` timed steps (HIP events around the launches of the
-    partial kernel that carries the most bytes, and nothing else), then `prof_steps` steps with
-    every kernel kind timed (for the per-kernel breakdown only)."""
+    """Prefill, `warmup` untimed steps, `steps` timed steps (HIP events around the attention partial
+    launches, and nothing else), then `prof_steps` steps with every kernel kind timed (for the
+    per-kernel breakdown only)."""
     import torch
     from paper_2609_07966_amd import _lib
     from paper_2609_07966_amd.cache import KVCache
@@ -224,12 +219,7 @@ def run_gpu(wl, steps, warmup, replicas=1, label="", prof_steps=24):
         caches[t % replicas].step(kn[t], vn[t], qn[t], out)
     torch.cuda.synchronize()
     n_tiles, n_uq, n_rk = caches[0].n_tiles()
-    tiles_of = {"mx": n_tiles - n_uq - n_rk, "rk": n_rk, "uq": n_uq}
-    kind_of = {"mx": "partial", "rk": "partial_rocket", "uq": "partial_uq"}
-    # the partial launch that carries most of the bytes (the fp16-row / KVQuant one when the
-    # batch has such sequences)
-    part = max(("mx", "rk", "uq"), key=lambda p: launch_bytes(wl, warmup, tiles_of[p], p) if tiles_of[p] else -1)
-    kind = kind_of[part]
+    kind = "partial"
 
     def read_kinds(names):
         out = {}
@@ -262,17 +252,14 @@ def run_gpu(wl, steps, warmup, replicas=1, label="", prof_steps=24):
     kinds = read_kinds(KIND_BITS)
     for c in caches:
         _lib.mkv_profile_enable(c.h, 0, 0)
-    bytes_steps = [launch_bytes(wl, warmup + i, tiles_of[part], part) for i in range(steps)]
+    bytes_steps = [launch_bytes(wl, warmup + i, n_tiles) for i in range(steps)]
     avg_bytes = float(np.mean(bytes_steps))
-    all_bytes = float(np.mean([sum(launch_bytes(wl, warmup + i, tiles_of[p], p) for p in tiles_of)
-                               for i in range(steps)]))
-    part = kind
     avg_part_ms = ms_part / max(n_part, 1)
     res = {
         "steps": steps, "ms_per_step": elapsed / steps * 1e3, "steps_per_s": steps / elapsed,
-        "partial_kernel": part, "partial_ms": avg_part_ms, "partial_bytes": avg_bytes,
+        "partial_ms": avg_part_ms, "partial_bytes": avg_bytes,
         "partial_gbs": avg_bytes / (avg_part_ms * 1e-3) / 1e9,
-        "step_gbs": all_bytes / (elapsed / steps) / 1e9,
+        "step_gbs": avg_bytes / (elapsed / steps) / 1e9,
         "n_tiles": n_tiles, "n_tiles_uq": n_uq, "n_tiles_rocket": n_rk, "replicas": replicas,
         "kernel_ms": {k: (v[1] / max(v[0], 1)) for k, v in kinds.items() if v[0]},
     }
@@ -290,7 +277,7 @@ def per_config_runs(args):
              ("llama_layer", "KVQ2"), ("h2o", "H2O-20"), ("rocket", "Rocket-4096")]
     for name, cfg in cases:
         wl = make_workload(name, seed=args.seed, config_ids=cfg)
-        b1 = sum(launch_bytes(wl, 0, 0, p) for p in ("mx", "rk", "uq"))
+        b1 = launch_bytes(wl, 0, 0)
         reps = max(1, math.ceil(2 * MALL_BYTES / b1))
         r = run_gpu(wl, args.cfg_steps, 2, replicas=reps, label=f"{name}/{cfg}")
         runs.append({"workload": name, "config": cfg, "steps_per_s": round(r["steps_per_s"], 1),
@@ -383,7 +370,7 @@ def main():
     ceiling = None if args.no_per_config else read_ceiling_gbs()
     per_cfg = [] if args.no_per_config else per_config_runs(args)
     cpu = None if args.no_cpu else cpu_baseline(wl, args.cpu_steps)
-    traffic = recorded_traffic() if head["partial_kernel"] == "partial" else None
+    traffic = recorded_traffic()
     counts = {}
     for s in range(wl.n_seqs):
         counts[wl.cfg(s)["name"]] = counts.get(wl.cfg(s)["name"], 0) + 1
@@ -397,7 +384,7 @@ def main():
         "dtype": "f16 storage (fp16 / packed 2-4 bit codes), f32 compute",
         "data": "synthetic (seeded; workloads.gen)",
         "config": {"workload": "mixed: 64 seqs, 32q/8kv x 128, prompts log-uniform [1024, 32768], "
-                               "11 configs assigned uniformly (seed 0); per step: append, top-k, attention, eviction, with independent launches overlapped on 3 streams",
+                               "11 configs assigned uniformly (seed 0); per step: append, top-k, attention (one partial launch over all sequences + combine), eviction, on one stream",
                    "n_seqs": wl.n_seqs, "prompt_tokens": int(sum(wl.prompt_lens)), "configs": counts,
                    "parallelism": "single GPU"},
         "hbm_TBs_attention": round(head["partial_gbs"] / 1e3, 3),

@@ -16,13 +16,9 @@
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     Calls validate on the host, enqueue on `stream` and return without
  *     synchronising (mkv_export and mkv_fit_codebooks are synchronous).
- *     Inputs must stay live until the stream has consumed them.  Work that
- *     does not depend on the rest runs on two streams the handle owns
- *     (default priority), forked from `stream` and joined back into it: the
- *     top-k selection and RocketKV attention, and uniform 4-bit attention.
- *     mkv_decode_attention's output, and mkv_topk_select's pos_out when
- *     given, are ordered on `stream`; use one stream for the decode calls of
- *     a step.
+ *     Inputs must stay live until the stream has consumed them.  Every
+ *     kernel runs on `stream` itself (the library owns no streams or events
+ *     outside profiling); use one stream for the decode calls of a step.
  *   - A call that fails validation returns an error, enqueues nothing and
  *     leaves the handle unchanged; mkv_last_error() then describes it.
  *   - One host thread at a time per handle; distinct handles are independent.
@@ -240,19 +236,16 @@ mkv_status mkv_fit_codebooks(const uint16_t *k, const uint16_t *v, int32_t n_tok
  * microseconds of device time, so time a step's rate with the fewest kinds
  * selected.  mkv_profile_read waits for them and returns, for kind `kind`,
  * the launch count and the summed device time in milliseconds.  Kinds:
- * 0 attention partial of fp16, H2O and KVQ sequences, 1 attention combine,
- * 2 append, 3 top-k select, 4 H2O eviction, 5 attention partial of uniform
- * 4-bit sequences, 6 attention partial of RocketKV sequences (each partial
- * launch happens only when it has sequences).
+ * 0 attention partial (one launch over every sequence's tiles), 1 attention
+ * combine, 2 append, 3 top-k select, 4 H2O eviction.
  */
 mkv_status mkv_profile_enable(mkv_cache *cache, int32_t enable, int32_t max_launches);
 mkv_status mkv_profile_read(mkv_cache *cache, int32_t kind, int32_t *launches, double *total_ms);
 
 /*
- * Workgroups of the attention partial kernels per decode step: `n_tiles` in
+ * Workgroups of the attention partial launch per decode step: `n_tiles` in
  * all, of which `n_tiles_uq` (may be NULL) belong to uniform 4-bit sequences
- * and `n_tiles_rocket` (may be NULL) to RocketKV sequences; each group runs in
- * a launch of its own.
+ * and `n_tiles_rocket` (may be NULL) to RocketKV sequences.
  */
 mkv_status mkv_attention_tiles(mkv_cache *cache, int32_t *n_tiles, int32_t *n_tiles_uq,
                                int32_t *n_tiles_rocket);

@@ -19,9 +19,9 @@
 // lane, and summed per token from LDS; value outliers accumulate in LDS rows private to each
 // lane and are folded into the output at the end.
 //
-// Uniform 4-bit tiles run the same matrix loop in an instantiation of their own: 4-bit codes
-// become exact fp16 integers, each 64-token block's key steps are folded into q, each token's
-// value steps into p, and the minima enter as per-head bias terms.
+// Uniform 4-bit tiles run the same matrix loop: 4-bit codes become exact fp16 integers, each
+// 64-token block's key steps are folded into q, each token's value steps into p, and the minima
+// enter as per-head bias terms.
 //
 // Logits use the base-2 exponent (scaled by log2(e)/sqrt(d)).  fp16-row tiles keep the loads of
 // the next 16 tokens in flight while computing the current 16; the other paths issue the loads
@@ -727,9 +727,7 @@ MKV_DEV void wave_mfma(L &ld, int a, int b, QB<D> &qb, float qscale, float &m_ru
 }
 
 // ================================================================================================
-// The partial kernel, instantiated twice: UQK = false for fp16 rows, gathered rows and KVQuant,
-// UQK = true for uniform 4-bit tiles (kept apart so that neither's register budget limits the
-// other's occupancy).
+// The partial kernel: one launch over the tiles of every sequence, whatever its method.
 // ================================================================================================
 // Contiguous token range [a, b) of this wave within its tile, a multiple of 32 tokens.
 struct WaveRange {
@@ -769,15 +767,15 @@ MKV_DEV void merge_waves(const float *red, int wstride, float *dst) {
   }
 }
 
-template <int D, int G, bool UQK>
+template <int D, int G>
 __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     const SeqDesc *__restrict__ seqs, const int32_t *__restrict__ state, const int4 *__restrict__ tiles,
     const uint16_t *__restrict__ q, float *__restrict__ partials, const float *__restrict__ cbtab,
-    int Hkv, float qscale, int tile_base) {
+    int Hkv, float qscale) {
   constexpr int NW = kTileThreads / 64, NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
   // per wave: KVQuant value-outlier terms, one row of D per (lane quad, head) while the wave
   // runs; then the wave's (max, sum, o) for the merge
-  constexpr int kWaveFloats = UQK ? G * (D + 2) : 4 * G * D;
+  constexpr int kWaveFloats = 4 * G * D;
   static_assert(kWaveFloats >= G * (D + 2), "wave region too small");
   __shared__ __attribute__((aligned(16))) float s_wave[NW][kWaveFloats];
   __shared__ float s_q[D][2 * G];            // KVQuant: scaled q of each head, then scaled q * tau
@@ -788,7 +786,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   __shared__ float2 s_vm[NW][64];            // uniform 4-bit: a batch's value (min, step) pairs
   __shared__ __attribute__((aligned(16))) float s_km[NW][2 * D];  // uniform 4-bit: a key block's pairs
 
-  const int tid = tile_base + blockIdx.x;
+  const int tid = blockIdx.x;
   const int4 tile = tiles[tid];
   const int seq = tile.x, h = tile.y;
   const SeqDesc &sd = seqs[seq];
@@ -800,9 +798,9 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   const uint16_t *qh = q + ((size_t)seq * Hq + h * G) * D;
   const WaveRange wr = wave_range(tile.z, min(tile.w, n_act), wave, NW);
   const int lr = lane & 15, lq = lane >> 4;
-  const bool kvq = !UQK && method == KVQ;
-  constexpr bool uq = UQK;
-  if constexpr (uq) {
+  const bool kvq = method == KVQ;
+  const bool uq = method == UQ;
+  if (uq) {
     for (int e = threadIdx.x; e < G * D; e += kTileThreads) {
       const int g = e / D, c = e % D;
       s_q[c][g] = h2f(qh[(size_t)g * D + c]) * qscale;
@@ -902,7 +900,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
       uq_om[gr] = v;
     }
   };
-  if constexpr (UQK) {
+  if (uq) {
     run_uq();
   } else if (method == FP16 || method == H2O) {
     MRows<D, G, false> ld;
@@ -975,7 +973,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
 #pragma unroll
       for (int i = 0; i < 4; ++i) O[m][i] += mirror_cols<G>(O[m][i]);
   }
-  if constexpr (uq) {
+  if (uq) {
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
@@ -1111,20 +1109,11 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
 }
 
 template <int D, int G>
-hipError_t partial_impl(const Dev &dv, const Shape &sh, const uint16_t *q, int part, hipStream_t st) {
+hipError_t partial_impl(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st) {
   const float qscale = kLog2e / sqrtf((float)D);
-  // tile groups: [fp16-row and KVQuant][RocketKV][uniform 4-bit]
-  const int n_main = dv.n_tiles - dv.n_tiles_uq - dv.n_tiles_rk;
-  if (part == 0 && n_main > 0)
-    hipLaunchKernelGGL((k_attn_partial_mx<D, G, false>), dim3(n_main), dim3(kTileThreads), 0, st, dv.seqs,
-                       dv.state, dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale, 0);
-  if (part == 2 && dv.n_tiles_rk > 0)
-    hipLaunchKernelGGL((k_attn_partial_mx<D, G, false>), dim3(dv.n_tiles_rk), dim3(kTileThreads), 0, st,
-                       dv.seqs, dv.state, dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale, n_main);
-  if (part == 1 && dv.n_tiles_uq > 0)
-    hipLaunchKernelGGL((k_attn_partial_mx<D, G, true>), dim3(dv.n_tiles_uq), dim3(kTileThreads), 0, st,
-                       dv.seqs, dv.state, dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale,
-                       n_main + dv.n_tiles_rk);
+  if (dv.n_tiles > 0)
+    hipLaunchKernelGGL((k_attn_partial_mx<D, G>), dim3(dv.n_tiles), dim3(kTileThreads), 0, st, dv.seqs,
+                       dv.state, dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale);
   return hipGetLastError();
 }
 
@@ -1150,8 +1139,8 @@ hipError_t combine_impl(const Dev &dv, const Shape &sh, float *out, hipStream_t 
     default: return hipErrorInvalidValue;                                     \
   }
 
-hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, int part, hipStream_t st) {
-  MKV_DISPATCH_DG(partial_impl, dv, sh, q, part, st)
+hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st) {
+  MKV_DISPATCH_DG(partial_impl, dv, sh, q, st)
 }
 
 hipError_t launch_attention_combine(const Dev &dv, const Shape &sh, float *out, hipStream_t st) {

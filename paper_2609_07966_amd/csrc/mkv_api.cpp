@@ -35,7 +35,7 @@ mkv_status hip_fail(hipError_t e, const char *what) {
 
 enum Phase { PH_CREATED, PH_PROMPT, PH_READY, PH_APPENDED, PH_SELECTED, PH_ATTENDED };
 
-constexpr int kProfKinds = 7;
+constexpr int kProfKinds = 5;
 
 struct Layout {
   std::vector<SeqDesc> seqs;  // offsets (relative to the arena) in the pointer fields
@@ -212,15 +212,14 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
     }
   }
   // attention tiles: per sequence and kv head, ranges of `chunk` tokens over its largest active set;
-  // grouped for three launches: fp16-row / KVQ sequences, then RocketKV sequences (after the
-  // top-k), then uniform 4-bit sequences (their own kernel instantiation)
+  // one launch covers them all, RocketKV sequences last (their gathered tiles are the shortest)
   L->tiles.clear();
   L->n_tiles_uq = 0;
   L->n_tiles_rk = 0;
-  for (int pass = 0; pass < 3; ++pass)
+  for (int pass = 0; pass < 2; ++pass)
   for (int s = 0; s < S; ++s) {
     SeqDesc &d = L->seqs[s];
-    const int grp = d.method == UQ ? 2 : d.method == ROCKET ? 1 : 0;
+    const int grp = d.method == ROCKET ? 1 : 0;
     if (grp != pass) continue;
     const int amax = d.method == ROCKET ? d.topk : d.cap;
     d.chunk = tile_tokens(d, D);
@@ -233,7 +232,7 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
     for (int h = 0; h < Hkv; ++h)
       for (int t = 0; t < d.tile_count; ++t)
         L->tiles.push_back(make_int4(s, h, t * d.chunk, std::min(amax, (t + 1) * d.chunk)));
-    if (pass == 2) L->n_tiles_uq += Hkv * d.tile_count;
+    if (d.method == UQ) L->n_tiles_uq += Hkv * d.tile_count;
     if (pass == 1) L->n_tiles_rk += Hkv * d.tile_count;
   }
   L->n_tiles = (int)L->tiles.size();
@@ -259,9 +258,6 @@ struct mkv_cache {
   int h2o_rows = 0, rocket_rows = 0;
   // independent kernels overlap on two library streams (default priority), forked from and joined
   // into the caller's stream: [0] top-k and RocketKV attention, [1] uniform 4-bit attention
-  hipStream_t aux[2] = {nullptr, nullptr};
-  hipEvent_t ev_fork = nullptr, ev_sel = nullptr, ev_done[2] = {nullptr, nullptr};
-  bool sel_pending = false;  // top-k work on aux[0] not yet joined into a caller stream
   // profiling
   int prof_mask = 0;  // bit k: launches of kind k are timed
   int prof_cap = 0;
@@ -383,14 +379,8 @@ mkv_status mkv_cache_create(const mkv_shape *shape, const mkv_config *cfg, const
   c->dv.n_tiles_uq = L.n_tiles_uq;
   c->dv.n_tiles_rk = L.n_tiles_rk;
   hipStream_t hst = static_cast<hipStream_t>(stream);
-  hipError_t e = hipSuccess;
-  for (int i = 0; i < 2 && e == hipSuccess; ++i) e = hipStreamCreateWithFlags(&c->aux[i], hipStreamNonBlocking);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_sel, hipEventDisableTiming);
-  for (int i = 0; i < 2 && e == hipSuccess; ++i) e = hipEventCreateWithFlags(&c->ev_done[i], hipEventDisableTiming);
-  if (e == hipSuccess)
-    e = hipMemcpyAsync(c->arena + L.off_seqs, c->hs.data(), sizeof(SeqDesc) * c->hs.size(),
-                       hipMemcpyHostToDevice, hst);
+  hipError_t e = hipMemcpyAsync(c->arena + L.off_seqs, c->hs.data(), sizeof(SeqDesc) * c->hs.size(),
+                                hipMemcpyHostToDevice, hst);
   if (e == hipSuccess)
     e = hipMemcpyAsync(c->arena + L.off_tiles, L.tiles.data(), sizeof(int4) * L.tiles.size(),
                        hipMemcpyHostToDevice, hst);
@@ -408,13 +398,6 @@ mkv_status mkv_cache_create(const mkv_shape *shape, const mkv_config *cfg, const
 
 mkv_status mkv_cache_destroy(mkv_cache *c) {
   if (!c) return MKV_OK;
-  for (hipStream_t s : c->aux)
-    if (s) {
-      hipStreamSynchronize(s);
-      hipStreamDestroy(s);
-    }
-  for (hipEvent_t e : {c->ev_fork, c->ev_sel, c->ev_done[0], c->ev_done[1]})
-    if (e) hipEventDestroy(e);
   for (int k = 0; k < kProfKinds; ++k)
     for (int w = 0; w < 2; ++w)
       for (hipEvent_t e : c->ev[k][w]) hipEventDestroy(e);
@@ -510,21 +493,10 @@ mkv_status mkv_topk_select(mkv_cache *c, const uint16_t *q, int32_t *pos_out, vo
   if (c->any_rocket) {
     if (!q) return fail(MKV_EINVAL, "q is NULL");
     hipStream_t hst = static_cast<hipStream_t>(stream);
-    // runs on aux[0] after the work already in `stream`; the attention call joins it back, or
-    // this call does when the caller asks for the positions
-    hipError_t e = hipEventRecord(c->ev_fork, hst);
-    if (e == hipSuccess) e = hipStreamWaitEvent(c->aux[0], c->ev_fork, 0);
-    if (e != hipSuccess) return hip_fail(e, "top-k fork");
-    prof_mark(c, 3, 0, c->aux[0]);
-    e = launch_topk(c->dv, c->sh, q, pos_out, c->topk_max, c->aux[0]);
-    prof_mark(c, 3, 1, c->aux[0]);
+    prof_mark(c, 3, 0, hst);
+    const hipError_t e = launch_topk(c->dv, c->sh, q, pos_out, c->topk_max, hst);
+    prof_mark(c, 3, 1, hst);
     if (e != hipSuccess) return hip_fail(e, "top-k select");
-    c->sel_pending = true;
-    if (pos_out != nullptr) {
-      e = hipEventRecord(c->ev_sel, c->aux[0]);
-      if (e == hipSuccess) e = hipStreamWaitEvent(hst, c->ev_sel, 0);
-      if (e != hipSuccess) return hip_fail(e, "top-k join");
-    }
   }
   c->phase = PH_SELECTED;
   return MKV_OK;
@@ -536,42 +508,11 @@ mkv_status mkv_decode_attention(mkv_cache *c, const uint16_t *q, float *out, voi
   if (!(c->phase == PH_SELECTED || (c->phase == PH_APPENDED && !c->any_rocket)))
     return fail(MKV_ESTATE, "attention must follow the decode append (and top-k selection)");
   hipStream_t hst = static_cast<hipStream_t>(stream);
-  const Dev &dv = c->dv;
-  const int n_main = dv.n_tiles - dv.n_tiles_uq - dv.n_tiles_rk;
-  // three independent partial launches: uniform 4-bit on aux[1], RocketKV on aux[0] (after its
-  // top-k), the rest on `stream`; the combine waits for all of them
-  hipError_t e = hipEventRecord(c->ev_fork, hst);
-  if (e != hipSuccess) return hip_fail(e, "attention fork");
-  if (dv.n_tiles_uq > 0) {
-    if ((e = hipStreamWaitEvent(c->aux[1], c->ev_fork, 0)) != hipSuccess) return hip_fail(e, "attention fork");
-    prof_mark(c, 5, 0, c->aux[1]);
-    e = launch_attention_partial(dv, c->sh, q, 1, c->aux[1]);
-    prof_mark(c, 5, 1, c->aux[1]);
-    if (e != hipSuccess) return hip_fail(e, "attention partial (uniform)");
-    if ((e = hipEventRecord(c->ev_done[1], c->aux[1])) != hipSuccess) return hip_fail(e, "attention join");
-  }
-  if (dv.n_tiles_rk > 0 || c->sel_pending) {
-    if (!c->sel_pending && (e = hipStreamWaitEvent(c->aux[0], c->ev_fork, 0)) != hipSuccess)
-      return hip_fail(e, "attention fork");
-    if (dv.n_tiles_rk > 0) {
-      prof_mark(c, 6, 0, c->aux[0]);
-      e = launch_attention_partial(dv, c->sh, q, 2, c->aux[0]);
-      prof_mark(c, 6, 1, c->aux[0]);
-      if (e != hipSuccess) return hip_fail(e, "attention partial (RocketKV)");
-    }
-    if ((e = hipEventRecord(c->ev_done[0], c->aux[0])) != hipSuccess) return hip_fail(e, "attention join");
-  }
-  if (n_main > 0) {
-    prof_mark(c, 0, 0, hst);
-    e = launch_attention_partial(dv, c->sh, q, 0, hst);
-    prof_mark(c, 0, 1, hst);
-    if (e != hipSuccess) return hip_fail(e, "attention partial");
-  }
-  if (dv.n_tiles_uq > 0 && (e = hipStreamWaitEvent(hst, c->ev_done[1], 0)) != hipSuccess)
-    return hip_fail(e, "attention join");
-  if ((dv.n_tiles_rk > 0 || c->sel_pending) && (e = hipStreamWaitEvent(hst, c->ev_done[0], 0)) != hipSuccess)
-    return hip_fail(e, "attention join");
-  c->sel_pending = false;
+  // one partial launch over the tiles of every sequence, then the combine
+  prof_mark(c, 0, 0, hst);
+  hipError_t e = launch_attention_partial(c->dv, c->sh, q, hst);
+  prof_mark(c, 0, 1, hst);
+  if (e != hipSuccess) return hip_fail(e, "attention partial");
   prof_mark(c, 1, 0, hst);
   e = launch_attention_combine(c->dv, c->sh, out, hst);
   prof_mark(c, 1, 1, hst);

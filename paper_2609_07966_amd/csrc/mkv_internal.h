@@ -112,16 +112,15 @@ struct Dev {
   float *partials;       // device [n_tiles][G][D+2]
   const float *cbtab;    // device [kCbTableFloats]
   int n_tiles;
-  int n_tiles_uq;        // the last n_tiles_uq tiles belong to uniform 4-bit sequences
-  int n_tiles_rk;        // the n_tiles_rk tiles before them belong to RocketKV sequences
+  int n_tiles_uq;        // tiles of uniform 4-bit sequences (reported, not used by the launches)
+  int n_tiles_rk;        // the last n_tiles_rk tiles belong to RocketKV sequences
 };
 
 hipError_t launch_append_decode(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
                                 hipStream_t st);
 hipError_t launch_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
                               const uint16_t *k, const uint16_t *v, hipStream_t st);
-// part 0: fp16-row and KVQuant tiles; part 1: uniform 4-bit tiles; part 2: RocketKV tiles.
-hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, int part, hipStream_t st);
+hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st);
 hipError_t launch_attention_combine(const Dev &dv, const Shape &sh, float *out, hipStream_t st);
 hipError_t launch_topk(const Dev &dv, const Shape &sh, const uint16_t *q, int32_t *pos_out, int topk_max,
                        hipStream_t st);
