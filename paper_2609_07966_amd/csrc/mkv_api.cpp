@@ -48,17 +48,27 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 constexpr int kMaxTiles = 32;  // per (sequence, kv head); the combine kernel holds up to 64
 
-int tile_tokens(const SeqDesc &s, int D) {
-  // bytes each token costs the attention pass; tiles carry about 64 KiB
-  double bpt;
+// Bytes each token costs the attention pass.
+double token_bytes(const SeqDesc &s, int D) {
   switch (s.method) {
-    case UQ: bpt = D + D / 64.0 * 8 + 8; break;
-    case KVQ: bpt = D * s.bits / 4.0 + 4 + 8 + 4; break;
-    default: bpt = 4.0 * D; break;
+    case UQ: return D + D / 64.0 * 8 + 8;
+    case KVQ: return D * s.bits / 4.0 + 4 + 8 + 4;
+    default: return 4.0 * D;
   }
-  int t = (int)(65536.0 / bpt) & ~63;
-  if (const char *e = getenv("MKV_TILE_TOKENS")) t = atoi(e) & ~63;
+}
+
+// Tokens per attention tile for a tile of about `tile_bytes`.
+int tile_tokens(const SeqDesc &s, int D, double tile_bytes) {
+  const int t = (int)(tile_bytes / token_bytes(s, D)) & ~63;
   return std::max(64, std::min(t, 4096));
+}
+
+// Tile size: large tiles amortise each workgroup's set-up, but a launch needs several
+// workgroups per slot (256 CUs x 3 resident workgroups) to balance: about 4 rounds, within
+// 64 to 192 KiB (measured best for batches of ~40 MB and ~600 MB per step).
+double tile_bytes_for(double total_bytes) {
+  constexpr double kSlots = 256 * 3, kRounds = 4;
+  return std::min(196608.0, std::max(65536.0, total_bytes / (kSlots * kRounds)));
 }
 
 mkv_status check_shape(const mkv_shape *sh) {
@@ -216,13 +226,19 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
   L->tiles.clear();
   L->n_tiles_uq = 0;
   L->n_tiles_rk = 0;
+  double total = 0.0;
+  for (int s = 0; s < S; ++s) {
+    const SeqDesc &d = L->seqs[s];
+    total += (double)Hkv * (d.method == ROCKET ? d.topk : d.cap) * token_bytes(d, D);
+  }
+  const double tile_bytes = tile_bytes_for(total);
   for (int pass = 0; pass < 2; ++pass)
   for (int s = 0; s < S; ++s) {
     SeqDesc &d = L->seqs[s];
     const int grp = d.method == ROCKET ? 1 : 0;
     if (grp != pass) continue;
     const int amax = d.method == ROCKET ? d.topk : d.cap;
-    d.chunk = tile_tokens(d, D);
+    d.chunk = tile_tokens(d, D, tile_bytes);
     d.tile_count = std::max(1, (amax + d.chunk - 1) / d.chunk);
     if (d.tile_count > kMaxTiles) {  // long sequences: fewer, larger tiles keep the combine short
       d.chunk = (((amax + kMaxTiles - 1) / kMaxTiles) + 63) & ~63;
