@@ -36,6 +36,68 @@ MKV_DEV int compact_ascending(int n, Flag flag, IsEq is_eq, Emit emit, int *s_tm
 }
 
 // ---- RocketKV decode top-k ---------------------------------------------------------------------
+// Radix select of the k-th largest of n keys (4 passes of 8 bits) for a workgroup of NT threads:
+// one histogram per wave, two sets used in turn so that the set of the next pass is cleared
+// while wave 0 searches the digit of this one (2 barriers per pass).  hist[0] must be zero and
+// visible on entry.  Returns the k-th key, how many keys equal it and how many of those are needed.
+template <int NTH, typename Get>
+MKV_DEV void topk_radix(int n, int k, Get get, int (*hist)[NTH / 64][256], int *s3, uint32_t *kth, int *n_equal,
+                        int *need) {
+  constexpr int NWV = NTH / 64;
+  const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  uint32_t prefix = 0, mask = 0;
+  int remaining = k, eq = 0;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int buf = pass & 1, shift = 24 - 8 * pass;
+    for (int i = threadIdx.x; i < n; i += NTH) {
+      const uint32_t key = get(i);
+      if ((key & mask) == prefix) atomicAdd(&hist[buf][wid][(key >> shift) & 255u], 1);
+    }
+    __syncthreads();
+    if (wid == 0) {
+      // lane l owns digits 255 - 4l .. 252 - 4l (descending), so the exclusive scan over lanes
+      // gives the count of larger digits
+      int cnt[4], tot = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int d = 255 - (4 * lane + i);
+        int c = 0;
+#pragma unroll
+        for (int w = 0; w < NWV; ++w) c += hist[buf][w][d];
+        cnt[i] = c;
+        tot += c;
+      }
+      int inc = tot;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(inc, o);
+        if (lane >= o) inc += y;
+      }
+      int above = inc - tot;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (above < remaining && remaining <= above + cnt[i]) {
+          s3[0] = 255 - (4 * lane + i);
+          s3[1] = remaining - above;
+          s3[2] = cnt[i];
+        }
+        above += cnt[i];
+      }
+    } else {
+      for (int e = threadIdx.x - 64; e < NWV * 256; e += NTH - 64) (&hist[buf ^ 1][0][0])[e] = 0;
+    }
+    __syncthreads();
+    prefix |= (uint32_t)s3[0] << shift;
+    mask |= 255u << shift;
+    remaining = s3[1];
+    eq = s3[2];
+  }
+  *kth = prefix;
+  *n_equal = eq;
+  *need = remaining;
+}
+
+
 // One workgroup of 1024 threads per (sequence, kv head): a kept set of up to a few thousand
 // tokens is scored with ~4 tokens per thread and selected by radix passes over LDS keys.
 constexpr int kTopkThreads = 1024;
@@ -46,7 +108,8 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(const SeqDesc *__restrict
   __shared__ float s_a[D];
   __shared__ float s_qb[D];
   __shared__ int s_ch[D];
-  __shared__ int whist[kTopkThreads / 64][256];
+  __shared__ int s_beats[kTopkThreads];
+  __shared__ int whist[2][kTopkThreads / 64][256];
   __shared__ int s3[3];
   __shared__ int s_tmp[kTopkThreads / 64];
   __shared__ uint32_t s_keys[kTopkLdsKeys];
@@ -76,15 +139,28 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(const SeqDesc *__restrict
   }
   __syncthreads();
   const int nch = min(sd.nch, D);
-  // channel c is selected iff fewer than nch channels beat it (larger a, or equal a and lower index)
-  for (int c = threadIdx.x; c < D; c += kTopkThreads) {
+  // channel c is selected iff fewer than nch channels beat it (larger a, or equal a and lower
+  // index); the kTopkThreads / D threads of channel c each count a slice of the others
+  {
+    static_assert(kTopkThreads % D == 0, "whole slices per channel");
+    constexpr int P = kTopkThreads / D, W = D / P;
+    const int c = threadIdx.x % D, part = threadIdx.x / D;
     const float a = s_a[c];
     int beats = 0;
-    for (int c2 = 0; c2 < D; ++c2) {
+#pragma unroll
+    for (int i = 0; i < W; ++i) {
+      const int c2 = part * W + i;
       const float b = s_a[c2];
       beats += (b > a || (b == a && c2 < c)) ? 1 : 0;
     }
-    s_ch[c] = beats < nch ? 1 : 0;
+    s_beats[threadIdx.x] = beats;
+  }
+  __syncthreads();
+  if (threadIdx.x < D) {
+    int t = 0;
+#pragma unroll
+    for (int p = 0; p < kTopkThreads / D; ++p) t += s_beats[p * D + threadIdx.x];
+    s_ch[threadIdx.x] = t < nch ? 1 : 0;
   }
   __syncthreads();
   __shared__ int s_sel_ch[D];
@@ -158,11 +234,12 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(const SeqDesc *__restrict
       }
     }
   }
+  for (int e = threadIdx.x; e < (kTopkThreads / 64) * 256; e += kTopkThreads) (&whist[0][0][0])[e] = 0;
   __syncthreads();
   auto getk = [&](int i) { return in_lds ? s_keys[i] : gld(akeys + i); };
   uint32_t kth;
   int n_eq, need;
-  radix_select_kth_waves<kTopkThreads>(n, k, getk, whist, s3, s_tmp, &kth, &n_eq, &need);
+  topk_radix<kTopkThreads>(n, k, getk, whist, s3, &kth, &n_eq, &need);
   // each thread takes a contiguous run of tokens; counts of keys above and equal to the
   // threshold before its run place its selected tokens in ascending order
   const int per = (n + kTopkThreads - 1) / kTopkThreads;
@@ -173,9 +250,16 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(const SeqDesc *__restrict
     gt += kk > kth ? 1 : 0;
     eq += kk == kth ? 1 : 0;
   }
-  int tot;
-  const int gt_before = block_exclusive_scan<kTopkThreads>(gt, s_tmp, &tot);
-  int eq_run = block_exclusive_scan<kTopkThreads>(eq, s_tmp, &tot);
+  // one scan of both counts when n < 2^15 keeps them apart in the two halves of a word
+  int tot, gt_before, eq_run;
+  if (n < 32768) {
+    const int both = block_exclusive_scan<kTopkThreads>((gt << 16) | eq, s_tmp, &tot);
+    gt_before = both >> 16;
+    eq_run = both & 0xFFFF;
+  } else {
+    gt_before = block_exclusive_scan<kTopkThreads>(gt, s_tmp, &tot);
+    eq_run = block_exclusive_scan<kTopkThreads>(eq, s_tmp, &tot);
+  }
   int slot = gt_before + min(eq_run, need);
   for (int j = ja; j < jb; ++j) {
     const uint32_t kk = getk(j);
