@@ -161,7 +161,7 @@ def product_codebooks(wl, tokens=1024):
     return flat
 
 
-KIND_BITS = {"partial": 0, "combine": 1, "append": 2, "topk": 3, "evict": 4}
+KIND_BITS = {"partial": 0, "combine": 1, "append": 2, "topk": 3}
 
 
 def run_gpu(wl, steps, warmup, replicas=1, label="", prof_steps=24):

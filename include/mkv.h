@@ -143,7 +143,10 @@ mkv_status mkv_append_quantize(mkv_cache *cache, const uint16_t *k, const uint16
  * tie).
  * After each decode mkv_decode_attention, with q_prompt = NULL: if a kv head
  * holds more than B tokens, evict the lowest-score token among those older
- * than the floor(B/2) most recent (older wins a tie).
+ * than the floor(B/2) most recent (older wins a tie).  The attention pass has
+ * already chosen that token; this call removes it from the retained set
+ * (mkv_export no longer reports it) and enqueues nothing: the next decode
+ * append writes its token into the freed slot.
  * A no-op when no sequence uses H2O.
  */
 mkv_status mkv_h2o_update_evict(mkv_cache *cache, const uint16_t *q_prompt, void *stream);
@@ -237,7 +240,7 @@ mkv_status mkv_fit_codebooks(const uint16_t *k, const uint16_t *v, int32_t n_tok
  * selected.  mkv_profile_read waits for them and returns, for kind `kind`,
  * the launch count and the summed device time in milliseconds.  Kinds:
  * 0 attention partial (one launch over every sequence's tiles), 1 attention
- * combine, 2 append, 3 top-k select, 4 H2O eviction.
+ * combine, 2 append, 3 top-k select.
  */
 mkv_status mkv_profile_enable(mkv_cache *cache, int32_t enable, int32_t max_launches);
 mkv_status mkv_profile_read(mkv_cache *cache, int32_t kind, int32_t *launches, double *total_ms);

@@ -194,7 +194,7 @@ template <int D>
 __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict__ seqs, int32_t *state,
                                                       const uint16_t *__restrict__ k,
                                                       const uint16_t *__restrict__ v,
-                                                      const float *__restrict__ cbtab, int Hkv) {
+                                                      const float *__restrict__ cbtab, int Hkv, int apply_evict) {
   __shared__ float s_abs[D];
   __shared__ float s_scale;
   __shared__ uint8_t s_code[D];
@@ -215,15 +215,20 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
       break;
     }
     case H2O: {
-      const int slot = st[ST_FREE_SLOT];
+      // an eviction decided by the last attention pass (and confirmed by the eviction call)
+      // frees its slot for this token; otherwise the token goes to the end
+      const int victim = apply_evict ? st[ST_VICTIM] : -1;
+      const int slot = victim >= 0 ? victim : st[ST_FREE_SLOT];
+      const int new_count = victim >= 0 ? count : count + 1;
       (reinterpret_cast<uint16_t *>(sd.k) + h * stride_rows(sd, D))[(size_t)slot * D + c] = (uint16_t)kb;
       (reinterpret_cast<uint16_t *>(sd.v) + h * stride_rows(sd, D))[(size_t)slot * D + c] = (uint16_t)vb;
       __syncthreads();
       if (c == 0) {
         (reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd))[slot] = pos;
         (reinterpret_cast<float *>(sd.score) + h * stride_slots(sd))[slot] = 0.f;
-        st[ST_COUNT] = count + 1;
-        st[ST_FREE_SLOT] = count + 1;
+        st[ST_COUNT] = new_count;
+        st[ST_FREE_SLOT] = new_count;
+        st[ST_VICTIM] = -1;
       }
       break;
     }
@@ -470,9 +475,9 @@ __global__ void k_init_state(int32_t *state, int n) {
 
 template <int D>
 hipError_t append_decode_impl(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
-                              hipStream_t st) {
+                              int apply_evict, hipStream_t st) {
   hipLaunchKernelGGL(k_append_decode<D>, dim3(sh.S * sh.Hkv), dim3(D), 0, st, dv.seqs, dv.state, k, v,
-                     dv.cbtab, sh.Hkv);
+                     dv.cbtab, sh.Hkv, apply_evict);
   return hipGetLastError();
 }
 
@@ -515,8 +520,9 @@ hipError_t prefill_impl(const Dev &dv, const Shape &sh, const SeqDesc &hs, int s
 }  // namespace
 
 hipError_t launch_append_decode(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
-                                hipStream_t st) {
-  return sh.D == 64 ? append_decode_impl<64>(dv, sh, k, v, st) : append_decode_impl<128>(dv, sh, k, v, st);
+                                int apply_evict, hipStream_t st) {
+  return sh.D == 64 ? append_decode_impl<64>(dv, sh, k, v, apply_evict, st)
+                    : append_decode_impl<128>(dv, sh, k, v, apply_evict, st);
 }
 
 hipError_t launch_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq, const uint16_t *k,

@@ -1063,10 +1063,12 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
   }
   if (sd.method == H2O) {
     // accumulate, and find the eviction candidate (lowest score among positions older than the
-    // R most recent, lower position on a tie) for the eviction call to apply
+    // R most recent, lower position on a tie); the next decode append writes its token there
     int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
     const int count = st[ST_COUNT];
     const int limit = st[ST_NEXT_POS] - 1 - sd.R + 1;
+    // no victim unless one is found below (the barrier of the search orders this write first)
+    if (threadIdx.x == 0) st[ST_VICTIM] = -1;
     const float *lg = reinterpret_cast<const float *>(sd.logits) + h * stride_logits(sd, G);
     float *score = reinterpret_cast<float *>(sd.score) + h * stride_slots(sd);
     const int32_t *pos = reinterpret_cast<const int32_t *>(sd.pos) + h * stride_slots(sd);

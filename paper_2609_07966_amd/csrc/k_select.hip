@@ -275,27 +275,6 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(const SeqDesc *__restrict
   if (threadIdx.x == 0) st[ST_SEL_COUNT] = k;
 }
 
-// ---- H2O decode eviction ------------------------------------------------------------------------
-// The attention combine pass has already accumulated the scores and picked the victim slot (the
-// lowest score among positions older than the R most recent, lower position on a tie); this
-// applies it.  One thread per (sequence, kv head).
-__global__ __launch_bounds__(64) void k_h2o_evict(const SeqDesc *__restrict__ seqs, int32_t *state, int Hkv,
-                                                  int n_pairs) {
-  const int i = blockIdx.x * 64 + (int)threadIdx.x;
-  if (i >= n_pairs) return;
-  const int seq = i / Hkv, h = i % Hkv;
-  const SeqDesc &sd = seqs[seq];
-  if (sd.method != H2O) return;
-  int32_t *st = state + (size_t)i * ST_WORDS;
-  const int count = st[ST_COUNT];
-  if (count <= sd.B) return;
-  const int slot = st[ST_VICTIM];
-  if (slot < 0 || slot >= count) return;
-  gst(reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd) + slot, -1);
-  st[ST_FREE_SLOT] = slot;
-  st[ST_COUNT] = count - 1;
-}
-
 // ---- causal prefill attention statistics (shared by H2O scoring) ---------------------------------
 // Tiles of 64 query rows x 64 keys; 256 threads as 16 x 16, each owning 4 rows x 4 keys.
 constexpr int TB = 64;
@@ -707,12 +686,6 @@ hipError_t launch_topk(const Dev &dv, const Shape &sh, const uint16_t *q, int32_
     case 128 * 16 + 8: return topk_impl<128, 8>(dv, sh, q, pos_out, topk_max, st);
     default: return hipErrorInvalidValue;
   }
-}
-
-hipError_t launch_h2o_evict(const Dev &dv, const Shape &sh, hipStream_t st) {
-  const int n_pairs = sh.S * sh.Hkv;
-  hipLaunchKernelGGL(k_h2o_evict, dim3((n_pairs + 63) / 64), dim3(64), 0, st, dv.seqs, dv.state, sh.Hkv, n_pairs);
-  return hipGetLastError();
 }
 
 hipError_t launch_h2o_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,

@@ -35,7 +35,7 @@ mkv_status hip_fail(hipError_t e, const char *what) {
 
 enum Phase { PH_CREATED, PH_PROMPT, PH_READY, PH_APPENDED, PH_SELECTED, PH_ATTENDED };
 
-constexpr int kProfKinds = 5;
+constexpr int kProfKinds = 4;
 
 struct Layout {
   std::vector<SeqDesc> seqs;  // offsets (relative to the arena) in the pointer fields
@@ -275,6 +275,7 @@ struct mkv_cache {
   // independent kernels overlap on two library streams (default priority), forked from and joined
   // into the caller's stream: [0] top-k and RocketKV attention, [1] uniform 4-bit attention
   // profiling
+  bool evict_pending = false;  // H2O: the last eviction call's victims await the next decode append
   int prof_mask = 0;  // bit k: launches of kind k are timed
   int prof_cap = 0;
   std::vector<hipEvent_t> ev[kProfKinds][2];
@@ -449,9 +450,10 @@ mkv_status mkv_append_quantize(mkv_cache *c, const uint16_t *k, const uint16_t *
   if (c->steps >= c->sh.max_new)
     return fail(MKV_ECAPACITY, "cache holds %d decode steps (max_new_tokens)", c->sh.max_new);
   prof_mark(c, 2, 0, hst);
-  hipError_t e = launch_append_decode(c->dv, c->sh, k, v, hst);
+  hipError_t e = launch_append_decode(c->dv, c->sh, k, v, c->evict_pending ? 1 : 0, hst);
   prof_mark(c, 2, 1, hst);
   if (e != hipSuccess) return hip_fail(e, "decode append");
+  c->evict_pending = false;
   c->steps++;
   c->phase = PH_APPENDED;
   return MKV_OK;
@@ -475,12 +477,9 @@ mkv_status mkv_h2o_update_evict(mkv_cache *c, const uint16_t *q_prompt, void *st
   }
   if (c->phase == PH_PROMPT && c->any_h2o) return fail(MKV_EINVAL, "H2O prefill needs q_prompt");
   if (c->phase != PH_ATTENDED) return fail(MKV_ESTATE, "eviction must follow mkv_decode_attention");
-  if (c->any_h2o) {
-    prof_mark(c, 4, 0, hst);
-    hipError_t e = launch_h2o_evict(c->dv, c->sh, hst);
-    prof_mark(c, 4, 1, hst);
-    if (e != hipSuccess) return hip_fail(e, "H2O evict");
-  }
+  // the victim chosen by the attention pass leaves the retained set now (exports see it gone);
+  // its slot is overwritten by the next decode append, which needs no extra launch for this
+  c->evict_pending = c->any_h2o;
   c->phase = PH_READY;
   return MKV_OK;
 }
@@ -663,6 +662,8 @@ extern "C" mkv_status mkv_export(mkv_cache *c, int32_t seq, int32_t h, int32_t w
   mkv_status st = dget(stv, (uint64_t)(uintptr_t)(c->dv.state + ((size_t)seq * c->sh.Hkv + h) * ST_WORDS), ST_WORDS);
   if (st != MKV_OK) return st;
   const int count = stv[ST_COUNT];
+  // H2O: a victim whose eviction is pending is no longer part of the retained set
+  const int gone = (d.method == H2O && c->evict_pending) ? stv[ST_VICTIM] : -1;
   std::vector<uint8_t> out;
   auto put = [&](const void *p, size_t bytes) {
     const uint8_t *b = static_cast<const uint8_t *>(p);
@@ -670,23 +671,23 @@ extern "C" mkv_status mkv_export(mkv_cache *c, int32_t seq, int32_t h, int32_t w
   };
   switch (what) {
     case MKV_EXPORT_COUNTS: {
-      int32_t v[4] = {count, stv[ST_NEXT_POS], d.method == ROCKET ? stv[ST_SEL_COUNT] : count, stv[ST_KEPT]};
+      const int held = gone >= 0 ? count - 1 : count;
+      int32_t v[4] = {held, stv[ST_NEXT_POS], d.method == ROCKET ? stv[ST_SEL_COUNT] : held, stv[ST_KEPT]};
       put(v, sizeof v);
       break;
     }
     case MKV_EXPORT_POSITIONS:
     case MKV_EXPORT_SCORES: {
       if (d.method == H2O || d.method == ROCKET) {
-        // H2O: after an eviction the freed slot can lie below `count`, and then slots
-        // 0..count hold the count retained tokens around that hole (pos -1)
-        const int nread = (d.method == H2O && stv[ST_FREE_SLOT] < count) ? count + 1 : count;
+        // slots 0..count-1 hold the retained tokens
+        const int nread = count;
         std::vector<int32_t> pos;
         if ((st = dget(pos, d.pos + (uint64_t)h * stride_slots(d) * 4, nread)) != MKV_OK) return st;
         std::vector<float> sc;
         if (d.method == H2O && (st = dget(sc, d.score + (uint64_t)h * stride_slots(d) * 4, nread)) != MKV_OK) return st;
         std::vector<int> order;
         for (int i = 0; i < nread; ++i)
-          if (pos[i] >= 0) order.push_back(i);
+          if (pos[i] >= 0 && i != gone) order.push_back(i);
         std::sort(order.begin(), order.end(), [&](int a, int b) { return pos[a] < pos[b]; });
         for (int i : order) {
           if (what == MKV_EXPORT_POSITIONS) put(&pos[i], 4);

@@ -18,7 +18,8 @@ enum StateWord : int32_t {
   ST_KOUT_FILL = 3,  // KVQ: entries used in the key-outlier pool
   ST_SEL_COUNT = 4,  // ROCKET: tokens selected by the last top-k
   ST_KEPT = 5,       // tokens kept after prefill (H2O / ROCKET), prompt length otherwise
-  ST_VICTIM = 6,     // H2O: slot chosen for eviction by the last attention pass
+  ST_VICTIM = 6,     // H2O: slot chosen for eviction by the last attention pass (-1: none); the
+                     // eviction takes effect when the next decode append reuses the slot
   ST_WORDS = 8
 };
 
@@ -116,15 +117,15 @@ struct Dev {
   int n_tiles_rk;        // the last n_tiles_rk tiles belong to RocketKV sequences
 };
 
+// apply_evict: H2O pairs whose last attention pass chose a victim write the token into its slot.
 hipError_t launch_append_decode(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
-                                hipStream_t st);
+                                int apply_evict, hipStream_t st);
 hipError_t launch_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
                               const uint16_t *k, const uint16_t *v, hipStream_t st);
 hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st);
 hipError_t launch_attention_combine(const Dev &dv, const Shape &sh, float *out, hipStream_t st);
 hipError_t launch_topk(const Dev &dv, const Shape &sh, const uint16_t *q, int32_t *pos_out, int topk_max,
                        hipStream_t st);
-hipError_t launch_h2o_evict(const Dev &dv, const Shape &sh, hipStream_t st);
 hipError_t launch_h2o_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
                                   const uint16_t *q_rows, hipStream_t st);
 hipError_t launch_snap_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
