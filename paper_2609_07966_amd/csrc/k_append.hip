@@ -87,18 +87,51 @@ MKV_DEV int kvq_value_token(const SeqDesc &sd, int h, int t, uint32_t vbits, con
   const int c = threadIdx.x;
   const float x = h2f(vbits);
   const float ax = fabsf(x);
-  s_abs[c] = ax;
-  __syncthreads();
-  int gt = 0, ge = 0;
-  for (int j = 0; j < D; ++j) {
-    const float y = s_abs[j];
-    gt += (y > ax) ? 1 : 0;
-    ge += (y >= ax) ? 1 : 0;
-  }
   const int nov = sd.bp > 0 ? sd.n_ov : 0;
-  if (gt <= nov && nov < ge) *s_scale = ax;
-  __syncthreads();
-  const float s = *s_scale;
+  float s;
+  if (nov <= 1) {
+    // the largest |v| or, for n_ov = 1, the largest after one occurrence of it is set aside:
+    // wave maxima with their multiplicities, then (maximum unique) the largest value below it
+    constexpr int NWV = D / 64;
+    const int lane = c & 63, w = c >> 6;
+    const float wm = wave_max(ax);
+    const int wc = __popcll(__ballot(ax == wm));
+    if (lane == 0) {
+      s_abs[w] = wm;
+      s_tmp[w] = wc;
+    }
+    __syncthreads();
+    float m1 = s_abs[0];
+#pragma unroll
+    for (int i = 1; i < NWV; ++i) m1 = fmaxf(m1, s_abs[i]);
+    int cnt = 0;
+#pragma unroll
+    for (int i = 0; i < NWV; ++i) cnt += s_abs[i] == m1 ? s_tmp[i] : 0;
+    s = m1;
+    if (nov == 1 && cnt < 2) {  // block-uniform
+      __syncthreads();
+      const float wm2 = wave_max(ax < m1 ? ax : -1.f);
+      if (lane == 0) s_abs[w] = wm2;
+      __syncthreads();
+      s = s_abs[0];
+#pragma unroll
+      for (int i = 1; i < NWV; ++i) s = fmaxf(s, s_abs[i]);
+    }
+    __syncthreads();  // s_abs and s_tmp are free again
+  } else {
+    s_abs[c] = ax;
+    __syncthreads();
+    int gt = 0, ge = 0;
+    for (int j = 0; j < D; ++j) {
+      const float y = s_abs[j];
+      gt += (y > ax) ? 1 : 0;
+      ge += (y >= ax) ? 1 : 0;
+    }
+    if (gt <= nov && nov < ge) *s_scale = ax;
+    __syncthreads();
+    s = *s_scale;
+    __syncthreads();
+  }
   const float inv = s > 0.f ? __fdiv_rn(1.0f, s) : 0.f;
   const float xhat = __fmul_rn(x, inv);
   const int nc = 1 << sd.bits;
@@ -200,7 +233,9 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
   __shared__ uint8_t s_code[D];
   __shared__ int s_tmp[4];
   __shared__ uint32_t s_blk[D / 2];
+  __shared__ float s_cbt[kCbTableFloats];  // codebooks and midpoints, read many times below
   const int seq = blockIdx.x / Hkv, h = blockIdx.x % Hkv, c = threadIdx.x;
+  for (int i = c; i < kCbTableFloats; i += D) s_cbt[i] = cbtab[i];
   const SeqDesc &sd = seqs[seq];
   int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
   const int count = st[ST_COUNT], pos = st[ST_NEXT_POS];
@@ -266,7 +301,7 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
     }
     case KVQ: {
       bool outl;
-      const int code = kvq_key_code(sd, h, c, kb, cbtab, D, &outl);
+      const int code = kvq_key_code(sd, h, c, kb, s_cbt, D, &outl);
       uint8_t *row = reinterpret_cast<uint8_t *>(sd.kc) + h * stride_codes(sd) + (size_t)count * sd.rowbytes;
       pack_row<D>(code, sd.bits, s_code, row);
       int total;
@@ -274,17 +309,24 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
       const int fill = st[ST_KOUT_FILL];
       uint32_t *ko = reinterpret_cast<uint32_t *>(sd.kout) + h * stride_kout(sd);
       if (outl) ko[fill + r] = outlier_entry(kb, count, code, c);
-      const int vcode = kvq_value_token<D>(sd, h, count, vb, cbtab, s_abs, &s_scale, s_tmp);
-      // the value code goes into its 4-token block: start from zero for the block's first token,
-      // otherwise from the stored block
+      const int vcode = kvq_value_token<D>(sd, h, count, vb, s_cbt, s_abs, &s_scale, s_tmp);
+      // the value code goes into its 4-token block: the block's first token writes the whole
+      // block (other tokens' codes zero); later tokens OR their bits into the stored words
       const int j = count & 3, words = D * sd.bits / 8;
-      const uint32_t *blk = reinterpret_cast<const uint32_t *>(reinterpret_cast<const uint8_t *>(sd.vc) +
-                                                               h * stride_codes(sd) + (size_t)(count / 4) * 4 * sd.rowbytes);
-      for (int w = c; w < words; w += D) s_blk[w] = j == 0 ? 0u : gld(blk + w);
-      __syncthreads();
-      or_quad_code(s_blk, c, j, vcode, sd.bits);
-      __syncthreads();
-      store_quad(sd, h, count & ~3, s_blk, D);
+      if (j == 0) {
+        for (int w = c; w < words; w += D) s_blk[w] = 0u;
+        __syncthreads();
+        or_quad_code(s_blk, c, j, vcode, sd.bits);
+        __syncthreads();
+        store_quad(sd, h, count & ~3, s_blk, D);
+      } else {
+        uint32_t *blk = reinterpret_cast<uint32_t *>(reinterpret_cast<uint8_t *>(sd.vc) + h * stride_codes(sd) +
+                                                     (size_t)(count / 4) * 4 * sd.rowbytes);
+        const int bit = sd.bits * (4 * c + j);
+        atomicOr(blk + (bit >> 5), (uint32_t)vcode << (bit & 31));
+        const int spill = (bit & 31) + sd.bits - 32;
+        if (spill > 0) atomicOr(blk + (bit >> 5) + 1, (uint32_t)vcode >> (sd.bits - spill));
+      }
       __syncthreads();
       if (c == 0) {
         (reinterpret_cast<uint32_t *>(sd.krow) + h * stride_krow(sd))[count + 1] = (uint32_t)(fill + total);

@@ -1003,21 +1003,24 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
 }
 
 // Log-sum-exp merge of one (sequence, kv head)'s tiles; H2O also adds every query head's
-// probability to each retained token's accumulated score.  One workgroup of 1024 threads per
-// pair: a wave per query head reduces the tile maxima and sums, a thread per output element
-// merges its tiles, and all threads share the score pass over the retained slots.
+// probability to each retained token's accumulated score and picks the eviction victim.  One
+// workgroup of 512 threads per pair: a wave per query head reduces the tile maxima and sums, each
+// thread merges its output elements over all tiles with the loads issued together, and an H2O
+// pair's slot data (logits, score, position) is loaded before the merge so that its latency
+// overlaps it.
 constexpr int kMaxTilesPerPair = 64;
-constexpr int kCombineThreads = 1024;
+constexpr int kCombineThreads = 512;
 
 template <int D, int G>
 __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc *__restrict__ seqs,
                                                                   int32_t *__restrict__ state,
                                                                   const float *__restrict__ partials,
                                                                   float *__restrict__ out, int Hkv) {
-  static_assert(G * D <= kCombineThreads && G * 64 <= kCombineThreads, "one thread per output element");
   constexpr int NWC = kCombineThreads / 64;
-  __shared__ float sm[kMaxTilesPerPair][G];
-  __shared__ float sl[kMaxTilesPerPair][G];
+  static_assert(G <= NWC, "a wave per query head");
+  constexpr int kChunk = 32;  // tiles whose output loads a thread issues together
+  constexpr int kU = G >= 8 ? 6 : 12;  // H2O slots per thread and round (G <= 4: 6144 slots per round)
+  __shared__ float sW[kMaxTilesPerPair][G];  // tile weights 2^(m_t - M) / L
   __shared__ float sM[G], sL[G];
   __shared__ unsigned long long s_best[NWC];
   const int seq = blockIdx.x / Hkv, h = blockIdx.x % Hkv;
@@ -1025,53 +1028,61 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
   const int first = sd.tile_first + h * sd.tile_count, nt = sd.tile_count;
   const float *P = partials + (size_t)first * G * (D + 2);
   const int wv = threadIdx.x >> 6, ln = threadIdx.x & 63;
-  if (threadIdx.x < nt * G) {
-    const int t = threadIdx.x / G, g = threadIdx.x % G;
-    sm[t][g] = P[((size_t)t * G + g) * (D + 2)];
-    sl[t][g] = P[((size_t)t * G + g) * (D + 2) + 1];
+  const bool h2o = sd.method == H2O;
+  int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
+  const float *lg = reinterpret_cast<const float *>(sd.logits) + h * stride_logits(sd, G);
+  float *score = reinterpret_cast<float *>(sd.score) + h * stride_slots(sd);
+  const int32_t *pos = reinterpret_cast<const int32_t *>(sd.pos) + h * stride_slots(sd);
+  // H2O: the first round's slot data, loaded ahead of the merge
+  int count = 0, limit = 0;
+  float lgv[kU][G], scv[kU];
+  int pv[kU];
+  if (h2o) {
+    count = st[ST_COUNT];
+    limit = st[ST_NEXT_POS] - 1 - sd.R + 1;
+    if (count > 0) {
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const int j = min((int)threadIdx.x + u * kCombineThreads, count - 1);
+#pragma unroll
+        for (int g = 0; g < G; ++g) lgv[u][g] = gld(lg + (size_t)j * G + g);
+        scv[u] = gld(score + j);
+        pv[u] = gld(pos + j);
+      }
+    }
   }
-  __syncthreads();
-  if (wv < G) {  // wave g: lane t takes tile t
-    const float m = ln < nt ? sm[ln][wv] : -INFINITY;
+  if (wv < G) {  // wave g: lane t takes tile t (nt <= 64)
+    const float m = ln < nt ? P[((size_t)ln * G + wv) * (D + 2)] : -INFINITY;
+    const float l = ln < nt ? P[((size_t)ln * G + wv) * (D + 2) + 1] : 0.f;
     const float M = wave_max(m);
-    const float L = wave_sum(ln < nt && m != -INFINITY ? sl[ln][wv] * exp2f(m - M) : 0.f);
+    const float L = wave_sum(m != -INFINITY ? l * exp2f(m - M) : 0.f);
+    if (ln < nt) sW[ln][wv] = m == -INFINITY ? 0.f : exp2f(m - M) / L;
     if (ln == 0) {
       sM[wv] = M;
       sL[wv] = L;
     }
   }
   __syncthreads();
-  if (threadIdx.x < nt * G) {
-    const int t = threadIdx.x / G, g = threadIdx.x % G;
-    sm[t][g] = sm[t][g] == -INFINITY ? 0.f : exp2f(sm[t][g] - sM[g]) / sL[g];
-  }
-  __syncthreads();
   const int Hq = Hkv * G;
-  if (threadIdx.x < G * D) {
-    const int g = threadIdx.x / D, c = threadIdx.x % D;
-    const float *pp = P + (size_t)g * (D + 2) + 2 + c;
-    // 8 independent partial sums keep 8 tile loads in flight
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    int t = 0;
-    for (; t + 8 <= nt; t += 8) {
+  for (int e = threadIdx.x; e < G * D; e += kCombineThreads) {
+    const int g = e / D, c = e % D;
+    const float *po = P + (size_t)g * (D + 2) + 2 + c;
+    float acc = 0.f;
+    for (int t0 = 0; t0 < nt; t0 += kChunk) {
+      float o[kChunk];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) acc[u] = fmaf(pp[(size_t)(t + u) * G * (D + 2)], sm[t + u][g], acc[u]);
+      for (int u = 0; u < kChunk; ++u) o[u] = po[(size_t)min(t0 + u, nt - 1) * G * (D + 2)];
+#pragma unroll
+      for (int u = 0; u < kChunk; ++u)
+        if (t0 + u < nt) acc = fmaf(o[u], sW[t0 + u][g], acc);
     }
-    for (; t < nt; ++t) acc[0] = fmaf(pp[(size_t)t * G * (D + 2)], sm[t][g], acc[0]);
-    out[((size_t)seq * Hq + h * G + g) * D + c] =
-        ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
+    out[((size_t)seq * Hq + h * G + g) * D + c] = acc;
   }
-  if (sd.method == H2O) {
+  if (h2o) {
     // accumulate, and find the eviction candidate (lowest score among positions older than the
     // R most recent, lower position on a tie); the next decode append writes its token there
-    int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
-    const int count = st[ST_COUNT];
-    const int limit = st[ST_NEXT_POS] - 1 - sd.R + 1;
-    // no victim unless one is found below (the barrier of the search orders this write first)
+    // (no victim unless one is found below: the barrier of the search orders this write first)
     if (threadIdx.x == 0) st[ST_VICTIM] = -1;
-    const float *lg = reinterpret_cast<const float *>(sd.logits) + h * stride_logits(sd, G);
-    float *score = reinterpret_cast<float *>(sd.score) + h * stride_slots(sd);
-    const int32_t *pos = reinterpret_cast<const int32_t *>(sd.pos) + h * stride_slots(sd);
     float invL[G], M[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -1080,18 +1091,31 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
     }
     unsigned long long best = ~0ull;
     int best_slot = -1;
-    for (int j = threadIdx.x; j < count; j += kCombineThreads) {
-      float acc = 0.f;
+    for (int j0 = threadIdx.x; j0 < count; j0 += kU * kCombineThreads) {
+      if (j0 != (int)threadIdx.x) {  // rounds after the first (more than 6144 slots)
 #pragma unroll
-      for (int g = 0; g < G; ++g) acc += exp2f(gld(lg + (size_t)j * G + g) - M[g]) * invL[g];
-      const float sc = gld(score + j) + acc;
-      gst(score + j, sc);
-      const int pj = gld(pos + j);
-      const unsigned long long key =
-          ((unsigned long long)__builtin_bit_cast(uint32_t, sc) << 32) | (unsigned long long)(uint32_t)pj;
-      if (pj < limit && key < best) {
-        best = key;
-        best_slot = j;
+        for (int u = 0; u < kU; ++u) {
+          const int j = min(j0 + u * kCombineThreads, count - 1);
+#pragma unroll
+          for (int g = 0; g < G; ++g) lgv[u][g] = gld(lg + (size_t)j * G + g);
+          scv[u] = gld(score + j);
+          pv[u] = gld(pos + j);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const int j = j0 + u * kCombineThreads;
+        float acc = 0.f;
+#pragma unroll
+        for (int g = 0; g < G; ++g) acc += exp2f(lgv[u][g] - M[g]) * invL[g];
+        const float sc = scv[u] + acc;
+        if (j < count) gst(score + j, sc);
+        const unsigned long long key =
+            ((unsigned long long)__builtin_bit_cast(uint32_t, sc) << 32) | (unsigned long long)(uint32_t)pv[u];
+        if (j < count && pv[u] < limit && key < best) {
+          best = key;
+          best_slot = j;
+        }
       }
     }
     if (count > sd.B) {
