@@ -343,7 +343,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cfg-steps", type=int, default=48)
-    ap.add_argument("--cpu-steps", type=int, default=2)
+    ap.add_argument("--cpu-steps", type=int, default=8)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-per-config", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MiB",
