@@ -98,6 +98,39 @@ MKV_DEV void topk_radix(int n, int k, Get get, int (*hist)[NTH / 64][256], int *
 }
 
 
+// Approximate scores of the T consecutive tokens [j0, j0 + T) (T = 4 or 8) from the channel-major
+// key copy: one 2T-byte load per selected channel, R channels' loads issued before any is used,
+// channels ascending, every product and sum rounded to fp32 separately (no fused multiply-add).
+// Rows are padded to 8 tokens and j0 is a multiple of T, so no load leaves its row.
+template <int T, int R>
+MKV_DEV void score_tokens(const uint16_t *kcm, int cstride, int j0, int nch, const int *sel_ch, const float *sel_qb,
+                          float (&acc)[T]) {
+#pragma unroll
+  for (int t = 0; t < T; ++t) acc[t] = 0.f;
+  for (int i0 = 0; i0 < nch; i0 += R) {
+    uint32_t w[R][T / 2];
+#pragma unroll
+    for (int ii = 0; ii < R; ++ii) {
+      const int i = min(i0 + ii, nch - 1);
+      const uint32_t *p = reinterpret_cast<const uint32_t *>(kcm + (size_t)sel_ch[i] * cstride + j0);
+#pragma unroll
+      for (int u = 0; u < T / 2; ++u) w[ii][u] = gld(p + u);
+    }
+#pragma unroll
+    for (int ii = 0; ii < R; ++ii) {
+      if (i0 + ii < nch) {
+        const float qb = sel_qb[i0 + ii];
+#pragma unroll
+        for (int u = 0; u < T / 2; ++u) {
+          acc[2 * u] = __fadd_rn(acc[2 * u], __fmul_rn(qb, h2f(w[ii][u])));
+          acc[2 * u + 1] = __fadd_rn(acc[2 * u + 1], __fmul_rn(qb, h2f(w[ii][u] >> 16)));
+        }
+      }
+    }
+  }
+}
+
+
 // One workgroup of 1024 threads per (sequence, kv head): a kept set of up to a few thousand
 // tokens is scored with ~4 tokens per thread and selected by radix passes over LDS keys.
 constexpr int kTopkThreads = 1024;
@@ -193,45 +226,34 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(const SeqDesc *__restrict
     return;
   }
 
-  // approximate scores from the channel-major key copy: one lane per token (4 independent tokens
-  // per lane in flight), channels ascending, acc = fl32(acc + fl32(qbar_c * k_jc)); the keys stay
-  // in LDS when they fit
+  // approximate scores from the channel-major key copy, channels ascending,
+  // acc = fl32(acc + fl32(qbar_c * k_jc)); the keys stay in LDS when they fit.  A lane scores 4
+  // consecutive tokens (8 for sets of more than 4 kTopkThreads tokens, so that one pass covers up
+  // to 8 kTopkThreads)
   const uint16_t *kcm = reinterpret_cast<const uint16_t *>(sd.kcm) + h * stride_kcm(sd, D);
   uint32_t *akeys = reinterpret_cast<uint32_t *>(sd.akeys) + h * stride_slots(sd);
   const bool in_lds = n <= kTopkLdsKeys;
   const int cstride = sd.cstride;
-  // each lane scores 4 consecutive tokens from one 8-byte load per channel; the loads of 16
-  // channels are issued before any is used (rows are padded to 8 tokens, so the load never
-  // leaves the row)
-  for (int j0 = 4 * (int)threadIdx.x; j0 < n; j0 += 4 * kTopkThreads) {
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int i0 = 0; i0 < nch; i0 += 16) {
-      uint32_t lo[16], hi[16];
-#pragma unroll
-      for (int ii = 0; ii < 16; ++ii) {
-        const int i = min(i0 + ii, nch - 1);
-        const uint32_t *p = reinterpret_cast<const uint32_t *>(kcm + (size_t)s_sel_ch[i] * cstride + j0);
-        lo[ii] = gld(p);
-        hi[ii] = gld(p + 1);
-      }
-#pragma unroll
-      for (int ii = 0; ii < 16; ++ii) {
-        if (i0 + ii < nch) {
-          const float qb = s_sel_qb[i0 + ii];
-          acc[0] = __fadd_rn(acc[0], __fmul_rn(qb, h2f(lo[ii])));
-          acc[1] = __fadd_rn(acc[1], __fmul_rn(qb, h2f(lo[ii] >> 16)));
-          acc[2] = __fadd_rn(acc[2], __fmul_rn(qb, h2f(hi[ii])));
-          acc[3] = __fadd_rn(acc[3], __fmul_rn(qb, h2f(hi[ii] >> 16)));
-        }
-      }
+  auto put = [&](int j, float a) {
+    if (j < n) {
+      if (in_lds) s_keys[j] = float_key(a);
+      else gst(akeys + j, float_key(a));
     }
+  };
+  if (n <= 4 * kTopkThreads) {
+    const int j0 = 4 * (int)threadIdx.x;
+    if (j0 < n) {
+      float acc[4];
+      score_tokens<4, 32>(kcm, cstride, j0, nch, s_sel_ch, s_sel_qb, acc);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int j = j0 + r;
-      if (j < n) {
-        if (in_lds) s_keys[j] = float_key(acc[r]);
-        else gst(akeys + j, float_key(acc[r]));
-      }
+      for (int r = 0; r < 4; ++r) put(j0 + r, acc[r]);
+    }
+  } else {
+    for (int j0 = 8 * (int)threadIdx.x; j0 < n; j0 += 8 * kTopkThreads) {
+      float acc[8];
+      score_tokens<8, 16>(kcm, cstride, j0, nch, s_sel_ch, s_sel_qb, acc);
+#pragma unroll
+      for (int r = 0; r < 8; ++r) put(j0 + r, acc[r]);
     }
   }
   for (int e = threadIdx.x; e < (kTopkThreads / 64) * 256; e += kTopkThreads) (&whist[0][0][0])[e] = 0;
