@@ -189,6 +189,15 @@ mkv_status mkv_decode_attention(mkv_cache *cache, const uint16_t *q, float *out,
 /*
  * The four decode calls in their order: append (k, v: device fp16
  * [S][Hkv][d]), top-k select, attention, eviction.
+ *
+ * Graph capture: the step enqueues four kernels on `stream` and nothing else
+ * (no allocation, copy, memset or synchronization; profiling events only
+ * when enabled), and every per-step quantity (counts, positions, H2O victims,
+ * outlier fills) lives in device state, so a captured step may be replayed
+ * any number of times with new k, v, q written into the captured buffers.
+ * The host-side step count then no longer follows the device: capacity is
+ * also checked on the device, where an append into a full region drops the
+ * token and leaves that (sequence, kv head) unchanged.
  */
 mkv_status mkv_decode_step(mkv_cache *cache, const uint16_t *k, const uint16_t *v,
                            const uint16_t *q, float *out, void *stream);

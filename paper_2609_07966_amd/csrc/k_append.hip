@@ -227,7 +227,7 @@ template <int D>
 __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict__ seqs, int32_t *state,
                                                       const uint16_t *__restrict__ k,
                                                       const uint16_t *__restrict__ v,
-                                                      const float *__restrict__ cbtab, int Hkv, int apply_evict) {
+                                                      const float *__restrict__ cbtab, int Hkv) {
   __shared__ float s_abs[D];
   __shared__ float s_scale;
   __shared__ uint8_t s_code[D];
@@ -239,6 +239,12 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
   const SeqDesc &sd = seqs[seq];
   int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
   const int count = st[ST_COUNT], pos = st[ST_NEXT_POS];
+  // H2O: an eviction decided by the last attention pass frees its slot for this token (-1: none)
+  const int victim = sd.method == H2O ? st[ST_VICTIM] : -1;
+  const int slot = sd.method == H2O ? (victim >= 0 ? victim : st[ST_FREE_SLOT]) : count;
+  // a full region (reachable only by replaying a captured decode step past max_new_tokens) drops
+  // the token instead of writing past the region; the decision is the same for every thread
+  if (slot >= sd.cap || (sd.method == KVQ && st[ST_KOUT_FILL] + D > sd.pool_cap)) return;
   const uint32_t kb = k[((size_t)seq * Hkv + h) * D + c];
   const uint32_t vb = v[((size_t)seq * Hkv + h) * D + c];
   __syncthreads();  // every thread has read the state before thread 0 updates it
@@ -250,10 +256,7 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
       break;
     }
     case H2O: {
-      // an eviction decided by the last attention pass (and confirmed by the eviction call)
-      // frees its slot for this token; otherwise the token goes to the end
-      const int victim = apply_evict ? st[ST_VICTIM] : -1;
-      const int slot = victim >= 0 ? victim : st[ST_FREE_SLOT];
+      // into the victim's slot, else at the end
       const int new_count = victim >= 0 ? count : count + 1;
       (reinterpret_cast<uint16_t *>(sd.k) + h * stride_rows(sd, D))[(size_t)slot * D + c] = (uint16_t)kb;
       (reinterpret_cast<uint16_t *>(sd.v) + h * stride_rows(sd, D))[(size_t)slot * D + c] = (uint16_t)vb;
@@ -508,6 +511,7 @@ __global__ void k_prefill_state(const SeqDesc *__restrict__ seqs, int seq, int32
   st[ST_NEXT_POS] = sd.n0;
   st[ST_FREE_SLOT] = 0;
   st[ST_KEPT] = sd.n0;
+  st[ST_VICTIM] = -1;
 }
 
 __global__ void k_init_state(int32_t *state, int n) {
@@ -517,9 +521,9 @@ __global__ void k_init_state(int32_t *state, int n) {
 
 template <int D>
 hipError_t append_decode_impl(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
-                              int apply_evict, hipStream_t st) {
+                              hipStream_t st) {
   hipLaunchKernelGGL(k_append_decode<D>, dim3(sh.S * sh.Hkv), dim3(D), 0, st, dv.seqs, dv.state, k, v,
-                     dv.cbtab, sh.Hkv, apply_evict);
+                     dv.cbtab, sh.Hkv);
   return hipGetLastError();
 }
 
@@ -562,9 +566,8 @@ hipError_t prefill_impl(const Dev &dv, const Shape &sh, const SeqDesc &hs, int s
 }  // namespace
 
 hipError_t launch_append_decode(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
-                                int apply_evict, hipStream_t st) {
-  return sh.D == 64 ? append_decode_impl<64>(dv, sh, k, v, apply_evict, st)
-                    : append_decode_impl<128>(dv, sh, k, v, apply_evict, st);
+                                hipStream_t st) {
+  return sh.D == 64 ? append_decode_impl<64>(dv, sh, k, v, st) : append_decode_impl<128>(dv, sh, k, v, st);
 }
 
 hipError_t launch_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq, const uint16_t *k,

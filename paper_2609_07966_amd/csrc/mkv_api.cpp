@@ -450,7 +450,7 @@ mkv_status mkv_append_quantize(mkv_cache *c, const uint16_t *k, const uint16_t *
   if (c->steps >= c->sh.max_new)
     return fail(MKV_ECAPACITY, "cache holds %d decode steps (max_new_tokens)", c->sh.max_new);
   prof_mark(c, 2, 0, hst);
-  hipError_t e = launch_append_decode(c->dv, c->sh, k, v, c->evict_pending ? 1 : 0, hst);
+  hipError_t e = launch_append_decode(c->dv, c->sh, k, v, hst);
   prof_mark(c, 2, 1, hst);
   if (e != hipSuccess) return hip_fail(e, "decode append");
   c->evict_pending = false;

@@ -117,9 +117,9 @@ struct Dev {
   int n_tiles_rk;        // the last n_tiles_rk tiles belong to RocketKV sequences
 };
 
-// apply_evict: H2O pairs whose last attention pass chose a victim write the token into its slot.
+// H2O pairs whose last attention pass chose a victim (ST_VICTIM >= 0) write the token into its slot.
 hipError_t launch_append_decode(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
-                                int apply_evict, hipStream_t st);
+                                hipStream_t st);
 hipError_t launch_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
                               const uint16_t *k, const uint16_t *v, hipStream_t st);
 hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st);
