@@ -1004,10 +1004,9 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
 
 // Log-sum-exp merge of one (sequence, kv head)'s tiles; H2O also adds every query head's
 // probability to each retained token's accumulated score and picks the eviction victim.  One
-// workgroup of 512 threads per pair: a wave per query head reduces the tile maxima and sums, each
-// thread merges its output elements over all tiles with the loads issued together, and an H2O
-// pair's slot data (logits, score, position) is loaded before the merge so that its latency
-// overlaps it.
+// workgroup of 512 threads per pair: a wave per query head reduces the tile maxima and sums while
+// every thread's output values of all tiles and an H2O pair's slot data (logits, score, position)
+// are already in flight, so the merge waits for one round of loads.
 constexpr int kMaxTilesPerPair = 64;
 constexpr int kCombineThreads = 512;
 
@@ -1033,23 +1032,32 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
   const float *lg = reinterpret_cast<const float *>(sd.logits) + h * stride_logits(sd, G);
   float *score = reinterpret_cast<float *>(sd.score) + h * stride_slots(sd);
   const int32_t *pos = reinterpret_cast<const int32_t *>(sd.pos) + h * stride_slots(sd);
-  // H2O: the first round's slot data, loaded ahead of the merge
+  // H2O: the first round's slot data, loaded ahead of the merge (every slot below the capacity
+  // is allocated, so the loads need not wait for the count)
   int count = 0, limit = 0;
   float lgv[kU][G], scv[kU];
   int pv[kU];
   if (h2o) {
     count = st[ST_COUNT];
     limit = st[ST_NEXT_POS] - 1 - sd.R + 1;
-    if (count > 0) {
 #pragma unroll
-      for (int u = 0; u < kU; ++u) {
-        const int j = min((int)threadIdx.x + u * kCombineThreads, count - 1);
+    for (int u = 0; u < kU; ++u) {
+      const int j = min((int)threadIdx.x + u * kCombineThreads, sd.cap - 1);
 #pragma unroll
-        for (int g = 0; g < G; ++g) lgv[u][g] = gld(lg + (size_t)j * G + g);
-        scv[u] = gld(score + j);
-        pv[u] = gld(pos + j);
-      }
+      for (int g = 0; g < G; ++g) lgv[u][g] = gld(lg + (size_t)j * G + g);
+      scv[u] = gld(score + j);
+      pv[u] = gld(pos + j);
     }
+  }
+  // the output values of the first kChunk tiles, loaded before the tile weights are known
+  constexpr int kE = (G * D + kCombineThreads - 1) / kCombineThreads;  // output elements per thread
+  float o0[kE][kChunk];
+#pragma unroll
+  for (int i = 0; i < kE; ++i) {
+    const int e = min((int)threadIdx.x + i * kCombineThreads, G * D - 1);
+    const float *po = P + (size_t)(e / D) * (D + 2) + 2 + e % D;
+#pragma unroll
+    for (int u = 0; u < kChunk; ++u) o0[i][u] = po[(size_t)min(u, nt - 1) * G * (D + 2)];
   }
   if (wv < G) {  // wave g: lane t takes tile t (nt <= 64)
     const float m = ln < nt ? P[((size_t)ln * G + wv) * (D + 2)] : -INFINITY;
@@ -1064,19 +1072,26 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
   }
   __syncthreads();
   const int Hq = Hkv * G;
-  for (int e = threadIdx.x; e < G * D; e += kCombineThreads) {
-    const int g = e / D, c = e % D;
-    const float *po = P + (size_t)g * (D + 2) + 2 + c;
-    float acc = 0.f;
-    for (int t0 = 0; t0 < nt; t0 += kChunk) {
-      float o[kChunk];
 #pragma unroll
-      for (int u = 0; u < kChunk; ++u) o[u] = po[(size_t)min(t0 + u, nt - 1) * G * (D + 2)];
+  for (int i = 0; i < kE; ++i) {
+    const int e = (int)threadIdx.x + i * kCombineThreads;
+    if (e < G * D) {
+      const int g = e / D, c = e % D;
+      float acc = 0.f;
 #pragma unroll
       for (int u = 0; u < kChunk; ++u)
-        if (t0 + u < nt) acc = fmaf(o[u], sW[t0 + u][g], acc);
+        if (u < nt) acc = fmaf(o0[i][u], sW[u][g], acc);
+      const float *po = P + (size_t)g * (D + 2) + 2 + c;
+      for (int t0 = kChunk; t0 < nt; t0 += kChunk) {  // more than kChunk tiles
+        float o[kChunk];
+#pragma unroll
+        for (int u = 0; u < kChunk; ++u) o[u] = po[(size_t)min(t0 + u, nt - 1) * G * (D + 2)];
+#pragma unroll
+        for (int u = 0; u < kChunk; ++u)
+          if (t0 + u < nt) acc = fmaf(o[u], sW[t0 + u][g], acc);
+      }
+      out[((size_t)seq * Hq + h * G + g) * D + c] = acc;
     }
-    out[((size_t)seq * Hq + h * G + g) * D + c] = acc;
   }
   if (h2o) {
     // accumulate, and find the eviction candidate (lowest score among positions older than the
