@@ -422,6 +422,26 @@ mkv_status mkv_cache_destroy(mkv_cache *c) {
   return MKV_OK;
 }
 
+namespace {
+
+// The decode append of one row per sequence (the row counts are already known to be 1).
+mkv_status decode_append(mkv_cache *c, const uint16_t *k, const uint16_t *v, hipStream_t hst) {
+  if (!(c->phase == PH_READY || (c->phase == PH_ATTENDED && !c->any_h2o)))
+    return fail(MKV_ESTATE, "decode append must follow prefill or a completed decode step");
+  if (c->steps >= c->sh.max_new)
+    return fail(MKV_ECAPACITY, "cache holds %d decode steps (max_new_tokens)", c->sh.max_new);
+  prof_mark(c, 2, 0, hst);
+  hipError_t e = launch_append_decode(c->dv, c->sh, k, v, hst);
+  prof_mark(c, 2, 1, hst);
+  if (e != hipSuccess) return hip_fail(e, "decode append");
+  c->evict_pending = false;
+  c->steps++;
+  c->phase = PH_APPENDED;
+  return MKV_OK;
+}
+
+}  // namespace
+
 mkv_status mkv_append_quantize(mkv_cache *c, const uint16_t *k, const uint16_t *v, const int32_t *cu_new,
                                void *stream) {
   if (!c) return fail(MKV_EINVAL, "cache is NULL");
@@ -445,18 +465,7 @@ mkv_status mkv_append_quantize(mkv_cache *c, const uint16_t *k, const uint16_t *
   }
   for (int s = 0; s < S; ++s)
     if (cu_new[s + 1] - cu_new[s] != 1) return fail(MKV_EINVAL, "decode: seq %d must append exactly 1 row", s);
-  if (!(c->phase == PH_READY || (c->phase == PH_ATTENDED && !c->any_h2o)))
-    return fail(MKV_ESTATE, "decode append must follow prefill or a completed decode step");
-  if (c->steps >= c->sh.max_new)
-    return fail(MKV_ECAPACITY, "cache holds %d decode steps (max_new_tokens)", c->sh.max_new);
-  prof_mark(c, 2, 0, hst);
-  hipError_t e = launch_append_decode(c->dv, c->sh, k, v, hst);
-  prof_mark(c, 2, 1, hst);
-  if (e != hipSuccess) return hip_fail(e, "decode append");
-  c->evict_pending = false;
-  c->steps++;
-  c->phase = PH_APPENDED;
-  return MKV_OK;
+  return decode_append(c, k, v, hst);
 }
 
 mkv_status mkv_h2o_update_evict(mkv_cache *c, const uint16_t *q_prompt, void *stream) {
@@ -539,9 +548,9 @@ mkv_status mkv_decode_attention(mkv_cache *c, const uint16_t *q, float *out, voi
 mkv_status mkv_decode_step(mkv_cache *c, const uint16_t *k, const uint16_t *v, const uint16_t *q, float *out,
                            void *stream) {
   if (!c) return fail(MKV_EINVAL, "cache is NULL");
-  std::vector<int32_t> cu(c->sh.S + 1);
-  for (int s = 0; s <= c->sh.S; ++s) cu[s] = s;
-  mkv_status st = mkv_append_quantize(c, k, v, cu.data(), stream);
+  if (!k || !v) return fail(MKV_EINVAL, "k and v must be non-NULL");
+  if (c->phase == PH_CREATED) return fail(MKV_ESTATE, "decode step before the prefill append");
+  mkv_status st = decode_append(c, k, v, static_cast<hipStream_t>(stream));
   if (st != MKV_OK) return st;
   if ((st = mkv_topk_select(c, q, nullptr, stream)) != MKV_OK) return st;
   if ((st = mkv_decode_attention(c, q, out, stream)) != MKV_OK) return st;
