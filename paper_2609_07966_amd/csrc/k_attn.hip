@@ -760,7 +760,7 @@ MKV_DEV void merge_waves(const float *red, int wstride, float *dst) {
 #pragma unroll
       for (int w = 0; w < NW; ++w) {
         if (at(w, g, 0) == -INFINITY) continue;
-        val += at(w, g, c) * exp2f(at(w, g, 0) - M);
+        val += at(w, g, c) * fexp2(at(w, g, 0) - M);  // argument <= 0
       }
     }
     dst[e] = val;
@@ -1032,8 +1032,23 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
   const float *lg = reinterpret_cast<const float *>(sd.logits) + h * stride_logits(sd, G);
   float *score = reinterpret_cast<float *>(sd.score) + h * stride_slots(sd);
   const int32_t *pos = reinterpret_cast<const int32_t *>(sd.pos) + h * stride_slots(sd);
-  // H2O: the first round's slot data, loaded ahead of the merge (every slot below the capacity
-  // is allocated, so the loads need not wait for the count)
+  // loads in the order they are needed: tile maxima and sums (wave g, lane t: tile t, nt <= 64),
+  // the output values of the first kChunk tiles, then an H2O pair's first round of slot data
+  // (every slot below the capacity is allocated, so these need not wait for the count)
+  float tm = -INFINITY, tl = 0.f;
+  if (wv < G && ln < nt) {
+    tm = P[((size_t)ln * G + wv) * (D + 2)];
+    tl = P[((size_t)ln * G + wv) * (D + 2) + 1];
+  }
+  constexpr int kE = (G * D + kCombineThreads - 1) / kCombineThreads;  // output elements per thread
+  float o0[kE][kChunk];
+#pragma unroll
+  for (int i = 0; i < kE; ++i) {
+    const int e = min((int)threadIdx.x + i * kCombineThreads, G * D - 1);
+    const float *po = P + (size_t)(e / D) * (D + 2) + 2 + e % D;
+#pragma unroll
+    for (int u = 0; u < kChunk; ++u) o0[i][u] = po[(size_t)min(u, nt - 1) * G * (D + 2)];
+  }
   int count = 0, limit = 0;
   float lgv[kU][G], scv[kU];
   int pv[kU];
@@ -1049,22 +1064,10 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
       pv[u] = gld(pos + j);
     }
   }
-  // the output values of the first kChunk tiles, loaded before the tile weights are known
-  constexpr int kE = (G * D + kCombineThreads - 1) / kCombineThreads;  // output elements per thread
-  float o0[kE][kChunk];
-#pragma unroll
-  for (int i = 0; i < kE; ++i) {
-    const int e = min((int)threadIdx.x + i * kCombineThreads, G * D - 1);
-    const float *po = P + (size_t)(e / D) * (D + 2) + 2 + e % D;
-#pragma unroll
-    for (int u = 0; u < kChunk; ++u) o0[i][u] = po[(size_t)min(u, nt - 1) * G * (D + 2)];
-  }
-  if (wv < G) {  // wave g: lane t takes tile t (nt <= 64)
-    const float m = ln < nt ? P[((size_t)ln * G + wv) * (D + 2)] : -INFINITY;
-    const float l = ln < nt ? P[((size_t)ln * G + wv) * (D + 2) + 1] : 0.f;
-    const float M = wave_max(m);
-    const float L = wave_sum(m != -INFINITY ? l * exp2f(m - M) : 0.f);
-    if (ln < nt) sW[ln][wv] = m == -INFINITY ? 0.f : exp2f(m - M) / L;
+  if (wv < G) {
+    const float M = wave_max(tm);
+    const float L = wave_sum_rows(tm != -INFINITY ? tl * fexp2(tm - M) : 0.f);  // arguments <= 0
+    if (ln < nt) sW[ln][wv] = tm == -INFINITY ? 0.f : fexp2(tm - M) / L;
     if (ln == 0) {
       sM[wv] = M;
       sL[wv] = L;
@@ -1122,7 +1125,7 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
         const int j = j0 + u * kCombineThreads;
         float acc = 0.f;
 #pragma unroll
-        for (int g = 0; g < G; ++g) acc += exp2f(lgv[u][g] - M[g]) * invL[g];
+        for (int g = 0; g < G; ++g) acc += fexp2(lgv[u][g] - M[g]) * invL[g];  // arguments <= 0
         const float sc = scv[u] + acc;
         if (j < count) gst(score + j, sc);
         const unsigned long long key =
@@ -1134,12 +1137,7 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
       }
     }
     if (count > sd.B) {
-      unsigned long long wb = best;
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) {
-        const unsigned long long x = __shfl_xor(wb, m);
-        wb = x < wb ? x : wb;
-      }
+      const unsigned long long wb = wave_min_u64(best);
       if (ln == 0) s_best[wv] = wb;
       __syncthreads();
       unsigned long long all = s_best[0];

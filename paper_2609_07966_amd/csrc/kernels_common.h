@@ -82,15 +82,48 @@ MKV_DEV float group_sum(float x) {
   return x;
 }
 
+// Maximum / minimum over the wave, in every lane (all lanes active): four DPP steps within each
+// row of 16 lanes, then two lane shuffles across the rows.
 MKV_DEV float wave_max(float x) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m));
-  return x;
+  x = fmaxf(x, dpp<0xB1>(x));   // quad_perm [1,0,3,2]
+  x = fmaxf(x, dpp<0x4E>(x));   // quad_perm [2,3,0,1]
+  x = fmaxf(x, dpp<0x141>(x));  // row_half_mirror
+  x = fmaxf(x, dpp<0x140>(x));  // row_mirror
+  x = fmaxf(x, __shfl_xor(x, 16));
+  return fmaxf(x, __shfl_xor(x, 32));
 }
 MKV_DEV float wave_min(float x) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) x = fminf(x, __shfl_xor(x, m));
-  return x;
+  x = fminf(x, dpp<0xB1>(x));
+  x = fminf(x, dpp<0x4E>(x));
+  x = fminf(x, dpp<0x141>(x));
+  x = fminf(x, dpp<0x140>(x));
+  x = fminf(x, __shfl_xor(x, 16));
+  return fminf(x, __shfl_xor(x, 32));
+}
+// Sum over the wave in every lane, rows first (DPP) then across rows; a different association
+// than wave_sum, so it is used only where that order is free.
+MKV_DEV float wave_sum_rows(float x) {
+  x = group_sum<16>(x);
+  x += __shfl_xor(x, 16);
+  return x + __shfl_xor(x, 32);
+}
+// Minimum of a 64-bit key over the wave, in every lane.
+MKV_DEV unsigned long long wave_min_u64(unsigned long long x) {
+  auto step = [&](auto ctrl) {
+    constexpr int C = decltype(ctrl)::value;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)x, C, 0xF, 0xF, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(x >> 32), C, 0xF, 0xF, false);
+    const unsigned long long y = ((unsigned long long)hi << 32) | lo;
+    x = y < x ? y : x;
+  };
+  step(std::integral_constant<int, 0xB1>{});
+  step(std::integral_constant<int, 0x4E>{});
+  step(std::integral_constant<int, 0x141>{});
+  step(std::integral_constant<int, 0x140>{});
+  unsigned long long y = __shfl_xor(x, 16);
+  x = y < x ? y : x;
+  y = __shfl_xor(x, 32);
+  return y < x ? y : x;
 }
 MKV_DEV float wave_sum(float x) {
 #pragma unroll
