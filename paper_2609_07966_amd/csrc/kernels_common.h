@@ -82,30 +82,30 @@ MKV_DEV float group_sum(float x) {
   return x;
 }
 
-// Maximum / minimum over the wave, in every lane (all lanes active): four DPP steps within each
-// row of 16 lanes, then two lane shuffles across the rows.
+// Reductions over the wave (all lanes active), without LDS traffic: four DPP steps give every lane
+// its row's result, row_bcast:15 and row_bcast:31 carry rows 0 and 2 into rows 1 and 3 and rows
+// 0-1 into rows 2-3, and lane 63's total is read back as a wave-uniform value.
+template <typename Op>
+MKV_DEV float wave_reduce(float x, float identity, Op op) {
+  x = op(x, dpp<0xB1>(x));   // quad_perm [1,0,3,2]
+  x = op(x, dpp<0x4E>(x));   // quad_perm [2,3,0,1]
+  x = op(x, dpp<0x141>(x));  // row_half_mirror
+  x = op(x, dpp<0x140>(x));  // row_mirror
+  const int id = __builtin_bit_cast(int, identity);
+  x = op(x, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(id, __builtin_bit_cast(int, x), 0x142, 0xA, 0xF, false)));
+  x = op(x, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(id, __builtin_bit_cast(int, x), 0x143, 0xC, 0xF, false)));
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 63));
+}
 MKV_DEV float wave_max(float x) {
-  x = fmaxf(x, dpp<0xB1>(x));   // quad_perm [1,0,3,2]
-  x = fmaxf(x, dpp<0x4E>(x));   // quad_perm [2,3,0,1]
-  x = fmaxf(x, dpp<0x141>(x));  // row_half_mirror
-  x = fmaxf(x, dpp<0x140>(x));  // row_mirror
-  x = fmaxf(x, __shfl_xor(x, 16));
-  return fmaxf(x, __shfl_xor(x, 32));
+  return wave_reduce(x, -INFINITY, [](float a, float b) { return fmaxf(a, b); });
 }
 MKV_DEV float wave_min(float x) {
-  x = fminf(x, dpp<0xB1>(x));
-  x = fminf(x, dpp<0x4E>(x));
-  x = fminf(x, dpp<0x141>(x));
-  x = fminf(x, dpp<0x140>(x));
-  x = fminf(x, __shfl_xor(x, 16));
-  return fminf(x, __shfl_xor(x, 32));
+  return wave_reduce(x, INFINITY, [](float a, float b) { return fminf(a, b); });
 }
-// Sum over the wave in every lane, rows first (DPP) then across rows; a different association
-// than wave_sum, so it is used only where that order is free.
+// Sum over the wave: rows first, then rows 0 + 1 and 2 + 3, then the two halves (an association
+// other than wave_sum's, so it is used only where that order is free).
 MKV_DEV float wave_sum_rows(float x) {
-  x = group_sum<16>(x);
-  x += __shfl_xor(x, 16);
-  return x + __shfl_xor(x, 32);
+  return wave_reduce(x, 0.f, [](float a, float b) { return a + b; });
 }
 // Minimum of a 64-bit key over the wave, in every lane.
 MKV_DEV unsigned long long wave_min_u64(unsigned long long x) {
