@@ -164,22 +164,27 @@ def product_codebooks(wl, tokens=1024):
 KIND_BITS = {"partial": 0, "combine": 1, "append": 2, "topk": 3}
 
 
-def run_gpu(wl, steps, warmup, replicas=1, label="", prof_steps=24):
+def run_gpu(wl, steps, warmup, replicas=1, label="", prof_steps=24, graph_steps=0):
     """Prefill, `warmup` untimed steps, `steps` timed steps (HIP events around the attention partial
     launches, and nothing else), then `prof_steps` steps with every kernel kind timed (for the
-    per-kernel breakdown only)."""
+    per-kernel breakdown only), then `graph_steps` further steps captured into one HIP graph and
+    replayed once (reported beside the headline, which launches eagerly)."""
     import torch
     from paper_2609_07966_amd import _lib
     from paper_2609_07966_amd.cache import KVCache
     from workloads import prompt_kv, prompt_q, step_inputs
     S, Hq, Hkv, D = wl.n_seqs, wl.n_q_heads, wl.n_kv_heads, wl.head_dim
     cfgs = [wl.cfg(s) for s in range(S)]
-    total_steps = warmup + steps + prof_steps
+    total_steps = warmup + steps + prof_steps + graph_steps
     per_rep = math.ceil(total_steps / replicas)
     t0 = time.time()
     cb = product_codebooks(wl) if any(c["method"] == "kvq" for c in cfgs) else None
     dev = "cuda"
-    stream = torch.cuda.current_stream()
+    # a stream of our own (graph capture needs one that is not the default stream); the caches
+    # launch on it and it is current for everything else here
+    prev_stream = torch.cuda.current_stream()
+    stream = torch.cuda.Stream()
+    torch.cuda.set_stream(stream)
     caches = [KVCache((S, Hq, Hkv, D, per_rep), cfgs, wl.prompt_lens, codebooks=cb, device=dev, stream=stream)
               for _ in range(replicas)]
     # prompt K/V (all sequences), H2O prompt queries, RocketKV window queries
@@ -252,6 +257,19 @@ def run_gpu(wl, steps, warmup, replicas=1, label="", prof_steps=24):
     kinds = read_kinds(KIND_BITS)
     for c in caches:
         _lib.mkv_profile_enable(c.h, 0, 0)
+    graph_ms = None
+    if graph_steps:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for i in range(graph_steps):
+                t = warmup + steps + prof_steps + i
+                caches[t % replicas].step(kn[t], vn[t], qn[t], out)
+        torch.cuda.synchronize()
+        a = time.perf_counter()
+        g.replay()
+        torch.cuda.synchronize()
+        graph_ms = (time.perf_counter() - a) / graph_steps * 1e3
+        del g
     bytes_steps = [launch_bytes(wl, warmup + i, n_tiles) for i in range(steps)]
     avg_bytes = float(np.mean(bytes_steps))
     avg_part_ms = ms_part / max(n_part, 1)
@@ -262,10 +280,13 @@ def run_gpu(wl, steps, warmup, replicas=1, label="", prof_steps=24):
         "step_gbs": avg_bytes / (elapsed / steps) / 1e9,
         "n_tiles": n_tiles, "n_tiles_uq": n_uq, "n_tiles_rocket": n_rk, "replicas": replicas,
         "kernel_ms": {k: (v[1] / max(v[0], 1)) for k, v in kinds.items() if v[0]},
+        "graph_ms_per_step": graph_ms, "graph_steps": graph_steps,
     }
     for c in caches:
         c.close()
     del caches, kn, vn, qn, out
+    torch.cuda.synchronize()
+    torch.cuda.set_stream(prev_stream)
     torch.cuda.empty_cache()
     return res
 
@@ -364,7 +385,7 @@ def main():
         raise SystemExit("bench.py needs a GPU")
     from workloads import make_workload
     wl = make_workload("mixed", seed=args.seed, steps=args.warmup + args.steps)
-    head = run_gpu(wl, args.steps, args.warmup, label="mixed")
+    head = run_gpu(wl, args.steps, args.warmup, label="mixed", graph_steps=24)
     if args.copy_probe:
         copy_probe(args.copy_probe)
     ceiling = None if args.no_per_config else read_ceiling_gbs()
@@ -397,6 +418,9 @@ def main():
         "read_ceiling_GBs": None if ceiling is None else round(ceiling, 1),
         "attention_frac_of_read_ceiling": None if ceiling is None else round(head["partial_gbs"] / ceiling, 4),
         "kernel_us": {k: round(v * 1e3, 2) for k, v in head["kernel_ms"].items()},
+        "graph_replay": {"ms_per_step": round(head["graph_ms_per_step"], 4), "steps": head["graph_steps"],
+                         "note": "further decode steps of the same batch captured into one HIP graph and "
+                                 "replayed once; the headline launches eagerly"},
         "per_config": per_cfg,
         "cpu_baseline": cpu,
     }
