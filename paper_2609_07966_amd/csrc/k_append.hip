@@ -244,7 +244,7 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
   const int slot = sd.method == H2O ? (victim >= 0 ? victim : st[ST_FREE_SLOT]) : count;
   // a full region (reachable only by replaying a captured decode step past max_new_tokens) drops
   // the token instead of writing past the region; the decision is the same for every thread
-  if (slot >= sd.cap || (sd.method == KVQ && st[ST_KOUT_FILL] + D > sd.pool_cap)) return;
+  if (slot >= sd.cap || (sd.method == KVQ && sd.bp > 0 && st[ST_KOUT_FILL] + D > sd.pool_cap)) return;
   const uint32_t kb = k[((size_t)seq * Hkv + h) * D + c];
   const uint32_t vb = v[((size_t)seq * Hkv + h) * D + c];
   __syncthreads();  // every thread has read the state before thread 0 updates it

@@ -100,6 +100,19 @@ def test_edge_cases():
     _run(wl, 12)
 
 
+def test_kvquant_without_outliers():
+    # outlier_bp = 0: no outliers anywhere, every value from its code (and no key-outlier pool to
+    # fill); ragged prompts so that the decode tokens cross 4-token value blocks
+    wl = make_workload("custom", seed=12, n_seqs=3, n_q_heads=8, n_kv_heads=2, head_dim=128,
+                       prompt_lens=[300, 517, 129], steps=10, config_ids=[0, 0, 0])
+    wl.config_ids = [2, 3, 4]
+    cfgs = [{"id": 2, "name": "KVQ4-no-outliers", "method": "kvq", "bits": 4, "outlier_bp": 0},
+            {"id": 3, "name": "KVQ3-no-outliers", "method": "kvq", "bits": 3, "outlier_bp": 0},
+            {"id": 4, "name": "KVQ2", "method": "kvq", "bits": 2, "outlier_bp": 100}]
+    wl.cfg = lambda s: dict(cfgs[s])
+    _run(wl, 10)
+
+
 def test_batch_invariance():
     """Every sequence of a mixed batch gets exactly (bit for bit) the outputs, codes, selections
     and evictions of its solo run: the ragged launch shares no arithmetic between sequences."""
