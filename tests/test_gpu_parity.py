@@ -113,6 +113,19 @@ def test_kvquant_without_outliers():
     _run(wl, 10)
 
 
+def test_kvquant_large_outlier_budgets():
+    # several value outliers per token (outlier_bp 500 at d = 128: 6 per token) and about 3-6 key
+    # outliers per token: the multi-entry paths of the append and the attention
+    wl = make_workload("custom", seed=13, n_seqs=3, n_q_heads=8, n_kv_heads=2, head_dim=128,
+                       prompt_lens=[400, 233, 650], steps=10, config_ids=[0, 0, 0])
+    wl.config_ids = [2, 3, 4]
+    cfgs = [{"id": 2, "name": "KVQ4-5%", "method": "kvq", "bits": 4, "outlier_bp": 500},
+            {"id": 3, "name": "KVQ3-3%", "method": "kvq", "bits": 3, "outlier_bp": 300},
+            {"id": 4, "name": "KVQ2-2.5%", "method": "kvq", "bits": 2, "outlier_bp": 250}]
+    wl.cfg = lambda s: dict(cfgs[s])
+    _run(wl, 10)
+
+
 def test_batch_invariance():
     """Every sequence of a mixed batch gets exactly (bit for bit) the outputs, codes, selections
     and evictions of its solo run: the ragged launch shares no arithmetic between sequences."""
