@@ -126,6 +126,20 @@ def test_kvquant_large_outlier_budgets():
     _run(wl, 10)
 
 
+def test_small_budgets_and_selections():
+    # H2O budgets of a few tokens (B = 3 and 1: eviction from the first decode step on; with
+    # B = 1 the recent part R = floor(B / 2) is empty); RocketKV with a top-k of 8
+    wl = make_workload("custom", seed=14, n_seqs=3, n_q_heads=8, n_kv_heads=2, head_dim=128,
+                       prompt_lens=[300, 150, 700], steps=12, config_ids=[0, 0, 0])
+    wl.config_ids = [5, 5, 8]
+    cfgs = [{"id": 5, "name": "H2O-1%", "method": "h2o", "budget_pct": 1},
+            {"id": 5, "name": "H2O-B1", "method": "h2o", "budget_pct": 1},
+            {"id": 8, "name": "Rocket-top8", "method": "rocket", "keep_tokens": 64, "window": 32, "pool": 7,
+             "topk": 8, "n_channels": 32}]
+    wl.cfg = lambda s: dict(cfgs[s])
+    _run(wl, 12)
+
+
 def test_batch_invariance():
     """Every sequence of a mixed batch gets exactly (bit for bit) the outputs, codes, selections
     and evictions of its solo run: the ragged launch shares no arithmetic between sequences."""
