@@ -140,6 +140,15 @@ def test_small_budgets_and_selections():
     _run(wl, 12)
 
 
+def test_tiny_prompts_quantized():
+    # prompts of 1, 2 and 5 tokens under the quantizers (KVQuant calibrates its key thresholds on
+    # a handful of rows; uniform 4-bit starts with every key in the fp16 residual) and H2O
+    # (B = 1 at 5 prompt tokens); 9 steps complete the first 4-token value blocks
+    wl = make_workload("custom", seed=15, n_seqs=4, n_q_heads=8, n_kv_heads=2, head_dim=128,
+                       prompt_lens=[1, 2, 5, 5], steps=9, config_ids=["KVQ4", "UQ4-g64", "KVQ2", "H2O-20"])
+    _run(wl, 9)
+
+
 def test_batch_invariance():
     """Every sequence of a mixed batch gets exactly (bit for bit) the outputs, codes, selections
     and evictions of its solo run: the ragged launch shares no arithmetic between sequences."""
