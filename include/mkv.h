@@ -177,9 +177,11 @@ mkv_status mkv_snap_prefill_evict(mkv_cache *cache, const uint16_t *q_window, vo
 mkv_status mkv_topk_select(mkv_cache *cache, const uint16_t *q, int32_t *pos_out, void *stream);
 
 /*
- * One decode step's attention for every sequence: softmax(q k~ / sqrt(d)) v~
- * over the tokens the sequence's method keeps (all tokens for FP16, UQ and
- * KVQ with k~, v~ their dequantized values; the retained set for H2O, whose
+ * One decode step's attention for every sequence (Section 2.1: each method
+ * ends in attention over what its cache keeps; Section 2.3: one configuration
+ * per prompt, so a batch mixes methods): softmax(q k~ / sqrt(d)) v~ over the
+ * tokens the sequence's method keeps (all tokens for FP16, UQ and KVQ with
+ * k~, v~ their dequantized values; the retained set for H2O, whose
  * accumulated scores are updated here; the selected set for ROCKET).
  *   q   device fp16 [S][Hq][d]
  *   out device float32 [S][Hq][d]
@@ -187,8 +189,14 @@ mkv_status mkv_topk_select(mkv_cache *cache, const uint16_t *q, int32_t *pos_out
 mkv_status mkv_decode_attention(mkv_cache *cache, const uint16_t *q, float *out, void *stream);
 
 /*
- * The four decode calls in their order: append (k, v: device fp16
- * [S][Hkv][d]), top-k select, attention, eviction.
+ * The four decode calls in their order (one decode step of Section 2.1's
+ * methods, each sequence under its own configuration as Section 2.3 selects
+ * per prompt): append (k, v: device fp16 [S][Hkv][d]), top-k select,
+ * attention (q, out as for mkv_decode_attention), eviction.  Every argument
+ * and the call order are checked before the first kernel is enqueued: a
+ * rejected step (MKV_EINVAL for a NULL pointer, MKV_ESTATE, MKV_ECAPACITY)
+ * enqueues nothing and leaves the handle unchanged.  Only MKV_EHIP can come
+ * after a launch, and then the step may be partly enqueued.
  *
  * Graph capture: the step enqueues four kernels on `stream` and nothing else
  * (no allocation, copy, memset or synchronization; profiling events only

@@ -8,6 +8,7 @@
 #include "mkv.h"
 #include "mkv_internal.h"
 
+using mkv::report_error;
 using mkv::round_to_half;
 
 namespace {
@@ -85,8 +86,10 @@ std::vector<float> lloyd(std::vector<double> x, int bits) {
 
 extern "C" mkv_status mkv_fit_codebooks(const uint16_t *k, const uint16_t *v, int32_t n, int32_t Hkv, int32_t D,
                                         int32_t bits, int32_t bp, float *cb_k, float *cb_v) {
-  if (!k || !v || !cb_k || !cb_v || n < 1 || Hkv < 1 || D < 1 || bits < 1 || bits > 8 || bp < 0 || bp > 5000)
-    return MKV_EINVAL;
+  if (!k || !v || !cb_k || !cb_v) return report_error(MKV_EINVAL, "k, v, cb_k and cb_v must be non-NULL");
+  if (n < 1 || Hkv < 1 || D < 1) return report_error(MKV_EINVAL, "n_tokens, n_kv_heads and head_dim must be >= 1");
+  if (bits < 1 || bits > 8) return report_error(MKV_EINVAL, "bits must be in 1..8");
+  if (bp < 0 || bp > 5000) return report_error(MKV_EINVAL, "outlier_bp must be in 0..5000");
   std::vector<double> ks, vs;
   std::vector<float> col(n), row(D);
   for (int h = 0; h < Hkv; ++h) {
@@ -115,7 +118,7 @@ extern "C" mkv_status mkv_fit_codebooks(const uint16_t *k, const uint16_t *v, in
         }
     }
   }
-  if (ks.empty() || vs.empty()) return MKV_EINVAL;
+  if (ks.empty() || vs.empty()) return report_error(MKV_EINVAL, "no non-outlier samples to fit");
   const std::vector<float> a = lloyd(ks, bits), b = lloyd(vs, bits);
   std::copy(a.begin(), a.end(), cb_k);
   std::copy(b.begin(), b.end(), cb_v);

@@ -29,6 +29,14 @@ mkv_status fail(mkv_status s, const char *fmt, ...) {
   return s;
 }
 
+}  // namespace
+
+namespace mkv {
+mkv_status report_error(mkv_status s, const char *msg) { return fail(s, "%s", msg); }
+}  // namespace mkv
+
+namespace {
+
 mkv_status hip_fail(hipError_t e, const char *what) {
   return fail(MKV_EHIP, "%s: %s", what, hipGetErrorString(e));
 }
@@ -548,8 +556,14 @@ mkv_status mkv_decode_attention(mkv_cache *c, const uint16_t *q, float *out, voi
 mkv_status mkv_decode_step(mkv_cache *c, const uint16_t *k, const uint16_t *v, const uint16_t *q, float *out,
                            void *stream) {
   if (!c) return fail(MKV_EINVAL, "cache is NULL");
-  if (!k || !v) return fail(MKV_EINVAL, "k and v must be non-NULL");
+  if (!k || !v || !q || !out) return fail(MKV_EINVAL, "k, v, q and out must be non-NULL");
+  // every check of the four calls below, made before the first of them enqueues anything, so that
+  // a rejected step leaves the handle as it was; past this point only a HIP launch can fail
   if (c->phase == PH_CREATED) return fail(MKV_ESTATE, "decode step before the prefill append");
+  if (!(c->phase == PH_READY || (c->phase == PH_ATTENDED && !c->any_h2o)))
+    return fail(MKV_ESTATE, "decode step must follow prefill or a completed decode step");
+  if (c->steps >= c->sh.max_new)
+    return fail(MKV_ECAPACITY, "cache holds %d decode steps (max_new_tokens)", c->sh.max_new);
   mkv_status st = decode_append(c, k, v, static_cast<hipStream_t>(stream));
   if (st != MKV_OK) return st;
   if ((st = mkv_topk_select(c, q, nullptr, stream)) != MKV_OK) return st;

@@ -6,7 +6,12 @@
 
 #include <hip/hip_runtime.h>
 
+#include "mkv.h"
+
 namespace mkv {
+
+// Record `msg` as this thread's mkv_last_error() text and return `s` (host code only).
+mkv_status report_error(mkv_status s, const char *msg);
 
 enum Method : int32_t { FP16 = 0, UQ = 1, KVQ = 2, H2O = 3, ROCKET = 4 };
 

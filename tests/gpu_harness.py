@@ -250,24 +250,60 @@ class Run:
                     seq.apply_evictions([None] * h + [g_ev] + [None] * (wl.n_kv_heads - h - 1))
                     np.testing.assert_allclose(gsc, hd.score, rtol=1e-4, atol=1e-5)
                     continue
-            if check_codes and c["method"] in ("kvq",):
-                self._check_decode_codes(s, seq)
+            if check_codes and c["method"] in ("kvq", "uq"):
+                self._check_decode_codes(s, seq, t)
         return gout
 
-    def _check_decode_codes(self, s, seq):
-        wl = self.wl
+    def _check_decode_codes(self, s, seq, t):
+        """Every token's codes (prompt and decode alike) against the oracle's quantizer, bit for
+        bit: KVQuant key / value codes, outlier sets and values, per-token value scales; uniform
+        4-bit value codes and (min, step) pairs of every token and key codes and pairs of every
+        complete 64-token block (blocks completed during decode included)."""
+        wl, D = self.wl, self.wl.head_dim
+        where = f"seq {s} step {t}"
         for h in range(wl.n_kv_heads):
-            n = seq.kq[h]["codes"].shape[0]
-            gk = self.cache.export(s, h, "codes_k").reshape(-1, wl.head_dim)[:n]
-            np.testing.assert_array_equal(gk, seq.kq[h]["codes"])
-            gv = self.cache.export(s, h, "codes_v").reshape(-1, wl.head_dim)[:n]
-            np.testing.assert_array_equal(gv, seq.vq[h]["codes"])
-            gok = self.cache.export(s, h, "outliers_k").reshape(-1, wl.head_dim)[:n]
-            np.testing.assert_array_equal(gok >= 0, seq.kq[h]["outlier"])
+            if seq.method == "kvq":
+                kq, vq = seq.kq[h], seq.vq[h]
+                n = kq["codes"].shape[0]
+                gk = self.cache.export(s, h, "codes_k").reshape(-1, D)[:n]
+                np.testing.assert_array_equal(gk, kq["codes"], err_msg=f"key codes {where} head {h}")
+                gv = self.cache.export(s, h, "codes_v").reshape(-1, D)[:n]
+                np.testing.assert_array_equal(gv, vq["codes"], err_msg=f"value codes {where} head {h}")
+                gok = self.cache.export(s, h, "outliers_k").reshape(-1, D)[:n]
+                np.testing.assert_array_equal(gok >= 0, kq["outlier"], err_msg=f"key outliers {where} head {h}")
+                np.testing.assert_array_equal(gok[kq["outlier"]].astype(np.uint16),
+                                              kq["raw"].view(np.uint16)[kq["outlier"]])
+                gov = self.cache.export(s, h, "outliers_v").reshape(-1, D)[:n]
+                np.testing.assert_array_equal(gov >= 0, vq["outlier"], err_msg=f"value outliers {where} head {h}")
+                np.testing.assert_array_equal(gov[vq["outlier"]].astype(np.uint16),
+                                              vq["raw"].view(np.uint16)[vq["outlier"]])
+                np.testing.assert_array_equal(self.cache.export(s, h, "scales_v")[:n], vq["scale"],
+                                              err_msg=f"value scales {where} head {h}")
+            else:
+                kk, vv = seq.k[h], seq.v[h]
+                n = kk.shape[0]
+                nb = n // 64
+                cv, mnv, rv = uniform.quantize_value_rows(vv, 4)
+                gv = self.cache.export(s, h, "codes_v").reshape(-1, D)[:n]
+                np.testing.assert_array_equal(gv, cv, err_msg=f"uniform value codes {where} head {h}")
+                sv = self.cache.export(s, h, "scales_v").reshape(n, D // 64, 2)
+                np.testing.assert_array_equal(sv[..., 0], mnv, err_msg=f"uniform value minima {where} head {h}")
+                np.testing.assert_array_equal(sv[..., 1], (rv / np.float32(15)).astype(np.float32),
+                                              err_msg=f"uniform value steps {where} head {h}")
+                gk = self.cache.export(s, h, "codes_k").reshape(-1, D)
+                assert gk.shape[0] == nb * 64, f"{where} head {h}: {gk.shape[0]} key code rows, {nb} blocks"
+                if nb:
+                    ck, mnk, rk = uniform.quantize_key_blocks(kk, 4)
+                    np.testing.assert_array_equal(gk, ck, err_msg=f"uniform key codes {where} head {h}")
+                    sk = self.cache.export(s, h, "scales_k").reshape(nb, D, 2)
+                    np.testing.assert_array_equal(sk[..., 0], mnk, err_msg=f"uniform key minima {where} head {h}")
+                    np.testing.assert_array_equal(sk[..., 1], (rk / np.float32(15)).astype(np.float32),
+                                                  err_msg=f"uniform key steps {where} head {h}")
 
     def run(self, check_codes=True):
         self.prefill(check_codes=check_codes)
+        checked = {self.steps - 1, self.steps // 2}
         for t in range(self.steps):
-            self.step(t, check_codes=check_codes and t == self.steps - 1)
+            self.step(t, check_codes=check_codes and t in checked)
         self.cache.close()
         return self

@@ -123,3 +123,37 @@ def test_host_codebook_fit_equals_oracle(L, bits):
     got_k, got_v = L.mkv_fit_codebooks(k.tobytes(), v.tobytes(), 256, 2, 64, bits, 100)
     np.testing.assert_array_equal(np.array(got_k, np.float32), ref_k)
     np.testing.assert_array_equal(np.array(got_v, np.float32), ref_v)
+
+
+def test_create_rejects_short_arena_and_bad_codebooks_on_the_host(L):
+    """mkv_cache_create checks the arena and the codebooks before any device work, so these
+    rejections need no GPU (the fake arena address is never dereferenced)."""
+    cfgs = [CONFIGS[0], CONFIGS[3]]
+    shape = _shape(S=2, mn=4)
+    need = L.mkv_cache_bytes(shape, cfgs, [300, 400])
+    cb = []
+    for b in (2, 3, 4):
+        grid = np.linspace(-1, 1, 1 << b).astype(np.float16).astype(np.float32).tolist()
+        cb += grid + grid
+    fake = 1 << 40
+
+    def status(codebooks, nbytes=need, ptr=fake):
+        with pytest.raises(L.MkvError) as e:
+            L.mkv_cache_create(shape, cfgs, [300, 400], codebooks, ptr, nbytes, 0)
+        return e.value.status
+
+    assert status(cb, need - 1) == 2
+    assert status(cb, need, fake + 64) == 1
+    assert status(None) == 1
+    bad = list(cb)
+    bad[5] += 1e-4
+    assert status(bad) == 1
+    desc = list(cb)
+    desc[8], desc[9] = desc[9], desc[8]
+    assert status(desc) == 1
+
+
+def test_fit_codebooks_reports_its_errors(L):
+    with pytest.raises(L.MkvError) as e:
+        L.mkv_fit_codebooks(b"\0" * 256, b"\0" * 256, 2, 1, 64, 9, 100)
+    assert e.value.status == 1 and "bits" in L.lib().mkv_last_error().decode()

@@ -144,6 +144,12 @@ def _oracle_dense(run, s, t, q, gout):
         elif c["method"] == "uq":
             kk = uniform.effective_keys(K[:, h], 4, 64)
             vv = uniform.effective_values(V[:, h], 4, 64)
+            n = K.shape[0]
+            nb = n // 64
+            ck, _, _ = uniform.quantize_key_blocks(K[:, h], 4)
+            cv, _, _ = uniform.quantize_value_rows(V[:, h], 4)
+            np.testing.assert_array_equal(run.cache.export(s, h, "codes_k").reshape(-1, wl.head_dim)[:nb * 64], ck)
+            np.testing.assert_array_equal(run.cache.export(s, h, "codes_v").reshape(-1, wl.head_dim)[:n], cv)
         else:
             b, bp = c["bits"], c.get("outlier_bp", 100)
             cbk, cbv = run.cbs[b]
@@ -276,10 +282,11 @@ class H2OWatch:
 
 
 def test_fullsize_llama_layer_fp16_uq_kvquant():
-    """8 sequences x 4096-token prompts, 32q/8kv x 128, 128 steps: two sequences each of FP16,
-    uniform 4-bit, KVQuant 4-bit and KVQuant 2-bit; sampled steps 0, 63 and 127."""
+    """8 sequences x 4096-token prompts, 32q/8kv x 128, 128 steps: FP16, uniform 4-bit and
+    KVQuant 4-, 3- and 2-bit (the Llama-layer workload's configurations); sampled steps 0, 63
+    and 127, codes of every token compared bit for bit."""
     wl = make_workload("llama_layer", seed=0,
-                       config_ids=["FP16", "UQ4-g64", "KVQ4", "KVQ2", "FP16", "UQ4-g64", "KVQ4", "KVQ2"])
+                       config_ids=["FP16", "UQ4-g64", "KVQ4", "KVQ3", "KVQ2", "FP16", "UQ4-g64", "KVQ3"])
     _log(f"[full] llama layer: {wl.n_seqs} x {wl.prompt_lens[0]}, cfgs {wl.config_ids}, 128 steps")
     run = FullRun(wl, 128)
     run.prefill()
@@ -288,7 +295,7 @@ def test_fullsize_llama_layer_fp16_uq_kvquant():
     worst = 0.0
     for t in samples:
         _, _, q = run.step_inputs(t)
-        for s in (0, 1, 2, 7):
+        for s in (0, 1, 2, 3, 4):
             worst = max(worst, _oracle_dense(run, s, t, q, outs[t]))
     _log(f"[full]   max normalised error {worst:.2e}")
     run.cache.close()
@@ -300,6 +307,21 @@ def test_fullsize_h2o_properties():
     _log(f"[full] h2o: {wl.n_seqs} x {wl.prompt_lens[0]}, 256 steps")
     run = FullRun(wl, 256)
     run.prefill()
+    # the prefill keep-set and scores of two (sequence, kv head) pairs against the oracle's
+    # causal column sums over the whole 8192-token prompt
+    from gpu_harness import _keep_set_tie_ok
+    from oracle import h2o as oh2o
+    G = wl.group
+    for s, h in ((0, 0), (5, 3)):
+        kp = run.prompts[s][0]
+        n0 = kp.shape[0]
+        B, R = budget(run.cfgs[s]["budget_pct"], n0)
+        S = oh2o.prefill_scores(prompt_q(wl, s)[:, h * G:(h + 1) * G], kp[:, h])
+        gk = np.asarray(run.cache.export(s, h, "positions"), np.int64)
+        ok, nt = _keep_set_tie_ok(S, gk, oh2o.prefill_keep(S, B, R), set(range(n0 - R, n0)))
+        assert ok, f"H2O prefill keep-set of seq {s} head {h} differs beyond the tie band"
+        np.testing.assert_allclose(run.cache.export(s, h, "scores"), S[gk], rtol=1e-4, atol=1e-5)
+        _log(f"[full]   prefill keep-set seq {s} head {h}: {len(gk)} kept, {nt} near-tie swaps")
     watch = H2OWatch(run, (0, 5))
     samples = (0, 100, 255)
     outs = run.run(set(samples), watches=[watch])

@@ -149,6 +149,16 @@ def test_tiny_prompts_quantized():
     _run(wl, 9)
 
 
+@pytest.mark.parametrize("hq,n0", [(4, 13001), (8, 7001)])
+def test_h2o_large_retained_sets(hq, n0):
+    # H2O-50 with one kv head of d = 64: B = 6500 (G = 4) and 3500 (G = 8) retained slots, more
+    # than the combine pass scores in one round of its workgroup (6144 and 3072 slots), so the
+    # score accumulation and the victim search also run their later rounds
+    wl = make_workload("custom", seed=16, n_seqs=1, n_q_heads=hq, n_kv_heads=1, head_dim=64,
+                       prompt_lens=[n0], steps=4, config_ids=["H2O-50"], boost_frac=0.05, boost=3.0)
+    _run(wl, 4)
+
+
 def test_batch_invariance():
     """Every sequence of a mixed batch gets exactly (bit for bit) the outputs, codes, selections
     and evictions of its solo run: the ragged launch shares no arithmetic between sequences."""

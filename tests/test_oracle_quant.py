@@ -212,3 +212,66 @@ def test_kvq_sequence_dequant_error_is_bounded_by_the_codebook_gap():
         vq = seq.vq[h]
         verr = np.abs(vq["eff"] - vq["raw"].astype(np.float64))
         assert np.all(verr[~vq["outlier"]] <= (vq["scale"][:, None] / 15 * (1 + 1e-6)).repeat(64, 1)[~vq["outlier"]])
+
+
+def test_uniform_value_groups_are_consecutive_channels():
+    """Values are grouped per token over 64 consecutive channels: the exact minimum of every
+    (token, channel 64g .. 64g + 63) group comes back exactly, its maximum to float32 rounding,
+    and every code equals a brute-force quantizer of that slice in exact rationals (a grouping
+    over any other channel sets moves some group's extremes and codes)."""
+    r = np.random.default_rng(16)
+    n, d = 40, 256
+    v = (r.standard_normal((n, d)) * r.lognormal(0, 0.7, d)).astype(np.float16)
+    eff = uniform.effective_values(v, 4)
+    codes, mn, rr = uniform.quantize_value_rows(v, 4)
+    assert codes.shape == (n, d) and mn.shape == (n, d // 64)
+    for t in range(n):
+        for g in range(d // 64):
+            sl = slice(64 * g, 64 * g + 64)
+            x = [Fraction(float(a)) for a in v[t, sl]]
+            lo, hi = min(x), max(x)
+            assert Fraction(float(eff[t, sl].min())) == lo
+            assert abs(float(eff[t, sl].max()) - float(hi)) <= 1e-6 * max(abs(float(hi)), 1e-3)
+            assert Fraction(float(mn[t, g])) == lo
+            for j, xj in enumerate(x):
+                u = (xj - lo) * 15 / (hi - lo)
+                if abs(u - int(u) - Fraction(1, 2)) > Fraction(1, 10**4):
+                    assert codes[t, 64 * g + j] == round(u), (t, g, j)
+
+
+def _brute_threshold(col, n_o):
+    """n_o-th largest magnitude (0-based), found by counting rather than sorting: the value a
+    with at most n_o magnitudes strictly above it and at least n_o + 1 at or above it."""
+    mags = [abs(Fraction(float(x))) for x in col]
+    for a in mags:
+        above = sum(1 for m in mags if m > a)
+        atleast = sum(1 for m in mags if m >= a)
+        if above <= n_o < atleast:
+            return a
+    raise AssertionError("no order statistic")
+
+
+@pytest.mark.parametrize("bp", [100, 400])
+def test_normalised_inliers_brute_force(bp):
+    """The codebook-fitting samples: per channel (keys) or per token (values), every entry at or
+    below its threshold, scaled by the float32 reciprocal of the threshold; the threshold is
+    found by counting magnitudes in exact rationals."""
+    r = np.random.default_rng(17 + bp)
+    k = (r.standard_normal((150, 8)) * r.lognormal(0, 1.0, 8)).astype(np.float16)
+    v = r.standard_normal((30, 64)).astype(np.float16)
+    want_k = []
+    for c in range(k.shape[1]):
+        tau = _brute_threshold(k[:, c], kvquant.outlier_count(k.shape[0], bp))
+        inv = np.float32(1.0) / np.float32(float(tau))
+        want_k += [float(np.float32(np.float32(float(x)) * inv)) for x in k[:, c]
+                   if abs(Fraction(float(x))) <= tau]
+    got_k = kvquant.normalised_inliers_keys(k, bp)
+    assert sorted(got_k.tolist()) == sorted(want_k)
+    want_v = []
+    for t in range(v.shape[0]):
+        s = _brute_threshold(v[t], kvquant.outlier_count(v.shape[1], bp))
+        inv = np.float32(1.0) / np.float32(float(s))
+        want_v += [float(np.float32(np.float32(float(x)) * inv)) for x in v[t] if abs(Fraction(float(x))) <= s]
+    got_v = kvquant.normalised_inliers_values(v, bp)
+    assert sorted(got_v.tolist()) == sorted(want_v)
+    assert np.all(np.abs(got_k) <= 1.0 + 2 ** -23) and np.all(np.abs(got_v) <= 1.0 + 2 ** -23)
