@@ -189,6 +189,21 @@ mkv_status mkv_topk_select(mkv_cache *cache, const uint16_t *q, int32_t *pos_out
 mkv_status mkv_decode_attention(mkv_cache *cache, const uint16_t *q, float *out, void *stream);
 
 /*
+ * mkv_decode_attention for callers that cannot allocate device memory, or
+ * must not touch the cache arena's workspace, during a step (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation).
+ * Same arguments, order rules and results as mkv_decode_attention; the
+ * split-K partials of the attention tiles go to a static device workspace of
+ * 8 MiB per GPU (held until the process ends) instead of the arena.  Calls no
+ * allocating routine.  MKV_ENOMEM if the step's partials (attention tiles x
+ * G x (d + 2) floats; see mkv_attention_tiles) exceed 8 MiB.  All calls on one
+ * GPU share the workspace: calls that overlap on one GPU (other streams,
+ * other handles, other threads) race and must be serialised by the caller.
+ * The device that is current must be the cache's device.
+ */
+mkv_status mkv_decode_attention_noalloc(mkv_cache *cache, const uint16_t *q, float *out, void *stream);
+
+/*
  * The four decode calls in their order (one decode step of Section 2.1's
  * methods, each sequence under its own configuration as Section 2.3 selects
  * per prompt): append (k, v: device fp16 [S][Hkv][d]), top-k select,

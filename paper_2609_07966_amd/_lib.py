@@ -53,6 +53,7 @@ _SIGS = {
     "mkv_snap_prefill_evict": (_I, [_P, _P, _P]),
     "mkv_topk_select": (_I, [_P, _P, _P, _P]),
     "mkv_decode_attention": (_I, [_P, _P, _P, _P]),
+    "mkv_decode_attention_noalloc": (_I, [_P, _P, _P, _P]),
     "mkv_decode_step": (_I, [_P, _P, _P, _P, _P, _P]),
     "mkv_export": (_I, [_P, _I, _I, _I, _P, ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t)]),
     "mkv_fit_codebooks": (_I, [_P, _P, _I, _I, _I, _I, _I, ctypes.POINTER(ctypes.c_float),
@@ -153,6 +154,10 @@ def mkv_topk_select(h, q_ptr, pos_out_ptr, stream):
 
 def mkv_decode_attention(h, q_ptr, out_ptr, stream):
     _check(lib().mkv_decode_attention(h, _P(q_ptr), _P(out_ptr), _P(stream)))
+
+
+def mkv_decode_attention_noalloc(h, q_ptr, out_ptr, stream):
+    _check(lib().mkv_decode_attention_noalloc(h, _P(q_ptr), _P(out_ptr), _P(stream)))
 
 
 def mkv_decode_step(h, k_ptr, v_ptr, q_ptr, out_ptr, stream):

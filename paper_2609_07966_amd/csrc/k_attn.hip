@@ -26,9 +26,43 @@
 // Logits use the base-2 exponent (scaled by log2(e)/sqrt(d)).  fp16-row tiles keep the loads of
 // the next 16 tokens in flight while computing the current 16; the other paths issue the loads
 // of a 32-token batch before computing any of it.
+#include <mutex>
+
 #include "kernels_common.h"
 
+// Split-K workspace of mkv_decode_attention_noalloc, for callers that cannot allocate: the
+// partial (max, sum, output) of every attention tile lives here instead of in the cache arena.
+// Each GPU the library runs on holds one copy until the process ends; every call on a GPU shares
+// it, so calls that overlap on one GPU race.  Nothing in it needs clearing between calls: each
+// tile writes its whole partial before the combine pass reads it.
+static __device__ __align__(256) float scratch[mkv::kStaticScratchBytes / sizeof(float)];
+
 namespace mkv {
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+float *g_scratch_ptr[kMaxDevices];
+}  // namespace
+
+hipError_t static_scratch(float **ptr, size_t *bytes) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  // the array's device address on this device, looked up once with the device current (in host
+  // code the name `scratch` is only a host-side stand-in and must never reach a kernel)
+  std::call_once(g_scratch_once[dev], [dev] {
+    void *p = nullptr;
+    g_scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    g_scratch_ptr[dev] = static_cast<float *>(p);
+  });
+  if (g_scratch_err[dev] != hipSuccess) return g_scratch_err[dev];
+  *ptr = g_scratch_ptr[dev];
+  *bytes = kStaticScratchBytes;
+  return hipSuccess;
+}
 
 namespace {
 

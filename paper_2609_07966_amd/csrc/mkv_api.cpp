@@ -553,6 +553,34 @@ mkv_status mkv_decode_attention(mkv_cache *c, const uint16_t *q, float *out, voi
   return MKV_OK;
 }
 
+mkv_status mkv_decode_attention_noalloc(mkv_cache *c, const uint16_t *q, float *out, void *stream) {
+  if (!c) return fail(MKV_EINVAL, "cache is NULL");
+  if (!q || !out) return fail(MKV_EINVAL, "q and out must be non-NULL");
+  if (!(c->phase == PH_SELECTED || (c->phase == PH_APPENDED && !c->any_rocket)))
+    return fail(MKV_ESTATE, "attention must follow the decode append (and top-k selection)");
+  const size_t need = sizeof(float) * (size_t)c->dv.n_tiles * c->sh.G * (c->sh.D + 2);
+  if (need > kStaticScratchBytes)
+    return fail(MKV_ENOMEM, "split-K workspace of %zu bytes exceeds the %zu-byte static workspace", need,
+                kStaticScratchBytes);
+  float *ws = nullptr;
+  size_t ws_bytes = 0;
+  hipError_t e = static_scratch(&ws, &ws_bytes);
+  if (e != hipSuccess) return hip_fail(e, "static workspace address");
+  Dev dv = c->dv;
+  dv.partials = ws;
+  hipStream_t hst = static_cast<hipStream_t>(stream);
+  prof_mark(c, 0, 0, hst);
+  e = launch_attention_partial(dv, c->sh, q, hst);
+  prof_mark(c, 0, 1, hst);
+  if (e != hipSuccess) return hip_fail(e, "attention partial");
+  prof_mark(c, 1, 0, hst);
+  e = launch_attention_combine(dv, c->sh, out, hst);
+  prof_mark(c, 1, 1, hst);
+  if (e != hipSuccess) return hip_fail(e, "attention combine");
+  c->phase = PH_ATTENDED;
+  return MKV_OK;
+}
+
 mkv_status mkv_decode_step(mkv_cache *c, const uint16_t *k, const uint16_t *v, const uint16_t *q, float *out,
                            void *stream) {
   if (!c) return fail(MKV_EINVAL, "cache is NULL");

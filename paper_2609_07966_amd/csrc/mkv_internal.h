@@ -128,6 +128,10 @@ hipError_t launch_append_decode(const Dev &dv, const Shape &sh, const uint16_t *
 hipError_t launch_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
                               const uint16_t *k, const uint16_t *v, hipStream_t st);
 hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st);
+// The static split-K workspace of the current device (kStaticScratchBytes), its address looked up
+// on the first call per device.
+constexpr size_t kStaticScratchBytes = size_t(8) << 20;
+hipError_t static_scratch(float **ptr, size_t *bytes);
 hipError_t launch_attention_combine(const Dev &dv, const Shape &sh, float *out, hipStream_t st);
 hipError_t launch_topk(const Dev &dv, const Shape &sh, const uint16_t *q, int32_t *pos_out, int topk_max,
                        hipStream_t st);
