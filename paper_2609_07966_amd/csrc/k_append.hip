@@ -142,8 +142,17 @@ MKV_DEV int kvq_value_token(const SeqDesc &sd, int h, int t, uint32_t vbits, con
   const int r = flag_rank<D>(outl, s_tmp, &total);
   // slot-major: entry r of token t at r * cap + t
   uint32_t *vo = reinterpret_cast<uint32_t *>(sd.vout) + h * stride_vout(sd) + t;
-  if (outl && r < sd.nov_slots) vo[(size_t)r * sd.cap] = outlier_entry(vbits, t, code, c);
-  if (c >= total && c < sd.nov_slots) vo[(size_t)c * sd.cap] = kNoOutlier;
+  uint32_t *vd = reinterpret_cast<uint32_t *>(sd.vdel) + h * stride_vout(sd) + t;
+  if (outl && r < sd.nov_slots) {
+    vo[(size_t)r * sd.cap] = outlier_entry(vbits, t, code, c);
+    // the attention's form: the outlier minus the value its code stands for, and the channel
+    const float cbv = cbtab[cb_offset(sd.bits) + nc + code];
+    vd[(size_t)r * sd.cap] = vdel_pack(__fsub_rn(x, __fmul_rn(s, cbv)), c);
+  }
+  if (c >= total && c < sd.nov_slots) {
+    vo[(size_t)c * sd.cap] = kNoOutlier;
+    vd[(size_t)c * sd.cap] = 0u;
+  }
   if (c == 0) (reinterpret_cast<float *>(sd.vmeta) + h * stride_slots(sd))[t] = s;
   return code;
 }
@@ -521,9 +530,9 @@ __global__ void k_init_state(int32_t *state, int n) {
 
 template <int D>
 hipError_t append_decode_impl(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
-                              hipStream_t st) {
-  hipLaunchKernelGGL(k_append_decode<D>, dim3(sh.S * sh.Hkv), dim3(D), 0, st, dv.seqs, dv.state, k, v,
-                     dv.cbtab, sh.Hkv);
+                              hipStream_t st, LaunchEv ev) {
+  hipExtLaunchKernelGGL(k_append_decode<D>, dim3(sh.S * sh.Hkv), dim3(D), 0, st, ev.start, ev.stop, 0, dv.seqs,
+                        dv.state, k, v, dv.cbtab, sh.Hkv);
   return hipGetLastError();
 }
 
@@ -566,8 +575,8 @@ hipError_t prefill_impl(const Dev &dv, const Shape &sh, const SeqDesc &hs, int s
 }  // namespace
 
 hipError_t launch_append_decode(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
-                                hipStream_t st) {
-  return sh.D == 64 ? append_decode_impl<64>(dv, sh, k, v, st) : append_decode_impl<128>(dv, sh, k, v, st);
+                                hipStream_t st, LaunchEv ev) {
+  return sh.D == 64 ? append_decode_impl<64>(dv, sh, k, v, st, ev) : append_decode_impl<128>(dv, sh, k, v, st, ev);
 }
 
 hipError_t launch_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq, const uint16_t *k,

@@ -82,7 +82,7 @@ MKV_DEV f4v mfma16(h4v a, h4v b, f4v c) { return __builtin_amdgcn_mfma_f32_16x16
 MKV_DEV uint32_t pk_lo(uint32_t a, uint32_t b) { return __builtin_amdgcn_perm(b, a, 0x05040100u); }
 MKV_DEV uint32_t pk_hi(uint32_t a, uint32_t b) { return __builtin_amdgcn_perm(b, a, 0x07060302u); }
 MKV_DEV uint32_t f16bits(float x) { return (uint32_t)__builtin_bit_cast(unsigned short, (_Float16)x); }
-MKV_DEV uint32_t pk_f16(float lo, float hi) { return f16bits(lo) | (f16bits(hi) << 16); }
+MKV_DEV uint32_t pk_f16(float lo, float hi) { return __builtin_bit_cast(uint32_t, h2v{(_Float16)lo, (_Float16)hi}); }
 
 // ================================================================================================
 // Matrix path
@@ -196,9 +196,8 @@ struct MRows {
   MKV_DEV void kfix(int, float (&)[4]) const {}
   MKV_DEV float vscale(const Raw &, int) const { return 1.f; }
   MKV_DEV void vfix(const Raw &, const float (&)[4], const float (&)[4], int) const {}
-  MKV_DEV void track_max(float) {}
   MKV_DEV void prep(int, QB<D> &) {}
-  MKV_DEV void rescale(float) {}
+  MKV_DEV void rescale(float) const {}
   MKV_DEV void pv(const Raw &r, const float (&)[4], const float (&pp)[4], int, f4v (&O)[NM]) const {
     const h4v P = mk_h4(pk_f16(pp[0], pp[1]), pk_f16(pp[2], pp[3]));
 #pragma unroll
@@ -212,14 +211,16 @@ struct MRows {
 };
 
 // KVQuant-style b-bit codes.  Key codes: code c of a row at bit b*c, so channels (2p, 2p+1)
-// form a 2b-bit field p.  Value codes: 4-token blocks with code (channel c, token j) at bit
-// b*(4c + j), so the tokens (0,1) and (2,3) of a channel form two 2b-bit fields.  A field
-// indexes a table of packed fp16 pairs (cb[first code], cb[second code]).
+// form a 2b-bit field p and channels 4m..4m+3 (one matrix operand) a 4b-bit one.  Value codes:
+// 4-token blocks with code (channel c, token j) at bit b*(4c + j), so a channel's 4 tokens (one
+// matrix operand) form a 4b-bit field.  At 2 bits that field is one byte and indexes a table of
+// packed fp16 quads; at 3 and 4 bits it is two 2b-bit fields indexing a table of packed fp16
+// pairs (cb[first code], cb[second code]).  The tables are built on the host at cache creation.
 template <int D, int G, int BITS>
 struct MKVQ {
   static constexpr int NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
-  static constexpr int NS = 2;           // 32-token batches (the key-outlier gather assumes 32)
-  static constexpr bool kSplit = true;   // fp16 residuals of q' and p in columns G..2G-1
+  static constexpr int NS = 2;           // 32-token batches (the key-outlier tags are slot mod 32)
+  static constexpr bool kSplit = true;   // fp16 residual of q' in columns G..2G-1
   static constexpr bool kScaled = true;  // q' carries log2(e)/sqrt(d)
   static constexpr int SEG = CPL * BITS;  // bits per lane segment (keys; values alike)
   // words per segment: a segment starts at bit SEG * lane_index, which is word aligned unless
@@ -227,25 +228,20 @@ struct MKVQ {
   static constexpr int NW = (SEG + 31) / 32;
   static constexpr int FMASK = (1 << (2 * BITS)) - 1;
   const uint8_t *kc, *vc;
-  const uint32_t *krow, *kout, *vout;
+  const uint32_t *krow, *kout, *vdel;
   const float *vsc;
-  const uint32_t *lutk, *lutv;    // LDS pair tables
-  const float *cbk, *cbv;         // LDS codebooks
+  const uint32_t *lutk, *lutv;    // LDS tables: quads (2 words per entry) at 2 bits, else pairs
+  const float *cbk;               // LDS key codebook
   const float *qq;                // LDS [D][2G]: scaled q of heads 0..G-1, then scaled q tau
-  float *vcorr;                   // LDS [D]: this lane's value-outlier terms (head lr), relative to vref
+  float *vacc;                    // LDS [G][D]: this wave's value-outlier terms
   float *kterm;                   // LDS [64][G]: this wave's per-entry key-outlier logit terms
   float *kcorr;                   // LDS [G + 1][32]: this wave's key-outlier logit terms of the
                                   // batch (row G stays zero)
   int lr, lq, rowbytes, nov, cap;
-  int prole;                      // p operand: 0 fp16 part, 1 residual, 2 zero
-  // The value-outlier terms of head lr are kept relative to a reference max vref <= m_run that
-  // moves only when m_run exceeds it by more than 8 (so the terms are rarely rescaled); a term
-  // computed against m_run is multiplied by vscl = 2^(m_run - vref) <= 2^8.
-  float vref, vscl;
   struct Raw {
     uint32_t kw[NW], vw[NW];
     float sv[4];
-    uint32_t vo[4];
+    uint32_t vd[4];
     int t0;
   };
   struct Batch {
@@ -277,6 +273,16 @@ struct MKVQ {
     if (s + 2 * BITS <= 32) return (w[i] >> s) & FMASK;
     return __builtin_amdgcn_alignbit(w[i + 1], w[i], s) & FMASK;
   }
+  // operand m of a segment: 4 codes as 4 fp16 codebook values
+  MKV_DEV h4v operand(const uint32_t *lut, const uint32_t (&w)[NW], int m) const {
+    if constexpr (BITS == 2) {
+      const uint32_t q = (w[m >> 2] >> (8 * (m & 3))) & 0xFFu;
+      const uint2 e = *reinterpret_cast<const uint2 *>(lut + 2 * q);
+      return mk_h4(e.x, e.y);
+    } else {
+      return mk_h4(lut[field(w, 2 * m)], lut[field(w, 2 * m + 1)]);
+    }
+  }
   // this lane's 4 tokens form one 4-token block (tile and wave ranges start at multiples of 32);
   // past the end, the last block is re-read, whose slots all lie below the slot capacity (a
   // multiple of 4)
@@ -287,11 +293,16 @@ struct MKVQ {
     const int t0 = FULL ? base + 4 * lq : min(base + 4 * lq, (b - 1) & ~3);
     r.t0 = t0;
     seg(vc + (size_t)t0 * rowbytes, SEG * lr, r.vw);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      r.sv[j] = gld(vsc + t0 + j);
-      r.vo[j] = gld(vout + t0 + j);  // entry 0 of each token (slot-major entries)
-    }
+    const U4 s = gld16u(vsc + t0);
+    r.sv[0] = __builtin_bit_cast(float, s.x);
+    r.sv[1] = __builtin_bit_cast(float, s.y);
+    r.sv[2] = __builtin_bit_cast(float, s.z);
+    r.sv[3] = __builtin_bit_cast(float, s.w);
+    const U4 e = gld16u(vdel + t0);  // entry 0 of each token (slot-major entries)
+    r.vd[0] = e.x;
+    r.vd[1] = e.y;
+    r.vd[2] = e.z;
+    r.vd[3] = e.w;
   }
   // lane l takes entry l of the batch's key-outlier range
   MKV_DEV void batch_fetch(const Carry &cy, Batch &bt) const {
@@ -303,13 +314,12 @@ struct MKVQ {
   // Per head, the logit correction q x - q' cb[code] of every key outlier of the batch (each
   // replaces its channel), summed per slot: lane e computes the terms of entry e of the batch's
   // range (64 entries per round) into LDS, then lane t < 32 adds those of its slot's entries
-  // [k0, k1) and writes the sums to kcorr[head][t].
+  // [k0, k1) (the CSR range; LDS atomics measured slower here) and writes the sums to kcorr.
   MKV_DEV void batch_fix(const Batch &bt) const {
     const int lane = threadIdx.x & 63;
     const uint32_t e0 = __builtin_amdgcn_readlane(bt.kr, 0), e1 = __builtin_amdgcn_readlane(bt.kr, 32);
     const int total = (int)(e1 - e0);  // wave-uniform
     const int k0 = (int)(bt.kr - e0);
-    // every lane takes part in the shuffle (lane 31 reads lane 32); lanes >= 32 sum nothing
     const int next = (int)((uint32_t)__shfl_down((int)bt.kr, 1) - e0);
     const int k1 = lane < 32 ? next : k0;
     float acc[G];
@@ -318,13 +328,11 @@ struct MKVQ {
     for (int r0 = 0; r0 < total; r0 += 64) {
       const bool on = r0 + lane < total;
       uint32_t ent = bt.ent;
-      if (r0 > 0) ent = on ? gld(kout + e0 + r0 + lane) : kNoOutlier;  // more than 64 in one batch
-      // lanes without an entry compute with channel 0 and x = c = 0
+      if (r0 > 0) ent = on ? gld(kout + e0 + r0 + lane) : kNoOutlier;
       const int ch = on ? min(outlier_ch(ent), D - 1) : 0;
       const float x = on ? h2f(ent >> 16) : 0.f, c = on ? cbk[outlier_code(ent)] : 0.f;
 #pragma unroll
       for (int g = 0; g < G; ++g) kterm[lane * G + g] = qq[ch * 2 * G + g] * x - qq[ch * 2 * G + G + g] * c;
-      // this round's entries of slot t, four loads in flight per pass
       const int a = max(k0 - r0, 0), b = min(k1 - r0, 64);
       for (int i = a; i < b; i += 4) {
         float t[4][G];
@@ -346,8 +354,7 @@ struct MKVQ {
   MKV_DEV int slot(int, const Raw &r, int j) const { return r.t0 + j; }
   MKV_DEV void qk(const Raw &r, const QB<D> &qb, f4v &S) const {
 #pragma unroll
-    for (int m = 0; m < NM; ++m)
-      S = mfma16(mk_h4(lutk[field(r.kw, 2 * m)], lutk[field(r.kw, 2 * m + 1)]), qb.b[m], S);
+    for (int m = 0; m < NM; ++m) S = mfma16(operand(lutk, r.kw, m), qb.b[m], S);
   }
   // step s of the batch: this lane's tokens 16 s + 4 lq + j, head lr (columns lr >= G read the
   // zero row)
@@ -359,71 +366,52 @@ struct MKVQ {
     x[3] += c.w;
   }
   MKV_DEV float vscale(const Raw &r, int j) const { return r.sv[j]; }
-  // value outliers replace their channel: p x - p' cb[code] accumulates in this lane's LDS row
-  // (an absent or masked entry adds 0 to channel 0)
-  MKV_DEV void vfix(const Raw &r, const float (&p)[4], const float (&pp)[4], int valid_mask) const {
+  // value outliers replace their channel: p (x - s cb[code]) goes to the channel's LDS sum.  The
+  // append stores that difference d = x - s cb[code] per outlier as a float32 whose 7 lowest
+  // mantissa bits hold the channel (a relative change of d below 2^-16); 0.0 marks no outlier
+  // and adds nothing to channel 0.
+  MKV_DEV void vfix(const Raw &r, const float (&p)[4], const float (&)[4], int valid_mask) const {
     if (lr >= G) return;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint32_t ent = r.vo[j];
-      const bool ok = ((valid_mask >> j) & 1) && ent != kNoOutlier;
-      const float val = (p[j] * h2f(ent >> 16) - pp[j] * cbv[outlier_code(ent)]) * vscl;
-      vcorr[ok ? outlier_ch(ent) : 0] += ok ? val : 0.f;
+      const uint32_t ent = r.vd[j];
+      const bool ok = (valid_mask >> j) & 1;
+      atomicAdd(vacc + lr * D + (ok ? (int)(ent & 127u) : 0), ok ? p[j] * __builtin_bit_cast(float, ent) : 0.f);
     }
     if (nov > 1) {  // further entries (outlier budgets above one per token)
       for (int j = 0; j < 4; ++j) {
-        if (!((valid_mask >> j) & 1) || r.vo[j] == kNoOutlier) continue;
+        if (!((valid_mask >> j) & 1)) continue;
         for (int i = 1; i < nov; ++i) {
-          const uint32_t ent = gld(vout + (size_t)i * cap + r.t0 + j);
-          if (ent == kNoOutlier) break;
-          vcorr[outlier_ch(ent)] += (p[j] * h2f(ent >> 16) - pp[j] * cbv[outlier_code(ent)]) * vscl;
+          const uint32_t ent = gld(vdel + (size_t)i * cap + r.t0 + j);
+          if (ent == 0u) break;
+          atomicAdd(vacc + lr * D + (int)(ent & 127u), p[j] * __builtin_bit_cast(float, ent));
         }
       }
     }
   }
-  MKV_DEV void track_max(float m_run) {
-    if (m_run - vref > 8.f) {
-      if (lr < G && vref != -INFINITY) {
-        const float f = fexp2(vref - m_run);
-        float4 *row = reinterpret_cast<float4 *>(vcorr);
-        for (int c = 0; c < D / 4; ++c) {
-          float4 v = row[c];
-          v.x *= f;
-          v.y *= f;
-          v.z *= f;
-          v.w *= f;
-          row[c] = v;
-        }
-      }
-      vref = m_run;
-    }
-    vscl = fexp2(m_run - vref);
-  }
-  // factor that brings the terms to the final m_run (0 when there are none)
-  MKV_DEV float vfactor(float m_run) const { return vref == -INFINITY ? 0.f : fexp2(vref - m_run); }
   MKV_DEV void prep(int, QB<D> &) {}
-  MKV_DEV void rescale(float) {}
-  MKV_DEV void pv(const Raw &r, const float (&)[4], const float (&pp)[4], int, f4v (&O)[NM]) const {
-    uint32_t w[2];
+  // a rescale of the running sums rescales the value-outlier terms with them (each lane quad
+  // takes a quarter of its head's row)
+  MKV_DEV void rescale(float corr) const {
+    if (lr >= G) return;
+    float4 *row = reinterpret_cast<float4 *>(vacc + lr * D + lq * (D / 4));
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const float a = pp[2 * i], b = pp[2 * i + 1];
-      const float ah = (float)(_Float16)a, bh = (float)(_Float16)b;
-      w[i] = prole == 0 ? pk_f16(ah, bh) : prole == 1 ? pk_f16(a - ah, b - bh) : 0u;
+    for (int c = 0; c < D / 16; ++c) {
+      float4 v = row[c];
+      v.x *= corr;
+      v.y *= corr;
+      v.z *= corr;
+      v.w *= corr;
+      row[c] = v;
     }
-    const h4v P = mk_h4(w[0], w[1]);
+  }
+  MKV_DEV void pv(const Raw &r, const float (&)[4], const float (&pp)[4], int, f4v (&O)[NM]) const {
+    const h4v P = lr < G ? mk_h4(pk_f16(pp[0], pp[1]), pk_f16(pp[2], pp[3])) : mk_h4(0u, 0u);
 #pragma unroll
-    for (int m = 0; m < NM; ++m)
-      O[m] = mfma16(mk_h4(lutv[field(r.vw, 2 * m)], lutv[field(r.vw, 2 * m + 1)]), P, O[m]);
+    for (int m = 0; m < NM; ++m) O[m] = mfma16(operand(lutv, r.vw, m), P, O[m]);
   }
 };
 
-// The fp16 pair of p (or of p times a scale) for operand column lr: 0 its fp16 part, 1 the
-// rounding residual, 2 zero.
-MKV_DEV uint32_t p_pair(float a, float b, int role) {
-  const float ah = (float)(_Float16)a, bh = (float)(_Float16)b;
-  return role == 0 ? pk_f16(ah, bh) : role == 1 ? pk_f16(a - ah, b - bh) : 0u;
-}
 // the 4-bit nibbles k and k + 4 of w as a packed pair of fp16 integers: each becomes the fp16
 // value 1024 + n by an and-or, then n by one packed fp16 subtraction (both exact)
 MKV_DEV uint32_t nib_pair(uint32_t w, int k) {
@@ -445,7 +433,7 @@ struct MUQ {
   static constexpr int NGRP = D / 64;     // value groups
   static constexpr int KW = RES ? CPL / 2 : CPL / 8;  // key words per lane and step
   static constexpr int NS = RES ? 1 : 2;  // the fp16 block (at most 63 tokens) in 16-token batches
-  static constexpr bool kSplit = true;    // fp16 residuals of q'' and p' in columns G..2G-1
+  static constexpr bool kSplit = true;    // fp16 residual of q'' in columns G..2G-1
   static constexpr bool kScaled = true;   // q'' carries log2(e)/sqrt(d)
   const uint8_t *kc, *vc;
   const float *kmeta, *vmeta;             // float2 pairs (min, step)
@@ -572,7 +560,6 @@ struct MUQ {
   }
   MKV_DEV float vscale(const Raw &, int) const { return 1.f; }
   MKV_DEV void vfix(const Raw &, const float (&)[4], const float (&)[4], int) const {}
-  MKV_DEV void track_max(float) {}
   MKV_DEV void rescale(float corr) {
 #pragma unroll
     for (int gr = 0; gr < NGRP; ++gr) om[gr] *= corr;
@@ -591,7 +578,7 @@ struct MUQ {
         pp[j] = ok ? p[j] * ms.y : 0.f;
         om[gr] += ok ? p[j] * ms.x : 0.f;
       }
-      const h4v P = mk_h4(p_pair(pp[0], pp[1], prole), p_pair(pp[2], pp[3], prole));
+      const h4v P = lr < G ? mk_h4(pk_f16(pp[0], pp[1]), pk_f16(pp[2], pp[3])) : mk_h4(0u, 0u);
 #pragma unroll
       for (int m = 4 * gr; m < 4 * gr + 4 && m < NM; ++m) {
         const uint32_t w = r.vw[m >> 1];
@@ -601,6 +588,28 @@ struct MUQ {
     }
   }
 };
+
+// The running max of head lr moves only when a logit exceeds it by more than kLazyMax (log2
+// units): between moves the probabilities 2^(s - m_run) stay below 2^kLazyMax, well inside fp16
+// and float32, and most steps skip the cross-lane max and the rescale altogether.  The max that
+// is kept is a reference for the sums, not the exact maximum; the merges of waves and tiles
+// rescale by the references' differences, so the results are the same.
+constexpr float kLazyMax = 8.f;
+
+// Move head lr's reference to the wave-wide max of this step's logits (lane max `mx`) and
+// rescale the sums; called wave-uniformly.
+template <class L, int NM>
+MKV_DEV void rescale_to(L &ld, float mx, float &m_run, float &l_part, f4v (&O)[NM]) {
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const bool up = mx > m_run;
+  const float corr = up ? fexp2(m_run - mx) : 1.f;  // factor 1 for the heads whose max held
+  l_part *= corr;
+#pragma unroll
+  for (int m = 0; m < NM; ++m) O[m] *= corr;
+  ld.rescale(corr);
+  if (up) m_run = mx;
+}
 
 // One 16-token step of fp16 rows (the loads of the next step are already in flight).
 template <int D, int G, bool GATHER>
@@ -622,16 +631,7 @@ MKV_DEV void rows_step(const MRows<D, G, GATHER> &ld, const typename MRows<D, G,
     for (int j = 0; j < 4; ++j)
       if (sc[j] != -INFINITY) gst(logit_out + (size_t)(base + 4 * lq + j) * G + lr, sc[j]);
   }
-  mx = fmaxf(mx, __shfl_xor(mx, 16));
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
-  const bool up = mx > m_run;
-  if (__any(up)) {  // wave-uniform: rescale with factor 1 for the heads whose max held
-    const float corr = up ? fexp2(m_run - mx) : 1.f;
-    l_part *= corr;
-#pragma unroll
-    for (int m = 0; m < MG<D>::NM; ++m) O[m] *= corr;
-    if (up) m_run = mx;
-  }
+  if (__any(mx > m_run + kLazyMax)) rescale_to(ld, mx, m_run, l_part, O);
   float pp[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -709,20 +709,7 @@ MKV_DEV void mfma_batch(L &ld, int base, int b, typename L::Carry &cy, QB<D> &qb
       for (int j = 0; j < 4; ++j)
         if (FULL || sc[s][j] != -INFINITY) gst(logit_out + (size_t)ld.slot(base + 16 * s, raw[s], j) * G + lr, sc[s][j]);
   }
-  mx = fmaxf(mx, __shfl_xor(mx, 16));
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
-  const bool up = mx > m_run;
-  if (__any(up)) {  // wave-uniform: rescale with factor 1 for the heads whose max held
-    const float corr = up ? fexp2(m_run - mx) : 1.f;
-    l_part *= corr;
-#pragma unroll
-    for (int m = 0; m < MG<D>::NM; ++m) O[m] *= corr;
-    ld.rescale(corr);
-    if (up) {
-      m_run = mx;
-      ld.track_max(m_run);
-    }
-  }
+  if (__any(mx > m_run + kLazyMax)) rescale_to(ld, mx, m_run, l_part, O);
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
     float p[4], pp[4];
@@ -807,16 +794,15 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     const uint16_t *__restrict__ q, float *__restrict__ partials, const float *__restrict__ cbtab,
     int Hkv, float qscale) {
   constexpr int NW = kTileThreads / 64, NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
-  // per wave: KVQuant value-outlier terms, one row of D per (lane quad, head) while the wave
-  // runs; then the wave's (max, sum, o) for the merge
-  constexpr int kWaveFloats = 4 * G * D;
-  static_assert(kWaveFloats >= G * (D + 2), "wave region too small");
+  // per wave: KVQuant value-outlier terms [G][D] while the wave runs; then the wave's (max,
+  // sum, o) for the merge
+  constexpr int kWaveFloats = (G * (D + 2) + 3) & ~3;
   __shared__ __attribute__((aligned(16))) float s_wave[NW][kWaveFloats];
   __shared__ float s_q[D][2 * G];            // KVQuant: scaled q of each head, then scaled q * tau
-  __shared__ uint32_t s_lut[2][256];         // KVQuant: key and value pair tables
-  __shared__ float s_cb[2][16];              // KVQuant: codebooks
+  __shared__ __attribute__((aligned(16))) uint32_t s_lut[1024];  // KVQuant: key, then value table
+  __shared__ float s_cbk[16];                // KVQuant: key codebook
+  __shared__ __attribute__((aligned(16))) float s_kt[NW][64 * G];  // KVQuant per-entry key-outlier terms
   __shared__ __attribute__((aligned(16))) float s_kc[NW][G + 1][32];  // KVQuant key-outlier logit terms
-  __shared__ __attribute__((aligned(16))) float s_kt[NW][64 * G];      // KVQuant per-entry key-outlier terms
   __shared__ float2 s_vm[NW][64];            // uniform 4-bit: a batch's value (min, step) pairs
   __shared__ __attribute__((aligned(16))) float s_km[NW][2 * D];  // uniform 4-bit: a key block's pairs
 
@@ -841,18 +827,13 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     }
   }
   if (kvq) {
-    // codebook tables and q, q * tau for this kv head
+    // the codebook's lookup tables (copied as built on the host), the key codebook, and q,
+    // q * tau for this kv head
     const int bits = sd.bits, nc = 1 << bits;
-    const float *cb = cbtab + cb_offset(bits);
-    if (threadIdx.x < 32) {
-      const int which = threadIdx.x >> 4, i = threadIdx.x & 15;
-      s_cb[which][i] = i < nc ? cb[which * nc + i] : 0.f;
-    }
-    for (int e = threadIdx.x; e < 2 * (1 << (2 * bits)); e += kTileThreads) {
-      const int which = e >> (2 * bits), f = e & ((1 << (2 * bits)) - 1);
-      const float *c = cb + which * nc;
-      s_lut[which][f] = pk_f16(c[f & (nc - 1)], c[f >> bits]);  // first, second code of the field
-    }
+    const uint32_t *lut = reinterpret_cast<const uint32_t *>(cbtab + kLutBase) + lut_offset(bits);
+    for (int e = threadIdx.x; e < lut_half_words(bits) / 2; e += kTileThreads)
+      reinterpret_cast<uint4 *>(s_lut)[e] = gld16(lut + 4 * e);
+    if (threadIdx.x < 16) s_cbk[threadIdx.x] = threadIdx.x < nc ? cbtab[cb_offset(bits) + threadIdx.x] : 0.f;
     const float *tau = reinterpret_cast<const float *>(sd.kmeta) + (size_t)h * D * 2;
     for (int e = threadIdx.x; e < G * D; e += kTileThreads) {
       const int g = e / D, c = e % D;
@@ -861,7 +842,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
       s_q[c][G + g] = qx * gld(tau + 2 * c);
     }
     float4 *vz = reinterpret_cast<float4 *>(&s_wave[wave][0]);
-    for (int e = lane; e < kWaveFloats / 4; e += 64) vz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int e = lane; e < G * D / 4; e += 64) vz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
     float4 *kz = reinterpret_cast<float4 *>(&s_kc[wave][0][0]);
     for (int e = lane; e < (G + 1) * 32 / 4; e += 64) kz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
@@ -961,51 +942,34 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
       ld.vc = reinterpret_cast<const uint8_t *>(sd.vc) + h * stride_codes(sd);
       ld.krow = reinterpret_cast<const uint32_t *>(sd.krow) + h * stride_krow(sd);
       ld.kout = reinterpret_cast<const uint32_t *>(sd.kout) + h * stride_kout(sd);
-      ld.vout = reinterpret_cast<const uint32_t *>(sd.vout) + h * stride_vout(sd);
+      ld.vdel = reinterpret_cast<const uint32_t *>(sd.vdel) + h * stride_vout(sd);
       ld.vsc = reinterpret_cast<const float *>(sd.vmeta) + h * stride_slots(sd);
-      ld.lutk = s_lut[0];
-      ld.lutv = s_lut[1];
-      ld.cbk = s_cb[0];
-      ld.cbv = s_cb[1];
+      ld.lutk = s_lut;
+      ld.lutv = s_lut + lut_half_words(BITS);
+      ld.cbk = s_cbk;
       ld.qq = &s_q[0][0];
       ld.kcorr = &s_kc[wave][0][0];
       ld.kterm = s_kt[wave];
-      ld.vcorr = &s_wave[wave][(lq * G + (lr < G ? lr : 0)) * D];
+      ld.vacc = &s_wave[wave][0];
       ld.lr = lr;
       ld.lq = lq;
       ld.rowbytes = sd.rowbytes;
       ld.nov = sd.nov_slots;
       ld.cap = sd.cap;
-      ld.prole = lr < G ? 0 : lr < 2 * G ? 1 : 2;
-      ld.vref = -INFINITY;
-      ld.vscl = 1.f;
       wave_mfma<D, G>(ld, wr.a, wr.b, qb, qscale, m_run, l_part, O, nullptr);
-      // fold the value-outlier rows of head lr (one per lane quad) into this lane's channels
+      // fold the value-outlier terms of head lr into this lane's channels (the wave's LDS
+      // accesses complete in order, so the merge may reuse the region afterwards)
       if (lr < G) {
-        const float f = ld.vfactor(m_run);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
 #pragma unroll
-          for (int m = 0; m < NM; ++m) {
-            const int c = VPL * (4 * lq + i) + m;
-            float v = 0.f;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) v += s_wave[wave][(k * G + lr) * D + c];
-            O[m][i] += v * f;
-          }
+          for (int m = 0; m < NM; ++m) O[m][i] += s_wave[wave][lr * D + VPL * (4 * lq + i) + m];
         }
       }
     };
     if (sd.bits == 4) run(std::integral_constant<int, 4>{});
     else if (sd.bits == 3) run(std::integral_constant<int, 3>{});
     else run(std::integral_constant<int, 2>{});
-  }
-  // KVQuant, uniform 4-bit: column 2G-1-lr holds the products of head lr's p residual
-  if (kvq || uq) {
-#pragma unroll
-    for (int m = 0; m < NM; ++m)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) O[m][i] += mirror_cols<G>(O[m][i]);
   }
   if (uq) {
 #pragma unroll
@@ -1016,8 +980,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   // the 4 quads of a query head hold disjoint tokens
   l_part += __shfl_xor(l_part, 16);
   l_part += __shfl_xor(l_part, 32);
-  // this wave's (max, sum, o) over its own region (the outlier rows were folded above; a wave's
-  // LDS accesses complete in order)
+  // this wave's (max, sum, o) over its own region (the outlier terms were folded above)
   float(*red)[D + 2] = reinterpret_cast<float(*)[D + 2]>(&s_wave[wave][0]);
   if (lr < G) {
     // O^T row 4 lq + i of operand m: channel VPL (4 lq + i) + m; uniform 4-bit values use the
@@ -1182,18 +1145,18 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
 }
 
 template <int D, int G>
-hipError_t partial_impl(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st) {
+hipError_t partial_impl(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st, LaunchEv ev) {
   const float qscale = kLog2e / sqrtf((float)D);
   if (dv.n_tiles > 0)
-    hipLaunchKernelGGL((k_attn_partial_mx<D, G>), dim3(dv.n_tiles), dim3(kTileThreads), 0, st, dv.seqs,
-                       dv.state, dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale);
+    hipExtLaunchKernelGGL((k_attn_partial_mx<D, G>), dim3(dv.n_tiles), dim3(kTileThreads), 0, st, ev.start, ev.stop,
+                          0, dv.seqs, dv.state, dv.tiles, q, dv.partials, dv.cbtab, sh.Hkv, qscale);
   return hipGetLastError();
 }
 
 template <int D, int G>
-hipError_t combine_impl(const Dev &dv, const Shape &sh, float *out, hipStream_t st) {
-  hipLaunchKernelGGL((k_attn_combine<D, G>), dim3(sh.S * sh.Hkv), dim3(kCombineThreads), 0, st, dv.seqs, dv.state,
-                     dv.partials, out, sh.Hkv);
+hipError_t combine_impl(const Dev &dv, const Shape &sh, float *out, hipStream_t st, LaunchEv ev) {
+  hipExtLaunchKernelGGL((k_attn_combine<D, G>), dim3(sh.S * sh.Hkv), dim3(kCombineThreads), 0, st, ev.start,
+                        ev.stop, 0, dv.seqs, dv.state, dv.partials, out, sh.Hkv);
   return hipGetLastError();
 }
 
@@ -1212,12 +1175,13 @@ hipError_t combine_impl(const Dev &dv, const Shape &sh, float *out, hipStream_t 
     default: return hipErrorInvalidValue;                                     \
   }
 
-hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st) {
-  MKV_DISPATCH_DG(partial_impl, dv, sh, q, st)
+hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st,
+                                    LaunchEv ev) {
+  MKV_DISPATCH_DG(partial_impl, dv, sh, q, st, ev)
 }
 
-hipError_t launch_attention_combine(const Dev &dv, const Shape &sh, float *out, hipStream_t st) {
-  MKV_DISPATCH_DG(combine_impl, dv, sh, out, st)
+hipError_t launch_attention_combine(const Dev &dv, const Shape &sh, float *out, hipStream_t st, LaunchEv ev) {
+  MKV_DISPATCH_DG(combine_impl, dv, sh, out, st, ev)
 }
 
 }  // namespace mkv

@@ -661,9 +661,9 @@ __global__ __launch_bounds__(NT) void k_snap_keep(const SeqDesc *__restrict__ se
 
 template <int D, int G>
 hipError_t topk_impl(const Dev &dv, const Shape &sh, const uint16_t *q, int32_t *pos_out, int topk_max,
-                     hipStream_t st) {
-  hipLaunchKernelGGL((k_topk<D, G>), dim3(sh.S * sh.Hkv), dim3(kTopkThreads), 0, st, dv.seqs, dv.state, q, pos_out,
-                     topk_max, sh.Hkv);
+                     hipStream_t st, LaunchEv ev) {
+  hipExtLaunchKernelGGL((k_topk<D, G>), dim3(sh.S * sh.Hkv), dim3(kTopkThreads), 0, st, ev.start, ev.stop, 0,
+                        dv.seqs, dv.state, q, pos_out, topk_max, sh.Hkv);
   return hipGetLastError();
 }
 
@@ -696,16 +696,16 @@ hipError_t snap_prefill_impl(const Dev &dv, const Shape &sh, const SeqDesc &hs, 
 }  // namespace
 
 hipError_t launch_topk(const Dev &dv, const Shape &sh, const uint16_t *q, int32_t *pos_out, int topk_max,
-                       hipStream_t st) {
+                       hipStream_t st, LaunchEv ev) {
   switch (sh.D * 16 + sh.G) {
-    case 64 * 16 + 1: return topk_impl<64, 1>(dv, sh, q, pos_out, topk_max, st);
-    case 64 * 16 + 2: return topk_impl<64, 2>(dv, sh, q, pos_out, topk_max, st);
-    case 64 * 16 + 4: return topk_impl<64, 4>(dv, sh, q, pos_out, topk_max, st);
-    case 64 * 16 + 8: return topk_impl<64, 8>(dv, sh, q, pos_out, topk_max, st);
-    case 128 * 16 + 1: return topk_impl<128, 1>(dv, sh, q, pos_out, topk_max, st);
-    case 128 * 16 + 2: return topk_impl<128, 2>(dv, sh, q, pos_out, topk_max, st);
-    case 128 * 16 + 4: return topk_impl<128, 4>(dv, sh, q, pos_out, topk_max, st);
-    case 128 * 16 + 8: return topk_impl<128, 8>(dv, sh, q, pos_out, topk_max, st);
+    case 64 * 16 + 1: return topk_impl<64, 1>(dv, sh, q, pos_out, topk_max, st, ev);
+    case 64 * 16 + 2: return topk_impl<64, 2>(dv, sh, q, pos_out, topk_max, st, ev);
+    case 64 * 16 + 4: return topk_impl<64, 4>(dv, sh, q, pos_out, topk_max, st, ev);
+    case 64 * 16 + 8: return topk_impl<64, 8>(dv, sh, q, pos_out, topk_max, st, ev);
+    case 128 * 16 + 1: return topk_impl<128, 1>(dv, sh, q, pos_out, topk_max, st, ev);
+    case 128 * 16 + 2: return topk_impl<128, 2>(dv, sh, q, pos_out, topk_max, st, ev);
+    case 128 * 16 + 4: return topk_impl<128, 4>(dv, sh, q, pos_out, topk_max, st, ev);
+    case 128 * 16 + 8: return topk_impl<128, 8>(dv, sh, q, pos_out, topk_max, st, ev);
     default: return hipErrorInvalidValue;
   }
 }

@@ -141,7 +141,7 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
   };
   L->off_seqs = take(sizeof(SeqDesc) * S);
   L->off_state = take(sizeof(int32_t) * S * Hkv * ST_WORDS);
-  L->off_cbtab = take(sizeof(float) * kCbTableFloats);
+  L->off_cbtab = take(sizeof(float) * kCbRegionFloats);
   L->seqs.assign(S, SeqDesc{});
   int q_h2o = 0, q_rk = 0;
   for (int s = 0; s < S; ++s) {
@@ -183,6 +183,7 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
         d.krow = take(H * (d.cap + 1) * 4);
         d.kout = take(H * d.pool_cap * 4);
         d.vout = take(H * d.cap * d.nov_slots * 4);
+        d.vdel = take(H * d.cap * d.nov_slots * 4);
         break;
       }
       case H2O: {
@@ -292,12 +293,14 @@ struct mkv_cache {
 
 namespace {
 
-void prof_mark(mkv_cache *c, int kind, int which, hipStream_t st) {
-  if (!(c->prof_mask >> kind & 1)) return;
+// The timing events of the next launch of `kind` (none when that kind is not timed or its events
+// are used up); the launch itself records its kernel's start and end in them.
+LaunchEv prof_ev(mkv_cache *c, int kind) {
+  if (!(c->prof_mask >> kind & 1)) return {};
   const int i = c->prof_n[kind];
-  if (i >= c->prof_cap) return;
-  hipEventRecord(c->ev[kind][which][i], st);
-  if (which == 1) c->prof_n[kind] = i + 1;
+  if (i >= c->prof_cap) return {};
+  c->prof_n[kind] = i + 1;
+  return LaunchEv{c->ev[kind][0][i], c->ev[kind][1][i]};
 }
 
 mkv_status check_hip(hipError_t e, const char *what) {
@@ -347,7 +350,7 @@ mkv_status mkv_cache_create(const mkv_shape *shape, const mkv_config *cfg, const
     return fail(MKV_ENOMEM, "arena has %zu bytes, the cache needs %zu", arena_bytes, L.total);
   bool any_kvq = false;
   for (int s = 0; s < shape->n_seqs; ++s) any_kvq |= cfg[s].method == MKV_KVQ;
-  float table[kCbTableFloats] = {};
+  float table[kCbRegionFloats] = {};
   if (any_kvq) {
     if (!codebooks) return fail(MKV_EINVAL, "codebooks are required for KVQ sequences");
     const float *src = codebooks;
@@ -369,6 +372,24 @@ mkv_status mkv_cache_create(const mkv_shape *shape, const mkv_config *cfg, const
       }
       src += 2 * nc;
     }
+    // the attention's lookup tables: packed fp16 codebook values per quad (b = 2) or pair of codes
+    uint32_t *lut = reinterpret_cast<uint32_t *>(table + kLutBase);
+    auto hb = [](float x) { return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)x); };
+    for (int b = 2; b <= 4; ++b) {
+      const int nc = 1 << b, half = lut_half_words(b);
+      for (int which = 0; which < 2; ++which) {
+        const float *cb = table + cb_offset(b) + which * nc;
+        uint32_t *dst = lut + lut_offset(b) + which * half;
+        if (b == 2) {
+          for (int q = 0; q < 256; ++q) {
+            dst[2 * q] = hb(cb[q & 3]) | hb(cb[(q >> 2) & 3]) << 16;
+            dst[2 * q + 1] = hb(cb[(q >> 4) & 3]) | hb(cb[(q >> 6) & 3]) << 16;
+          }
+        } else {
+          for (int f = 0; f < half; ++f) dst[f] = hb(cb[f & (nc - 1)]) | hb(cb[f >> b]) << 16;
+        }
+      }
+    }
   }
   mkv_cache *c = new mkv_cache();
   c->sh = Shape{shape->n_seqs, shape->n_q_heads, shape->n_kv_heads, shape->head_dim,
@@ -379,7 +400,7 @@ mkv_status mkv_cache_create(const mkv_shape *shape, const mkv_config *cfg, const
   const uint64_t base = (uint64_t)(uintptr_t)arena;
   c->hs = L.seqs;
   for (auto &d : c->hs) {
-    uint64_t *ptrs[] = {&d.k, &d.v, &d.kc, &d.vc, &d.kmeta, &d.vmeta, &d.kres, &d.krow, &d.kout, &d.vout,
+    uint64_t *ptrs[] = {&d.k, &d.v, &d.kc, &d.vc, &d.kmeta, &d.vmeta, &d.kres, &d.krow, &d.kout, &d.vout, &d.vdel,
                         &d.pos, &d.score, &d.logits, &d.stage_k, &d.stage_v, &d.kcm, &d.sel, &d.akeys,
                         &d.aux0, &d.aux1};
     // offset 0 holds the descriptor table, so a zero offset marks a region the method lacks
@@ -438,9 +459,7 @@ mkv_status decode_append(mkv_cache *c, const uint16_t *k, const uint16_t *v, hip
     return fail(MKV_ESTATE, "decode append must follow prefill or a completed decode step");
   if (c->steps >= c->sh.max_new)
     return fail(MKV_ECAPACITY, "cache holds %d decode steps (max_new_tokens)", c->sh.max_new);
-  prof_mark(c, 2, 0, hst);
-  hipError_t e = launch_append_decode(c->dv, c->sh, k, v, hst);
-  prof_mark(c, 2, 1, hst);
+  hipError_t e = launch_append_decode(c->dv, c->sh, k, v, hst, prof_ev(c, 2));
   if (e != hipSuccess) return hip_fail(e, "decode append");
   c->evict_pending = false;
   c->steps++;
@@ -525,9 +544,7 @@ mkv_status mkv_topk_select(mkv_cache *c, const uint16_t *q, int32_t *pos_out, vo
   if (c->any_rocket) {
     if (!q) return fail(MKV_EINVAL, "q is NULL");
     hipStream_t hst = static_cast<hipStream_t>(stream);
-    prof_mark(c, 3, 0, hst);
-    const hipError_t e = launch_topk(c->dv, c->sh, q, pos_out, c->topk_max, hst);
-    prof_mark(c, 3, 1, hst);
+    const hipError_t e = launch_topk(c->dv, c->sh, q, pos_out, c->topk_max, hst, prof_ev(c, 3));
     if (e != hipSuccess) return hip_fail(e, "top-k select");
   }
   c->phase = PH_SELECTED;
@@ -541,13 +558,9 @@ mkv_status mkv_decode_attention(mkv_cache *c, const uint16_t *q, float *out, voi
     return fail(MKV_ESTATE, "attention must follow the decode append (and top-k selection)");
   hipStream_t hst = static_cast<hipStream_t>(stream);
   // one partial launch over the tiles of every sequence, then the combine
-  prof_mark(c, 0, 0, hst);
-  hipError_t e = launch_attention_partial(c->dv, c->sh, q, hst);
-  prof_mark(c, 0, 1, hst);
+  hipError_t e = launch_attention_partial(c->dv, c->sh, q, hst, prof_ev(c, 0));
   if (e != hipSuccess) return hip_fail(e, "attention partial");
-  prof_mark(c, 1, 0, hst);
-  e = launch_attention_combine(c->dv, c->sh, out, hst);
-  prof_mark(c, 1, 1, hst);
+  e = launch_attention_combine(c->dv, c->sh, out, hst, prof_ev(c, 1));
   if (e != hipSuccess) return hip_fail(e, "attention combine");
   c->phase = PH_ATTENDED;
   return MKV_OK;
@@ -569,13 +582,9 @@ mkv_status mkv_decode_attention_noalloc(mkv_cache *c, const uint16_t *q, float *
   Dev dv = c->dv;
   dv.partials = ws;
   hipStream_t hst = static_cast<hipStream_t>(stream);
-  prof_mark(c, 0, 0, hst);
-  e = launch_attention_partial(dv, c->sh, q, hst);
-  prof_mark(c, 0, 1, hst);
+  e = launch_attention_partial(dv, c->sh, q, hst, prof_ev(c, 0));
   if (e != hipSuccess) return hip_fail(e, "attention partial");
-  prof_mark(c, 1, 0, hst);
-  e = launch_attention_combine(dv, c->sh, out, hst);
-  prof_mark(c, 1, 1, hst);
+  e = launch_attention_combine(dv, c->sh, out, hst, prof_ev(c, 1));
   if (e != hipSuccess) return hip_fail(e, "attention combine");
   c->phase = PH_ATTENDED;
   return MKV_OK;

@@ -4,6 +4,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "mkv.h"
@@ -56,6 +57,7 @@ struct SeqDesc {
   uint64_t kmeta, vmeta;    // UQ: float2 [nblk][d], float2 [cap][d/64]; KVQ: float2 tau/inv [d], float [cap]
   uint64_t kres;            // UQ: fp16 [64][d] residual key block
   uint64_t krow, kout, vout;// KVQ: u32 [cap+1] CSR, u32 [pool_cap], u32 [nov_slots][cap]
+  uint64_t vdel;            // KVQ: u32 [nov_slots][cap] value-outlier differences for the attention
   uint64_t pos, score;      // H2O / ROCKET: int32 [cap], float [cap]
   uint64_t logits;          // H2O: float [cap][G] log2-domain logits of the last attention
   uint64_t stage_k, stage_v;// H2O / ROCKET: fp16 [n0][d] prompt staging
@@ -101,6 +103,24 @@ __host__ __device__ inline int cb_offset(int bits) {
 }
 constexpr int kCbTableFloats = 14 + 30 + 62;
 
+// Lookup tables of the KVQ codebooks for the attention, built on the host at cache creation and
+// stored after the codebook table (kLutBase floats into the same device region): for b = 2 one
+// entry per byte of four codes, the four codebook values as packed fp16 (2 words, 256 entries);
+// for b = 3 and 4 one entry per field of two codes, the two values as packed fp16 (2^(2b)
+// entries).  Per b, the key table then the value table; lut_offset and lut_half_words in words.
+constexpr int kLutBase = 112;
+__host__ __device__ inline int lut_half_words(int bits) { return bits == 2 ? 512 : 1 << (2 * bits); }
+__host__ __device__ inline int lut_offset(int bits) { return bits == 2 ? 0 : bits == 3 ? 1024 : 1152; }
+constexpr int kLutWords = 1024 + 128 + 512;
+constexpr int kCbRegionFloats = kLutBase + kLutWords;
+
+// A KVQ value outlier as the attention reads it: d = x - s cb[code] (x the fp16 outlier, s the
+// token's scale, cb[code] the codebook value its stored code stands for), float32 with the 7
+// lowest mantissa bits replaced by the channel; 0 marks an empty slot.
+__host__ __device__ inline uint32_t vdel_pack(float d, int ch) {
+  return (__builtin_bit_cast(uint32_t, d) & ~127u) | (uint32_t)ch;
+}
+
 // Host: x rounded once, to nearest even, to the nearest fp16 value (finite |x| < 65520).
 inline float round_to_half(double x) {
   if (x == 0.0 || !isfinite(x)) return (float)x;
@@ -122,19 +142,27 @@ struct Dev {
   int n_tiles_rk;        // the last n_tiles_rk tiles belong to RocketKV sequences
 };
 
+// Optional timing events of one launch: when set, they record the kernel's own start and end
+// (hipExtLaunchKernelGGL), with no marker packets of their own around the launch.
+struct LaunchEv {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+
 // H2O pairs whose last attention pass chose a victim (ST_VICTIM >= 0) write the token into its slot.
 hipError_t launch_append_decode(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
-                                hipStream_t st);
+                                hipStream_t st, LaunchEv ev = {});
 hipError_t launch_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
                               const uint16_t *k, const uint16_t *v, hipStream_t st);
-hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st);
+hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16_t *q, hipStream_t st,
+                                    LaunchEv ev = {});
 // The static split-K workspace of the current device (kStaticScratchBytes), its address looked up
 // on the first call per device.
 constexpr size_t kStaticScratchBytes = size_t(8) << 20;
 hipError_t static_scratch(float **ptr, size_t *bytes);
-hipError_t launch_attention_combine(const Dev &dv, const Shape &sh, float *out, hipStream_t st);
+hipError_t launch_attention_combine(const Dev &dv, const Shape &sh, float *out, hipStream_t st,
+                                    LaunchEv ev = {});
 hipError_t launch_topk(const Dev &dv, const Shape &sh, const uint16_t *q, int32_t *pos_out, int topk_max,
-                       hipStream_t st);
+                       hipStream_t st, LaunchEv ev = {});
 hipError_t launch_h2o_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
                                   const uint16_t *q_rows, hipStream_t st);
 hipError_t launch_snap_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
