@@ -75,6 +75,9 @@ typedef struct {
   int32_t pool;         /* ROCKET: odd max-pool kernel over votes (7) */
   int32_t topk;         /* ROCKET: tokens attended per decode step; 0 = keep_tokens/2 */
   int32_t n_channels;   /* ROCKET: query channels used for approximate scores (32) */
+  int32_t keep_ratio;   /* ROCKET: when > 0, SnapKV keeps max(floor(prompt_len / keep_ratio),
+                           window) tokens instead of keep_tokens (the paper's r-times
+                           compression settings, Section 2.1, RocketKV paragraph) */
 } mkv_config;
 
 typedef struct {
@@ -276,6 +279,50 @@ mkv_status mkv_fit_codebooks(const uint16_t *k, const uint16_t *v, int32_t n_tok
  */
 mkv_status mkv_profile_enable(mkv_cache *cache, int32_t enable, int32_t max_launches);
 mkv_status mkv_profile_read(mkv_cache *cache, int32_t kind, int32_t *launches, double *total_ms);
+
+/*
+ * KV-cache memory of one sequence under one configuration (the paper's peak KV
+ * memory metric, Table 1; Section 2.2 compares the methods by it), in this
+ * library's storage format, host only: `resident` = bytes of the cache state
+ * holding the tokens the method keeps after prompt_len prompt tokens and
+ * n_generated decode steps (codes, fp16 rows, scales, outliers, per-slot
+ * positions and scores; capacity reserved for later tokens and the per-step
+ * attention workspace excluded); `peak` = the largest such state from prefill
+ * to that step, where H2O and RocketKV hold the whole fp16 prompt before their
+ * prefill eviction.  KVQ key outliers of decode tokens are counted at their
+ * expected rate (outlier_bp), those of the prompt at their bound (the n_o-th
+ * order statistic per channel).  shape->n_seqs and max_new_tokens are ignored.
+ */
+mkv_status mkv_kv_memory(const mkv_shape *shape, const mkv_config *cfg, int32_t prompt_len,
+                         int32_t n_generated, size_t *resident, size_t *peak);
+
+/*
+ * MetaKV's per-prompt choice among candidate configurations (Section 2.3,
+ * Steps 3-7, and the violation score v_c), host only.  Each candidate carries
+ * its method, its compression level within the method (0 = least compressed,
+ * e.g. KVQuant 4 bits, H2O 60 %, RocketKV 8x), and the predicted end-to-end
+ * latency, peak memory and probability of a correct response for the prompt.
+ *   1. Budget filter: keep the candidates with latency <= l_max and
+ *      memory <= m_max.
+ *   2. If FP16 (method MKV_FP16) is kept, choose it.
+ *   3. Otherwise keep only the least compressed kept setting of each method;
+ *      if one candidate remains choose it, else the highest p_correct.
+ *   4. If no candidate passes the filter, choose the smallest
+ *      v_c = latency / l_max + memory / m_max, the higher p_correct breaking
+ *      a tie; *violated is then 1 (else 0).
+ * Remaining ties go to the lower index.  *chosen is an index into cands.
+ * MKV_EINVAL for n < 1, a NULL pointer or a non-positive budget.
+ */
+typedef struct {
+  int32_t method;    /* mkv_method */
+  int32_t level;     /* compression level within the method, 0 = least compressed */
+  double latency;    /* predicted end-to-end latency (the unit of l_max) */
+  double memory;     /* predicted peak memory (the unit of m_max) */
+  double p_correct;  /* predicted probability of a correct response */
+} mkv_candidate;
+
+mkv_status mkv_select_config(const mkv_candidate *cands, int32_t n, double l_max, double m_max,
+                             int32_t *chosen, int32_t *violated);
 
 /*
  * Workgroups of the attention partial launch per decode step: `n_tiles` in

@@ -54,7 +54,7 @@ class Sequence:
                 self.adopt_h2o_prefill([h2o.prefill_keep(self.S[h], self.B, self.R)
                                         for h in range(self.hkv)])
         elif m == "rocket":
-            self.T = int(cfg["keep_tokens"])
+            self.T = snapkv.keep_budget(cfg, self.n0)
             self.w = int(cfg.get("window", 32))
             self.pool = int(cfg.get("pool", 7))
             self.nc = int(cfg.get("n_channels", 32))

@@ -49,6 +49,17 @@ def max_pool(v, kernel):
     return np.array([v[max(0, j - h):min(n, j + h + 1)].max() for j in range(n)]) if n else v
 
 
+def keep_budget(cfg, n0):
+    """Tokens SnapKV keeps for a configuration row: `keep_tokens`, or for the paper's r-times
+    settings (`keep_ratio` = r > 0) floor(n0 / r), but never fewer than the window rows, which
+    are always kept (reading of Section 2.1, RocketKV paragraph: the ratio compresses the
+    prompt's cache)."""
+    r = int(cfg.get("keep_ratio", 0))
+    if r > 0:
+        return max(int(n0) // r, int(cfg.get("window", 32)))
+    return int(cfg["keep_tokens"])
+
+
 def snap_keep(q_window, k_prompt, keep_tokens, window=32, pool=7):
     """Positions kept by SnapKV (ascending) for one (sequence, kv head)."""
     n0 = np.asarray(k_prompt).shape[0]

@@ -22,7 +22,13 @@ PROFILE_KINDS = {"partial": 0, "combine": 1, "append": 2, "topk": 3}
 
 class mkv_config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("method", "bits", "group", "outlier_bp", "budget_pct",
-                                              "keep_tokens", "window", "pool", "topk", "n_channels")]
+                                              "keep_tokens", "window", "pool", "topk", "n_channels",
+                                              "keep_ratio")]
+
+
+class mkv_candidate(ctypes.Structure):
+    _fields_ = [("method", ctypes.c_int32), ("level", ctypes.c_int32), ("latency", ctypes.c_double),
+                ("memory", ctypes.c_double), ("p_correct", ctypes.c_double)]
 
 
 class mkv_shape(ctypes.Structure):
@@ -61,6 +67,10 @@ _SIGS = {
     "mkv_profile_enable": (_I, [_P, _I, _I]),
     "mkv_profile_read": (_I, [_P, _I, ctypes.POINTER(_I), ctypes.POINTER(ctypes.c_double)]),
     "mkv_attention_tiles": (_I, [_P, ctypes.POINTER(_I), ctypes.POINTER(_I), ctypes.POINTER(_I)]),
+    "mkv_select_config": (_I, [ctypes.POINTER(mkv_candidate), _I, ctypes.c_double, ctypes.c_double,
+                               ctypes.POINTER(_I), ctypes.POINTER(_I)]),
+    "mkv_kv_memory": (_I, [ctypes.POINTER(mkv_shape), ctypes.POINTER(mkv_config), _I, _I,
+                           ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t)]),
     "mkv_probe_read_bandwidth": (_I, [_P, ctypes.c_size_t, _P, _I, ctypes.POINTER(ctypes.c_double), _P]),
 }
 SYMBOLS = tuple(_SIGS)
@@ -100,6 +110,7 @@ def make_config(row):
     c.pool = int(row.get("pool", 0))
     c.topk = int(row.get("topk", 0))
     c.n_channels = int(row.get("n_channels", 0))
+    c.keep_ratio = int(row.get("keep_ratio", 0))
     return c
 
 
@@ -199,6 +210,26 @@ def mkv_probe_read_bandwidth(buf_ptr, nbytes, sink_ptr, reps, stream=0):
     g = ctypes.c_double()
     _check(lib().mkv_probe_read_bandwidth(buf_ptr, nbytes, sink_ptr, reps, ctypes.byref(g), stream))
     return g.value
+
+
+def mkv_kv_memory(shape, cfg, prompt_len, n_generated):
+    """-> (resident, peak) KV-cache bytes of one sequence (host only)."""
+    sh = mkv_shape(*[int(x) for x in shape])
+    c = make_config(cfg)
+    a, b = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib().mkv_kv_memory(ctypes.byref(sh), ctypes.byref(c), int(prompt_len), int(n_generated),
+                               ctypes.byref(a), ctypes.byref(b)))
+    return a.value, b.value
+
+
+def mkv_select_config(cands, l_max, m_max):
+    """cands: sequence of (method name, level, latency, memory, p_correct).
+    -> (chosen index, violated flag)."""
+    arr = (mkv_candidate * len(cands))(*[mkv_candidate(METHODS[m], int(lv), float(l), float(mem), float(p))
+                                         for m, lv, l, mem, p in cands])
+    ch, vi = _I(), _I()
+    _check(lib().mkv_select_config(arr, len(cands), float(l_max), float(m_max), ctypes.byref(ch), ctypes.byref(vi)))
+    return ch.value, bool(vi.value)
 
 
 def mkv_attention_tiles(h):

@@ -13,7 +13,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmkv.so")
 
-SOURCES = ["mkv_api.cpp", "calib.cpp", "k_attn.hip", "k_append.hip", "k_select.hip", "k_probe.hip"]
+SOURCES = ["mkv_api.cpp", "calib.cpp", "select.cpp", "k_attn.hip", "k_append.hip", "k_select.hip", "k_probe.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

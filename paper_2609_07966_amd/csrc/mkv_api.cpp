@@ -92,6 +92,11 @@ mkv_status check_shape(const mkv_shape *sh) {
   return MKV_OK;
 }
 
+// RocketKV's SnapKV budget: keep_tokens, or in ratio mode max(floor(n0 / keep_ratio), window).
+int rocket_keep(const mkv_config &c, int n0) {
+  return c.keep_ratio > 0 ? std::max(n0 / c.keep_ratio, c.window) : c.keep_tokens;
+}
+
 mkv_status check_config(const mkv_config &c, int n0, int D, int s) {
   if (n0 < 1) return fail(MKV_EINVAL, "seq %d: prompt_len must be >= 1", s);
   switch (c.method) {
@@ -113,11 +118,12 @@ mkv_status check_config(const mkv_config &c, int n0, int D, int s) {
     }
     case MKV_ROCKET:
       if (c.window < 1) return fail(MKV_EINVAL, "seq %d: window must be >= 1", s);
-      if (c.keep_tokens < c.window) return fail(MKV_EINVAL, "seq %d: keep_tokens must be >= window", s);
+      if (c.keep_ratio < 0) return fail(MKV_EINVAL, "seq %d: keep_ratio must be >= 0", s);
+      if (c.keep_ratio == 0 && c.keep_tokens < c.window) return fail(MKV_EINVAL, "seq %d: keep_tokens must be >= window", s);
       if (c.pool < 1 || (c.pool & 1) == 0) return fail(MKV_EINVAL, "seq %d: pool must be odd and >= 1", s);
       if (c.n_channels < 1 || c.n_channels > D) return fail(MKV_EINVAL, "seq %d: n_channels in 1..head_dim", s);
       if (c.topk < 0) return fail(MKV_EINVAL, "seq %d: topk must be >= 0", s);
-      if (c.topk == 0 && c.keep_tokens / 2 < 1) return fail(MKV_EINVAL, "seq %d: keep_tokens/2 is 0", s);
+      if (c.topk == 0 && rocket_keep(c, n0) / 2 < 1) return fail(MKV_EINVAL, "seq %d: the keep budget / 2 is 0", s);
       return MKV_OK;
     default:
       return fail(MKV_EINVAL, "seq %d: unknown method %d", s, c.method);
@@ -204,12 +210,12 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
         break;
       }
       case ROCKET: {
-        d.T = c.keep_tokens;
+        d.T = rocket_keep(c, n0);
         d.window = c.window;
         d.w_eff = std::min(c.window, n0);
         d.pool = c.pool;
         d.nch = c.n_channels;
-        d.topk = c.topk > 0 ? c.topk : c.keep_tokens / 2;
+        d.topk = c.topk > 0 ? c.topk : d.T / 2;
         const int kept = std::min(d.T, n0);
         d.cap = kept + mn;
         const int nchunk = (n0 + 255) / 256;
@@ -606,6 +612,59 @@ mkv_status mkv_decode_step(mkv_cache *c, const uint16_t *k, const uint16_t *v, c
   if ((st = mkv_topk_select(c, q, nullptr, stream)) != MKV_OK) return st;
   if ((st = mkv_decode_attention(c, q, out, stream)) != MKV_OK) return st;
   return mkv_h2o_update_evict(c, nullptr, stream);
+}
+
+mkv_status mkv_kv_memory(const mkv_shape *shape, const mkv_config *cfg, int32_t prompt_len, int32_t n_generated,
+                         size_t *resident, size_t *peak) {
+  mkv_status st = check_shape(shape);
+  if (st != MKV_OK) return st;
+  if (!cfg || !resident || !peak) return fail(MKV_EINVAL, "cfg, resident and peak must be non-NULL");
+  if (n_generated < 0) return fail(MKV_EINVAL, "n_generated must be >= 0");
+  const int D = shape->head_dim, G = shape->n_q_heads / shape->n_kv_heads;
+  if ((st = check_config(*cfg, prompt_len, D, 0)) != MKV_OK) return st;
+  const long long n0 = prompt_len, gen = n_generated, n = n0 + gen, row = 4LL * D;  // K and V fp16 rows
+  long long now = 0, top = 0;
+  switch (cfg->method) {
+    case MKV_FP16:
+      now = top = n * row;
+      break;
+    case MKV_UQ: {
+      const long long nb = n / 64;  // complete key blocks are codes, the rest fp16
+      const long long k = nb * 64 * (D / 2) + nb * D * 8 + (n - nb * 64) * 2 * D;
+      const long long v = n * (D / 2) + n * (D / 64) * 8;
+      now = top = k + v;
+      break;
+    }
+    case MKV_KVQ: {
+      const long long bp = cfg->outlier_bp, codes = 2 * n * D * cfg->bits / 8;
+      const long long n_o = (n0 * bp + 5000) / 10000, n_ov = ((long long)D * bp + 5000) / 10000;
+      const long long slots = bp > 0 ? std::max(1LL, n_ov) : 1;
+      // key outliers: at most n_o per channel over the prompt; decode tokens at their expected rate
+      const long long kout = std::min(n_o, n0) * D + (gen * D * bp + 5000) / 10000;
+      now = top = codes + D * 8 + n * 4 + (n + 1) * 4 + kout * 4 + n * slots * 8;
+      break;
+    }
+    case MKV_H2O: {
+      const long long B = (long long)cfg->budget_pct * n0 / 100, kept = std::min(B, n0);
+      const long long slot = row + 8 + 4LL * G;  // rows, position, score, last logits
+      now = std::min(B, kept + gen) * slot;
+      // prefill: the whole prompt in fp16 with its scores, beside the kept slots; decode: B + 1
+      const long long pre = n0 * row + n0 * 4 + kept * slot;
+      top = std::max(pre, (gen > 0 ? std::min(B + 1, kept + gen) : kept) * slot);
+      break;
+    }
+    case MKV_ROCKET: {
+      const long long T = rocket_keep(*cfg, prompt_len), kept = std::min(T, n0);
+      const long long topk = cfg->topk > 0 ? cfg->topk : T / 2;
+      const long long slot = row + 2LL * D + 8;  // rows, channel-major key copy, position, score key
+      now = (kept + gen) * slot + topk * 4;
+      top = std::max(n0 * row + kept * slot, now);  // prefill: the whole prompt in fp16 before SnapKV
+      break;
+    }
+  }
+  *resident = (size_t)(now * shape->n_kv_heads);
+  *peak = (size_t)(top * shape->n_kv_heads);
+  return MKV_OK;
 }
 
 mkv_status mkv_attention_tiles(mkv_cache *c, int32_t *n_tiles, int32_t *n_tiles_uq, int32_t *n_tiles_rocket) {

@@ -187,7 +187,7 @@ def _oracle_rocket(run, s, t, q, gout, keeps, topk):
     K, V = run.tokens(s, t)
     n0 = run.prompts[s][0].shape[0]
     G, worst = wl.group, 0.0
-    T = int(c["keep_tokens"])
+    T = snapkv.keep_budget(c, n0)
     k = rocketkv.default_topk(T, c.get("topk", 0))
     for h in range(wl.n_kv_heads):
         rows = np.concatenate([keeps[h], np.arange(n0, K.shape[0])])
@@ -208,7 +208,7 @@ def _rocket_keeps(run, s):
     wl, c = run.wl, run.cfgs[s]
     kp = run.prompts[s][0]
     n0, G = kp.shape[0], wl.group
-    T, w, pool = int(c["keep_tokens"]), int(c.get("window", 32)), int(c.get("pool", 7))
+    T, w, pool = snapkv.keep_budget(c, n0), int(c.get("window", 32)), int(c.get("pool", 7))
     qw = prompt_q(wl, s, last=w)
     keeps = []
     for h in range(wl.n_kv_heads):

@@ -149,6 +149,17 @@ def test_tiny_prompts_quantized():
     _run(wl, 9)
 
 
+def test_paper_grid_settings():
+    # the paper's own settings (Table 1) beyond the benchmark grid: H2O at 40 % and 60 % of the
+    # prompt, and RocketKV at 8x, 16x and 32x compression of each prompt (keep prompt_len / r
+    # tokens, at least the window); lock step against the oracle
+    wl = make_workload("custom", seed=17, n_seqs=5, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                       prompt_lens=[900, 1300, 3000, 2500, 4100], steps=6,
+                       config_ids=["H2O-40", "H2O-60", "Rocket-8x", "Rocket-16x", "Rocket-32x"],
+                       boost_frac=0.05, boost=3.0)
+    _run(wl, 6)
+
+
 @pytest.mark.parametrize("hq,n0", [(4, 13001), (8, 7001)])
 def test_h2o_large_retained_sets(hq, n0):
     # H2O-50 with one kv head of d = 64: B = 6500 (G = 4) and 3500 (G = 8) retained slots, more

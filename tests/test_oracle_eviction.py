@@ -299,3 +299,21 @@ def test_uq_sixteen_bits_tracks_dense():
         a, _ = dense.step(kn[0], vn[0], q[0])
         b, _ = uq.step(kn[0], vn[0], q[0])
         np.testing.assert_allclose(a, b, atol=2e-3)
+
+
+def test_rocket_ratio_budget_is_prompt_over_r():
+    """The paper's r-times RocketKV settings keep floor(prompt_len / r) tokens (never fewer than
+    the window): at a 32768-token prompt, 8x, 16x and 32x are the 4096-, 2048- and 1024-token
+    budgets, and the keep-set equals the absolute-budget keep-set."""
+    from workloads import config
+    for r, T in ((8, 4096), (16, 2048), (32, 1024)):
+        assert snapkv.keep_budget(config(f"Rocket-{r}x"), 32768) == T
+        assert snapkv.keep_budget(config(f"Rocket-{T}"), 32768) == T
+    assert snapkv.keep_budget(config("Rocket-32x"), 500) == 32      # 15 < window
+    rng = np.random.default_rng(3)
+    n0, G, d = 700, 2, 16
+    q = rng.standard_normal((32, G, d)).astype(np.float16)
+    k = rng.standard_normal((n0, d)).astype(np.float16)
+    a = snapkv.snap_keep(q, k, snapkv.keep_budget(config("Rocket-8x"), n0), 32, 7)
+    b = snapkv.snap_keep(q, k, n0 // 8, 32, 7)
+    assert np.array_equal(a, b) and len(a) == n0 // 8

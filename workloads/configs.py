@@ -14,6 +14,15 @@ here.  IDs follow one fixed order:
                          SnapKV prefill eviction to T tokens, then top-(T/2)
                          sparse decode attention (Section 2.1, RocketKV
                          paragraph)
+
+The paper's own settings (Section 2.1, Table 1) add:
+
+  11,12  H2O-40/60       heavy-hitter eviction at 40 % and 60 % of the prompt
+  13,14,15 Rocket-8x/16x/32x
+                         SnapKV keeping prompt_len / r tokens (r = 8, 16, 32),
+                         then top-(T/2) sparse decode attention
+
+PAPER_GRID lists the paper's ten configurations (Table 1) by name.
 """
 
 CONFIGS = [
@@ -31,7 +40,18 @@ CONFIGS = [
      "window": 32, "pool": 7, "topk": 0, "n_channels": 32},
     {"id": 10, "name": "Rocket-4096", "method": "rocket", "keep_tokens": 4096,
      "window": 32, "pool": 7, "topk": 0, "n_channels": 32},
+    {"id": 11, "name": "H2O-40", "method": "h2o", "budget_pct": 40},
+    {"id": 12, "name": "H2O-60", "method": "h2o", "budget_pct": 60},
+    {"id": 13, "name": "Rocket-8x", "method": "rocket", "keep_ratio": 8, "keep_tokens": 0,
+     "window": 32, "pool": 7, "topk": 0, "n_channels": 32},
+    {"id": 14, "name": "Rocket-16x", "method": "rocket", "keep_ratio": 16, "keep_tokens": 0,
+     "window": 32, "pool": 7, "topk": 0, "n_channels": 32},
+    {"id": 15, "name": "Rocket-32x", "method": "rocket", "keep_ratio": 32, "keep_tokens": 0,
+     "window": 32, "pool": 7, "topk": 0, "n_channels": 32},
 ]
+
+PAPER_GRID = ["FP16", "KVQ4", "KVQ3", "KVQ2", "H2O-60", "H2O-40", "H2O-20", "Rocket-8x",
+              "Rocket-16x", "Rocket-32x"]
 
 BY_NAME = {c["name"]: c for c in CONFIGS}
 
