@@ -204,12 +204,22 @@ def run_gpu(wl, steps, warmup, replicas=1, label="", prof_steps=24, graph_steps=
                 q = np.concatenate([np.zeros((w - q.shape[0],) + q.shape[1:], np.float16), q])
             qw.append(q)
     q_win = torch.from_numpy(np.concatenate(qw)).to(dev) if qw else None
-    for c in caches:
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    prefill_ms = {}
+    for i, c in enumerate(caches):
+        ev[0].record(stream)
         c.append_prompt(k_all, v_all)
+        ev[1].record(stream)
         if q_h2o is not None:
             c.h2o_prefill(q_h2o)
+        ev[2].record(stream)
         if q_win is not None:
             c.snap_prefill(q_win)
+        ev[3].record(stream)
+        if i == 0:  # the first replica's prefill stages, timed on the cache's stream
+            torch.cuda.synchronize()
+            prefill_ms = {"append": ev[0].elapsed_time(ev[1]), "h2o_scoring": ev[1].elapsed_time(ev[2]),
+                          "snapkv": ev[2].elapsed_time(ev[3])}
     torch.cuda.synchronize()
     del k_all, v_all, q_h2o, q_win
     t_prefill = time.time() - t0
@@ -283,7 +293,7 @@ def run_gpu(wl, steps, warmup, replicas=1, label="", prof_steps=24, graph_steps=
         "step_gbs": avg_bytes / (elapsed / steps) / 1e9,
         "n_tiles": n_tiles, "n_tiles_uq": n_uq, "n_tiles_rocket": n_rk, "replicas": replicas,
         "kernel_ms": {k: (v[1] / max(v[0], 1)) for k, v in kinds.items() if v[0]},
-        "graph_ms_per_step": graph_ms, "graph_steps": graph_steps,
+        "graph_ms_per_step": graph_ms, "graph_steps": graph_steps, "prefill_ms": prefill_ms,
     }
     for c in caches:
         c.close()
@@ -312,7 +322,8 @@ def per_config_runs(args):
                      "attn_partial_GBs": round(r["partial_gbs"], 1),
                      "attn_partial_frac_of_peak": round(r["partial_gbs"] / PEAK_HBM_GBS, 4),
                      "step_GBs": round(r["step_gbs"], 1), "replicas": reps,
-                     "bytes_per_step_MB": round(r["partial_bytes"] / 1e6, 2)})
+                     "bytes_per_step_MB": round(r["partial_bytes"] / 1e6, 2),
+                     "prefill_ms": {k: round(v, 3) for k, v in r["prefill_ms"].items() if v > 0.01}})
         log(f"[bench] {name}/{cfg}: {json.dumps(runs[-1])}")
     return runs
 
@@ -511,6 +522,7 @@ def main():
         "read_ceiling_GBs": None if ceiling is None else round(ceiling, 1),
         "attention_frac_of_read_ceiling": None if ceiling is None else round(head["partial_gbs"] / ceiling, 4),
         "kernel_us": {k: round(v * 1e3, 2) for k, v in head["kernel_ms"].items()},
+        "prefill_ms": {k: round(v, 3) for k, v in head["prefill_ms"].items()},
         "graph_replay": {"ms_per_step": (round(head["graph_ms_per_step"], 4)
                                          if head["graph_ms_per_step"] is not None else None),
                          "steps": head["graph_steps"],

@@ -297,143 +297,201 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(const SeqDesc *__restrict
   if (threadIdx.x == 0) st[ST_SEL_COUNT] = k;
 }
 
-// ---- causal prefill attention statistics (shared by H2O scoring) ---------------------------------
-// Tiles of 64 query rows x 64 keys; 256 threads as 16 x 16, each owning 4 rows x 4 keys.
+// ---- causal prefill attention statistics for H2O scoring, on the matrix cores ------------------
+// Logit tiles S = Q K^T of 16 query rows x 16 keys come from v_mfma_f32_16x16x32_f16: Q and K are
+// fp16 exactly, products exact, sums in float32.  Operand lane roles (lr = lane % 16, lq = lane /
+// 16): A (16 rows x 32 channels) row lr, channels 8 lq .. 8 lq + 7 of the k-step; B (32 channels x
+// 16 keys) key lr, the same channels; result rows 4 lq + j (j = 0..3), key lr.
 constexpr int TB = 64;
 
-template <int D>
-MKV_DEV void load_tile_f32(float (*dst)[D + 1], const uint16_t *src, int64_t row_stride, int r0, int nrows) {
-  for (int e = threadIdx.x; e < TB * D; e += NT) {
-    const int r = e / D, c = e % D;
-    dst[r][c] = (r0 + r < nrows) ? h2f(src[(int64_t)(r0 + r) * row_stride + c]) : 0.f;
-  }
+typedef _Float16 h8v __attribute__((ext_vector_type(8)));
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+MKV_DEV f4v mfma_k32(const uint4 &a, const uint4 &b, f4v c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8v, a), __builtin_bit_cast(h8v, b), c, 0, 0, 0);
 }
 
-// Row statistics (max, sum of exp2) of the causal logits of query head gq over all prompt keys.
+// Sum and max over the 16 lanes of a row (lanes with the same lq).
+MKV_DEV float row16_max(float x) {
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) x = fmaxf(x, __shfl_xor(x, o));
+  return x;
+}
+MKV_DEV float row16_sum(float x) {
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+// Row statistics (max, sum of exp2) of query head gq's causal logits over the prompt keys: a
+// workgroup takes 64 query rows (16 per wave, their Q operands in registers) and walks the
+// 64-key tiles up to the diagonal, each staged once in LDS for the four waves.  Every lane keeps
+// a running (max, sum) for its 4 rows over the keys of its column, merged across the row's 16
+// lanes at the end.
 template <int D>
 __global__ __launch_bounds__(NT) void k_h2o_rowstats(const SeqDesc *__restrict__ seqs, int seq,
                                                      const uint16_t *__restrict__ qrows, int Hq, int G,
                                                      float scale2) {
-  __shared__ float sq[TB][D + 1];
-  __shared__ float sk[TB][D + 1];
+  constexpr int KS = D / 32, U = D / 8;  // k-steps; 16-byte units per row
+  __shared__ uint4 sk[TB][U + 1];
   const SeqDesc &sd = seqs[seq];
   const int n0 = sd.n0;
   const int rb = blockIdx.x, gq = blockIdx.y, h = gq / G, g = gq % G;
-  const int ty = threadIdx.x / 16, tx = threadIdx.x % 16;
-  const int i0 = rb * TB;
-  load_tile_f32<D>(sq, qrows + (size_t)gq * D, (int64_t)Hq * D, i0, n0);
-  const uint16_t *ks = reinterpret_cast<const uint16_t *>(sd.stage_k) + h * stride_stage(sd, D);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, lr = lane & 15, lq = lane >> 4;
+  const int r0 = rb * TB + 16 * wave;  // this wave's first row
+  uint4 qa[KS];
+  {
+    const uint4 *qp = reinterpret_cast<const uint4 *>(qrows + (size_t)min(r0 + lr, n0 - 1) * Hq * D + (size_t)gq * D);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) qa[s] = gld16(qp + 4 * s + lq);
+  }
+  const uint4 *ks = reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(sd.stage_k) +
+                                                    h * stride_stage(sd, D));
   float m[4], l[4];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) { m[r] = -INFINITY; l[r] = 0.f; }
+  for (int j = 0; j < 4; ++j) {
+    m[j] = -INFINITY;
+    l[j] = 0.f;
+  }
+  // the next tile's loads are in flight while the current one is computed
+  constexpr int PER = TB * U / NT;  // 16-byte units per thread and tile
+  uint4 nxt[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int e = threadIdx.x + k * NT, r = e / U, u = e % U;
+    nxt[k] = gld16(ks + (size_t)min(r, n0 - 1) * U + u);
+  }
   for (int kb = 0; kb <= rb; ++kb) {
     __syncthreads();
-    load_tile_f32<D>(sk, ks, D, kb * TB, n0);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int e = threadIdx.x + k * NT;
+      sk[e / U][e % U] = nxt[k];
+    }
     __syncthreads();
-    float s[4][4] = {};
-    for (int c = 0; c < D; ++c) {
-      float qv[4], kv[4];
+    if (kb < rb) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) qv[r] = sq[ty * 4 + r][c];
+      for (int k = 0; k < PER; ++k) {
+        const int e = threadIdx.x + k * NT, r = e / U, u = e % U;
+        nxt[k] = gld16(ks + (size_t)min((kb + 1) * TB + r, n0 - 1) * U + u);
+      }
+    }
+    if (kb * TB > r0 + 15) continue;  // the tile lies wholly above this wave's rows
+    float v[4][4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) kv[j] = sk[tx * 4 + j][c];
+    for (int n = 0; n < 4; ++n) {
+      f4v S = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
+      for (int s = 0; s < KS; ++s) S = mfma_k32(qa[s], sk[16 * n + lr][4 * s + lq], S);
+      const int key = kb * TB + 16 * n + lr;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) s[r][j] = fmaf(qv[r], kv[j], s[r][j]);
+      for (int j = 0; j < 4; ++j) v[n][j] = (key <= r0 + 4 * lq + j && key < n0) ? S[j] * scale2 : -INFINITY;
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int i = i0 + ty * 4 + r;
-      float mx = m[r];
+    for (int j = 0; j < 4; ++j) {
+      const float mx = fmaxf(fmaxf(m[j], fmaxf(v[0][j], v[1][j])), fmaxf(v[2][j], v[3][j]));
+      if (mx == -INFINITY) continue;
+      float acc = l[j] * fexp2(m[j] - mx);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int jj = kb * TB + tx * 4 + j;
-        s[r][j] = (jj <= i && jj < n0) ? s[r][j] * scale2 : -INFINITY;
-        mx = fmaxf(mx, s[r][j]);
-      }
-      if (mx != -INFINITY) {
-        float acc = l[r] * exp2f(m[r] - mx);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc += exp2f(s[r][j] - mx);
-        l[r] = acc;
-        m[r] = mx;
-      }
+      for (int n = 0; n < 4; ++n) acc += fexp2(v[n][j] - mx);
+      l[j] = acc;
+      m[j] = mx;
     }
   }
-  // merge the 16 threads of each row (consecutive lanes)
+  float2 *out = reinterpret_cast<float2 *>(sd.aux1) + (size_t)h * G * n0 + (size_t)g * n0;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    float M = m[r];
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) M = fmaxf(M, __shfl_xor(M, o));
-    float L = (m[r] == -INFINITY) ? 0.f : l[r] * exp2f(m[r] - M);
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) L += __shfl_xor(L, o);
-    const int i = i0 + ty * 4 + r;
-    if (tx == 0 && i < n0)
-      (reinterpret_cast<float2 *>(sd.aux1) + (size_t)h * G * n0)[(size_t)g * n0 + i] = make_float2(M, L);
+  for (int j = 0; j < 4; ++j) {
+    const float M = row16_max(m[j]);
+    const float L = row16_sum(m[j] == -INFINITY ? 0.f : l[j] * fexp2(m[j] - M));
+    const int i = r0 + 4 * lq + j;
+    if (lr == 0 && i < n0) out[i] = make_float2(M, L);
   }
 }
 
-// Column sums S_j = sum_g sum_{i >= j} p_gij over a 64-key block.
+// Column sums S_j = sum_g sum_{i >= j} p_gij over a block of 64 keys: every wave holds the
+// block's K operands in registers and takes every fourth 16-row chunk of the rows at or below
+// the block, for each of the kv head's query heads; the waves' sums meet in LDS.
 template <int D>
 __global__ __launch_bounds__(NT) void k_h2o_colsums(const SeqDesc *__restrict__ seqs, int seq,
                                                     const uint16_t *__restrict__ qrows, int Hq, int G,
                                                     float scale2) {
-  __shared__ float sq[TB][D + 1];
-  __shared__ float sk[TB][D + 1];
-  __shared__ float2 sstat[TB];
-  __shared__ float scol[16][TB];
+  constexpr int KS = D / 32, U = D / 8;
+  __shared__ float scol[NT / 64][TB];
   const SeqDesc &sd = seqs[seq];
   const int n0 = sd.n0;
   const int kb = blockIdx.x, h = blockIdx.y;
-  const int ty = threadIdx.x / 16, tx = threadIdx.x % 16;
-  const uint16_t *ks = reinterpret_cast<const uint16_t *>(sd.stage_k) + h * stride_stage(sd, D);
-  load_tile_f32<D>(sk, ks, D, kb * TB, n0);
-  const int nrb = (n0 + TB - 1) / TB;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, lr = lane & 15, lq = lane >> 4;
+  const uint4 *ks = reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(sd.stage_k) +
+                                                    h * stride_stage(sd, D));
+  uint4 kop[4][KS];
+#pragma unroll
+  for (int n = 0; n < 4; ++n)
+#pragma unroll
+    for (int s = 0; s < KS; ++s) kop[n][s] = gld16(ks + (size_t)min(kb * TB + 16 * n + lr, n0 - 1) * U + 4 * s + lq);
   const float2 *stat = reinterpret_cast<const float2 *>(sd.aux1) + (size_t)h * G * n0;
   float col[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int g = 0; g < G; ++g) {
-    const int gq = h * G + g;
-    for (int rb = kb; rb < nrb; ++rb) {
-      __syncthreads();
-      load_tile_f32<D>(sq, qrows + (size_t)gq * D, (int64_t)Hq * D, rb * TB, n0);
-      for (int r = threadIdx.x; r < TB; r += NT) {
-        const int i = rb * TB + r;
-        sstat[r] = i < n0 ? stat[(size_t)g * n0 + i] : make_float2(0.f, 1.f);
-      }
-      __syncthreads();
-      float s[4][4] = {};
-      for (int c = 0; c < D; ++c) {
-        float qv[4], kv[4];
+  const int nchunk = (n0 + 15) / 16;
+  // (query head, 16-row chunk) items of this wave in order, the next item's loads in flight while
+  // the current one is computed
+  const int c0 = kb * (TB / 16) + wave, per_g = c0 < nchunk ? (nchunk - c0 + NT / 64 - 1) / (NT / 64) : 0;
+  const int items = G * per_g;
+  auto load = [&](int it, uint4 (&qa)[KS], float (&M)[4], float (&iL)[4]) {
+    const int g = it / per_g, c = c0 + (it % per_g) * (NT / 64);
+    const uint4 *qp = reinterpret_cast<const uint4 *>(qrows + (size_t)min(16 * c + lr, n0 - 1) * Hq * D +
+                                                      (size_t)(h * G + g) * D);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) qv[r] = sq[ty * 4 + r][c];
+    for (int s = 0; s < KS; ++s) qa[s] = gld16(qp + 4 * s + lq);
+    const float2 *sg = stat + (size_t)g * n0;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) kv[j] = sk[tx * 4 + j][c];
+    for (int j = 0; j < 4; ++j) {
+      const float *ml = reinterpret_cast<const float *>(sg + min(16 * c + 4 * lq + j, n0 - 1));
+      M[j] = gld(ml);
+      iL[j] = gld(ml + 1);
+    }
+  };
+  uint4 qn[KS];
+  float Mn[4], Ln[4];
+  if (items > 0) load(0, qn, Mn, Ln);
+  for (int it = 0; it < items; ++it) {
+    const int c = c0 + (it % per_g) * (NT / 64);
+    uint4 qa[KS];
+    float M[4], iL[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
+    for (int s = 0; s < KS; ++s) qa[s] = qn[s];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) s[r][j] = fmaf(qv[r], kv[j], s[r][j]);
-      }
+    for (int j = 0; j < 4; ++j) {
+      M[j] = Mn[j];
+      iL[j] = 1.f / Ln[j];
+    }
+    if (it + 1 < items) load(it + 1, qn, Mn, Ln);
+    {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i = rb * TB + ty * 4 + r;
-        const float2 ml = sstat[ty * 4 + r];
+      for (int n = 0; n < 4; ++n) {
+        f4v S = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) S = mfma_k32(qa[s], kop[n][s], S);
+        const int key = kb * TB + 16 * n + lr;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int jj = kb * TB + tx * 4 + j;
-          if (i < n0 && jj <= i && jj < n0) col[j] += exp2f(s[r][j] * scale2 - ml.x) / ml.y;
+          const int i = 16 * c + 4 * lq + j;
+          // arguments <= 0 wherever the row statistics hold this logit
+          col[n] += (i < n0 && key <= i && key < n0) ? fexp2(S[j] * scale2 - M[j]) * iL[j] : 0.f;
         }
       }
     }
   }
 #pragma unroll
-  for (int j = 0; j < 4; ++j) scol[ty][tx * 4 + j] = col[j];
+  for (int n = 0; n < 4; ++n) {
+    float x = col[n];
+    x += __shfl_xor(x, 16);
+    x += __shfl_xor(x, 32);
+    if (lq == 0) scol[wave][16 * n + lr] = x;
+  }
   __syncthreads();
   if (threadIdx.x < TB) {
     float acc = 0.f;
-    for (int y = 0; y < 16; ++y) acc += scol[y][threadIdx.x];
+#pragma unroll
+    for (int w = 0; w < NT / 64; ++w) acc += scol[w][threadIdx.x];
     const int jj = kb * TB + threadIdx.x;
     if (jj < n0) (reinterpret_cast<float *>(sd.aux0) + (size_t)h * n0)[jj] = acc;
   }
