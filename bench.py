@@ -311,6 +311,9 @@ def per_config_runs(args):
              ("llama_layer", "KVQ2"), ("h2o", "H2O-20"), ("rocket", "Rocket-4096"),
              # the paper's own settings (Table 1) beyond the benchmark grid
              ("h2o", "H2O-40"), ("h2o", "H2O-60"), ("rocket", "Rocket-16x"), ("rocket", "Rocket-32x")]
+    if args.cases:
+        want = [tuple(c.split("/")) for c in args.cases.split(",")]
+        cases = [c for c in cases if c in want]
     for name, cfg in cases:
         wl = make_workload(name, seed=args.seed, config_ids=cfg)
         b1 = launch_bytes(wl, 0, 0)
@@ -466,6 +469,8 @@ def main():
     ap.add_argument("--no-per-config", action="store_true")
     ap.add_argument("--per-config-only", action="store_true",
                     help="only the per-configuration runs (one JSON line each), for profiling them")
+    ap.add_argument("--cases", default="",
+                    help="comma-separated workload/config pairs to limit the per-configuration runs to")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MiB",
                     help="after the run, launch a plain copy of this size (for memory-counter scaling)")
     args = ap.parse_args()
@@ -486,6 +491,8 @@ def main():
     if args.per_config_only:
         for r in per_config_runs(args):
             print(json.dumps(r), flush=True)
+        if args.copy_probe:
+            copy_probe(args.copy_probe)
         return
     wl = make_workload("mixed", seed=args.seed, steps=args.warmup + args.steps)
     head = run_gpu(wl, args.steps, args.warmup, label="mixed", graph_steps=24)
@@ -506,7 +513,7 @@ def main():
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(head["ms_per_step"], 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f16 storage (fp16 / packed 2-4 bit codes), f32 compute",
+        "dtype": "fp16 operands (fp16 rows, codes dequantized to fp16), fp32 accumulate",
         "data": "synthetic (seeded; workloads.gen)",
         "config": {"workload": "mixed: 64 seqs, 32q/8kv x 128, prompts log-uniform [1024, 32768], "
                                "11 configs assigned uniformly (seed 0); per step: append, top-k, attention (one partial launch over all sequences + combine), eviction, on one stream",
