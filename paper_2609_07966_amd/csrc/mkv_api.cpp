@@ -452,7 +452,7 @@ mkv_status mkv_cache_destroy(mkv_cache *c) {
   if (!c) return MKV_OK;
   for (int k = 0; k < kProfKinds; ++k)
     for (int w = 0; w < 2; ++w)
-      for (hipEvent_t e : c->ev[k][w]) hipEventDestroy(e);
+      for (hipEvent_t e : c->ev[k][w]) (void)hipEventDestroy(e);
   delete c;
   return MKV_OK;
 }
@@ -712,7 +712,7 @@ mkv_status mkv_profile_enable(mkv_cache *c, int32_t enable, int32_t max_launches
   if (e != hipSuccess) return hip_fail(e, "profile enable");
   for (int k = 0; k < kProfKinds; ++k) {
     for (int w = 0; w < 2; ++w) {
-      for (hipEvent_t ev : c->ev[k][w]) hipEventDestroy(ev);
+      for (hipEvent_t ev : c->ev[k][w]) (void)hipEventDestroy(ev);
       c->ev[k][w].clear();
       if (enable >> k & 1)
         for (int i = 0; i < max_launches; ++i) {
