@@ -227,15 +227,18 @@ struct MKVQ {
   // SEG = 48 (d = 64, 3 bits), where it starts at bit 0 or 16 of a word and still spans 2 words
   static constexpr int NW = (SEG + 31) / 32;
   static constexpr int FMASK = (1 << (2 * BITS)) - 1;
+  // LDS row strides of the value-outlier sums and the key-outlier slot sums, padded so that the
+  // heads' rows start in different banks (the same channel or slot of G heads is touched at once)
+  static constexpr int VS = D + 4, KCS = 36;
   const uint8_t *kc, *vc;
   const uint32_t *krow, *kout, *vdel;
   const float *vsc;
   const uint32_t *lutk, *lutv;    // LDS tables: quads (2 words per entry) at 2 bits, else pairs
   const float *cbk;               // LDS key codebook
   const float *qq;                // LDS [D][2G]: scaled q of heads 0..G-1, then scaled q tau
-  float *vacc;                    // LDS [G][D]: this wave's value-outlier terms
+  float *vacc;                    // LDS [G][VS]: this wave's value-outlier terms
   float *kterm;                   // LDS [64][G]: this wave's per-entry key-outlier logit terms
-  float *kcorr;                   // LDS [G + 1][32]: this wave's key-outlier logit terms of the
+  float *kcorr;                   // LDS [G + 1][KCS]: this wave's key-outlier logit terms of the
                                   // batch (row G stays zero)
   int lr, lq, rowbytes, nov, cap;
   struct Raw {
@@ -348,7 +351,7 @@ struct MKVQ {
     }
     if (lane < 32) {
 #pragma unroll
-      for (int g = 0; g < G; ++g) kcorr[g * 32 + lane] = acc[g];
+      for (int g = 0; g < G; ++g) kcorr[g * KCS + lane] = acc[g];
     }
   }
   MKV_DEV int slot(int, const Raw &r, int j) const { return r.t0 + j; }
@@ -359,7 +362,7 @@ struct MKVQ {
   // step s of the batch: this lane's tokens 16 s + 4 lq + j, head lr (columns lr >= G read the
   // zero row)
   MKV_DEV void kfix(int s, float (&x)[4]) const {
-    const float4 c = *reinterpret_cast<const float4 *>(kcorr + min(lr, G) * 32 + 16 * s + 4 * lq);
+    const float4 c = *reinterpret_cast<const float4 *>(kcorr + min(lr, G) * KCS + 16 * s + 4 * lq);
     x[0] += c.x;
     x[1] += c.y;
     x[2] += c.z;
@@ -376,7 +379,7 @@ struct MKVQ {
     for (int j = 0; j < 4; ++j) {
       const uint32_t ent = r.vd[j];
       const bool ok = (valid_mask >> j) & 1;
-      atomicAdd(vacc + lr * D + (ok ? (int)(ent & 127u) : 0), ok ? p[j] * __builtin_bit_cast(float, ent) : 0.f);
+      atomicAdd(vacc + lr * VS + (ok ? (int)(ent & 127u) : 0), ok ? p[j] * __builtin_bit_cast(float, ent) : 0.f);
     }
     if (nov > 1) {  // further entries (outlier budgets above one per token)
       for (int j = 0; j < 4; ++j) {
@@ -384,7 +387,7 @@ struct MKVQ {
         for (int i = 1; i < nov; ++i) {
           const uint32_t ent = gld(vdel + (size_t)i * cap + r.t0 + j);
           if (ent == 0u) break;
-          atomicAdd(vacc + lr * D + (int)(ent & 127u), p[j] * __builtin_bit_cast(float, ent));
+          atomicAdd(vacc + lr * VS + (int)(ent & 127u), p[j] * __builtin_bit_cast(float, ent));
         }
       }
     }
@@ -394,7 +397,7 @@ struct MKVQ {
   // takes a quarter of its head's row)
   MKV_DEV void rescale(float corr) const {
     if (lr >= G) return;
-    float4 *row = reinterpret_cast<float4 *>(vacc + lr * D + lq * (D / 4));
+    float4 *row = reinterpret_cast<float4 *>(vacc + lr * VS + lq * (D / 4));
 #pragma unroll
     for (int c = 0; c < D / 16; ++c) {
       float4 v = row[c];
@@ -796,13 +799,13 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   constexpr int NW = kTileThreads / 64, NM = MG<D>::NM, CPL = MG<D>::CPL, VPL = MG<D>::VPL;
   // per wave: KVQuant value-outlier terms [G][D] while the wave runs; then the wave's (max,
   // sum, o) for the merge
-  constexpr int kWaveFloats = (G * (D + 2) + 3) & ~3;
+  constexpr int kWaveFloats = G * (D + 4);  // holds [G][D + 2] for the merge
   __shared__ __attribute__((aligned(16))) float s_wave[NW][kWaveFloats];
   __shared__ float s_q[D][2 * G];            // KVQuant: scaled q of each head, then scaled q * tau
   __shared__ __attribute__((aligned(16))) uint32_t s_lut[1024];  // KVQuant: key, then value table
   __shared__ float s_cbk[16];                // KVQuant: key codebook
   __shared__ __attribute__((aligned(16))) float s_kt[NW][64 * G];  // KVQuant per-entry key-outlier terms
-  __shared__ __attribute__((aligned(16))) float s_kc[NW][G + 1][32];  // KVQuant key-outlier logit terms
+  __shared__ __attribute__((aligned(16))) float s_kc[NW][G + 1][36];  // KVQuant key-outlier logit terms
   __shared__ float2 s_vm[NW][64];            // uniform 4-bit: a batch's value (min, step) pairs
   __shared__ __attribute__((aligned(16))) float s_km[NW][2 * D];  // uniform 4-bit: a key block's pairs
 
@@ -842,9 +845,9 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
       s_q[c][G + g] = qx * gld(tau + 2 * c);
     }
     float4 *vz = reinterpret_cast<float4 *>(&s_wave[wave][0]);
-    for (int e = lane; e < G * D / 4; e += 64) vz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int e = lane; e < kWaveFloats / 4; e += 64) vz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
     float4 *kz = reinterpret_cast<float4 *>(&s_kc[wave][0][0]);
-    for (int e = lane; e < (G + 1) * 32 / 4; e += 64) kz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int e = lane; e < (G + 1) * 36 / 4; e += 64) kz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
   __syncthreads();
   // q.k operand B: query head lr, channels CPL*lq + 4m .. +3 (KVQuant: fp16 part of the scaled
@@ -963,7 +966,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
 #pragma unroll
-          for (int m = 0; m < NM; ++m) O[m][i] += s_wave[wave][lr * D + VPL * (4 * lq + i) + m];
+          for (int m = 0; m < NM; ++m) O[m][i] += s_wave[wave][lr * (D + 4) + VPL * (4 * lq + i) + m];
         }
       }
     };
