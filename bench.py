@@ -161,7 +161,7 @@ def product_codebooks(wl, tokens=1024):
     return flat
 
 
-KIND_BITS = {"partial": 0, "combine": 1, "append": 2, "topk": 3}
+KIND_BITS = {"partial": 0, "combine": 1, "append": 2, "topk": 3, "append_score": 4}
 
 
 def run_gpu(wl, steps, warmup, replicas=1, label="", prof_steps=24, graph_steps=0):

@@ -216,9 +216,14 @@ mkv_status mkv_decode_attention_noalloc(mkv_cache *cache, const uint16_t *q, flo
  * enqueues nothing and leaves the handle unchanged.  Only MKV_EHIP can come
  * after a launch, and then the step may be partly enqueued.
  *
- * Graph capture: the step enqueues four kernels on `stream` and nothing else
- * (no allocation, copy, memset or synchronization; profiling events only
- * when enabled), and every per-step quantity (counts, positions, H2O victims,
+ * With RocketKV sequences in the batch the step's append launch also computes
+ * their approximate scores, spread over several workgroups per kv head, and a
+ * selection launch follows (the effect is that of the two calls in order).
+ *
+ * Graph capture: the step enqueues three or four kernels on `stream` (the
+ * append, with the scores when RocketKV sequences are present; their
+ * selection; attention partial; combine) and nothing else (no allocation,
+ * copy, memset or synchronization; profiling events only when enabled), and every per-step quantity (counts, positions, H2O victims,
  * outlier fills) lives in device state, so a captured step may be replayed
  * any number of times with new k, v, q written into the captured buffers.
  * The host-side step count then no longer follows the device: capacity is
@@ -275,7 +280,9 @@ mkv_status mkv_fit_codebooks(const uint16_t *k, const uint16_t *v, int32_t n_tok
  * selected.  mkv_profile_read waits for them and returns, for kind `kind`,
  * the launch count and the summed device time in milliseconds.  Kinds:
  * 0 attention partial (one launch over every sequence's tiles), 1 attention
- * combine, 2 append, 3 top-k select.
+ * combine, 2 append, 3 top-k select, 4 the append of mkv_decode_step with
+ * RocketKV sequences present (it also computes their approximate scores; the
+ * step's selection then counts as kind 3).
  */
 mkv_status mkv_profile_enable(mkv_cache *cache, int32_t enable, int32_t max_launches);
 mkv_status mkv_profile_read(mkv_cache *cache, int32_t kind, int32_t *launches, double *total_ms);

@@ -17,7 +17,7 @@ EXPORT = {
     "scales_k": 6, "scales_v": 7, "scores": 8, "topk": 9, "channels": 10,
 }
 
-PROFILE_KINDS = {"partial": 0, "combine": 1, "append": 2, "topk": 3}
+PROFILE_KINDS = {"partial": 0, "combine": 1, "append": 2, "topk": 3, "append_score": 4}
 
 
 class mkv_config(ctypes.Structure):

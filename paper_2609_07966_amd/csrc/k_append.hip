@@ -5,7 +5,7 @@
 // per-channel key thresholds calibrated on the prompt and fp16 outliers.  The quantizer steps are
 // written with explicit round-to-nearest float32 operations (__fmul_rn, __fsub_rn, __fdiv_rn)
 // so that codes are reproducible bit for bit.
-#include "kernels_common.h"
+#include "select_dev.h"
 
 namespace mkv {
 
@@ -39,7 +39,7 @@ MKV_DEV uint32_t packed_word(const uint8_t *codes, int n, int bits, int w) {
   return word;
 }
 
-// Pack one code per thread (thread c = channel c, blockDim.x == D) into a key row (see
+// Pack one code per thread (thread c = channel c of threads 0..D-1) into a key row (see
 // packed_word).  `s_code` is D bytes of LDS.
 template <int D>
 MKV_DEV void pack_row(int code, int bits, uint8_t *s_code, uint8_t *row) {
@@ -61,7 +61,7 @@ MKV_DEV void or_quad_code(uint32_t *s_blk, int c, int j, int code, int bits) {
   if (spill > 0) atomicOr(&s_blk[(bit >> 5) + 1], (uint32_t)code >> (bits - spill));
 }
 
-// Inclusive rank among flagged threads of the block (blockDim.x == D <= 128) and the total.
+// Inclusive rank among flagged threads 0..D-1 (D <= 128, the threads that reach the barriers).
 template <int D>
 MKV_DEV int flag_rank(bool f, int *s_tmp, int *total) {
   const uint64_t m = __ballot(f);
@@ -162,7 +162,7 @@ MKV_DEV void store_quad(const SeqDesc &sd, int h, int t0, const uint32_t *s_blk,
   const int words = D * sd.bits / 8;  // 4 tokens x D codes x bits / 32
   uint32_t *dst = reinterpret_cast<uint32_t *>(reinterpret_cast<uint8_t *>(sd.vc) + h * stride_codes(sd) +
                                                (size_t)(t0 / 4) * 4 * sd.rowbytes);
-  for (int w = threadIdx.x; w < words; w += blockDim.x) gst(dst + w, s_blk[w]);
+  for (int w = threadIdx.x; w < words; w += D) gst(dst + w, s_blk[w]);
 }
 
 // KVQ key of one token: code under the frozen per-channel threshold, and the outlier flag.
@@ -200,11 +200,12 @@ MKV_DEV void or_uq_code(uint32_t *s_blk, int ch, int j, int code, int D) {
   atomicOr(&s_blk[bit >> 5], (uint32_t)code << (bit & 31));
 }
 
-// Write a 4-token block (D/2 words) from an LDS image; t0 is the block's first slot.
+// Write a 4-token block (D/2 words) from an LDS image by D threads; t0 is the block's first slot.
+template <int D>
 MKV_DEV void store_block(uint8_t *codes, int h_stride_bytes, int h, int t0, int rowbytes, const uint32_t *s_blk,
                          int words) {
   uint32_t *dst = reinterpret_cast<uint32_t *>(codes + (size_t)h * h_stride_bytes + (size_t)(t0 / 4) * 4 * rowbytes);
-  for (int w = threadIdx.x; w < words; w += blockDim.x) gst(dst + w, s_blk[w]);
+  for (int w = threadIdx.x; w < words; w += D) gst(dst + w, s_blk[w]);
 }
 
 // UQ key block: thread c quantizes channel c over 64 tokens read through `get(t)`.
@@ -231,22 +232,28 @@ MKV_DEV void uq_key_block(const SeqDesc &sd, int h, int blk, Get get) {
       make_float2(mn, __fdiv_rn(r, 15.0f));
 }
 
-// ---- decode append: one workgroup of D threads per (sequence, kv head) -----------------------
+// ---- decode append: D threads per (sequence, kv head) ------------------------------------------
 template <int D>
-__global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict__ seqs, int32_t *state,
-                                                      const uint16_t *__restrict__ k,
-                                                      const uint16_t *__restrict__ v,
-                                                      const float *__restrict__ cbtab, int Hkv) {
-  __shared__ float s_abs[D];
-  __shared__ float s_scale;
-  __shared__ uint8_t s_code[D];
-  __shared__ int s_tmp[4];
-  __shared__ uint32_t s_blk[D / 2];
-  __shared__ float s_cbt[kCbTableFloats];  // codebooks and midpoints, read many times below
-  const int seq = blockIdx.x / Hkv, h = blockIdx.x % Hkv, c = threadIdx.x;
+struct AppendLds {
+  float abs[D];
+  float scale;
+  uint8_t code[D];
+  int tmp[4];
+  uint32_t blk[D / 2];
+  float cbt[kCbTableFloats];  // codebooks and midpoints, read many times below
+};
+
+// Append the new token of (seq, h) by threads 0..D-1 of the workgroup (every barrier below is
+// reached by exactly those threads).
+template <int D>
+MKV_DEV void append_pair(const SeqDesc &sd, int32_t *st, int seq, int h, int Hkv, const uint16_t *__restrict__ k,
+                         const uint16_t *__restrict__ v, const float *__restrict__ cbtab, AppendLds<D> &L) {
+  float *s_abs = L.abs, *s_cbt = L.cbt;
+  uint8_t *s_code = L.code;
+  int *s_tmp = L.tmp;
+  uint32_t *s_blk = L.blk;
+  const int c = threadIdx.x;
   for (int i = c; i < kCbTableFloats; i += D) s_cbt[i] = cbtab[i];
-  const SeqDesc &sd = seqs[seq];
-  int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
   const int count = st[ST_COUNT], pos = st[ST_NEXT_POS];
   // H2O: an eviction decided by the last attention pass frees its slot for this token (-1: none)
   const int victim = sd.method == H2O ? st[ST_VICTIM] : -1;
@@ -300,7 +307,7 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
       __syncthreads();
       or_uq_code(s_blk, c, j, vcode, D);
       __syncthreads();
-      store_block(reinterpret_cast<uint8_t *>(sd.vc), (int)stride_codes(sd), h, count & ~3, sd.rowbytes, s_blk, words);
+      store_block<D>(reinterpret_cast<uint8_t *>(sd.vc), (int)stride_codes(sd), h, count & ~3, sd.rowbytes, s_blk, words);
       uint16_t *res = reinterpret_cast<uint16_t *>(sd.kres) + (size_t)h * 64 * D;
       res[(size_t)(count & 63) * D + c] = (uint16_t)kb;
       if ((count & 63) == 63) {
@@ -321,7 +328,7 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
       const int fill = st[ST_KOUT_FILL];
       uint32_t *ko = reinterpret_cast<uint32_t *>(sd.kout) + h * stride_kout(sd);
       if (outl) ko[fill + r] = outlier_entry(kb, count, code, c);
-      const int vcode = kvq_value_token<D>(sd, h, count, vb, s_cbt, s_abs, &s_scale, s_tmp);
+      const int vcode = kvq_value_token<D>(sd, h, count, vb, s_cbt, s_abs, &L.scale, s_tmp);
       // the value code goes into its 4-token block: the block's first token writes the whole
       // block (other tokens' codes zero); later tokens OR their bits into the stored words
       const int j = count & 3, words = D * sd.bits / 8;
@@ -351,6 +358,94 @@ __global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict
       break;
   }
   if (c == 0) st[ST_NEXT_POS] = pos + 1;
+}
+
+// One workgroup of D threads per (sequence, kv head).
+template <int D>
+__global__ __launch_bounds__(128) void k_append_decode(const SeqDesc *__restrict__ seqs, int32_t *state,
+                                                      const uint16_t *__restrict__ k,
+                                                      const uint16_t *__restrict__ v,
+                                                      const float *__restrict__ cbtab, int Hkv) {
+  __shared__ AppendLds<D> L;
+  const int seq = blockIdx.x / Hkv, h = blockIdx.x % Hkv;
+  append_pair<D>(seqs[seq], state + ((size_t)seq * Hkv + h) * ST_WORDS, seq, h, Hkv, k, v, cbtab, L);
+}
+
+// The decode step's first two launches when RocketKV sequences are present.
+//
+// k_append_score, workgroups of kScoreThreads threads over a work list (int4: seq, kv head,
+// part, parts): part -1 appends the token of a non-RocketKV pair on its first D threads (the
+// other waves leave at once; a barrier waits only for waves that have not ended).  A RocketKV pair
+// has ceil(cap / kScoreTokens) parts: part 0 appends its token (rows, channel-major copy,
+// position) and every part picks the channels and scores its kScoreTokens tokens, the new one
+// from the key it holds in LDS.  The state of a RocketKV pair is left to the selecting launch.
+//
+// k_rocket_select, one workgroup of kTopkThreads threads per RocketKV pair (int2: seq, kv head):
+// the top-k of the scores, then the pair's state (count, next position, selection count).
+template <int D, int G>
+__global__ __launch_bounds__(kScoreThreads) void k_append_score(const SeqDesc *__restrict__ seqs, int32_t *state,
+                                                                const int4 *__restrict__ items,
+                                                                const uint16_t *__restrict__ k,
+                                                                const uint16_t *__restrict__ v,
+                                                                const uint16_t *__restrict__ q,
+                                                                const float *__restrict__ cbtab, int Hkv) {
+  __shared__ union {
+    AppendLds<D> a;
+    ChanLds<D, kScoreThreads> c;
+  } L;
+  const int4 it = items[blockIdx.x];
+  const int seq = it.x, h = it.y, part = it.z, c = threadIdx.x;
+  const SeqDesc &sd = seqs[seq];
+  int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
+  if (part < 0) {
+    if (c >= D) return;
+    append_pair<D>(sd, st, seq, h, Hkv, k, v, cbtab, L.a);
+    return;
+  }
+  const int count = st[ST_COUNT];
+  // a full region (reachable only by replaying a captured decode step past max_new_tokens) drops
+  // the token, as the separate append does
+  const bool room = count < sd.cap;
+  if (room && c < D) {
+    const uint16_t kb = k[((size_t)seq * Hkv + h) * D + c];
+    L.c.knew[c] = kb;
+    if (part == 0) {
+      const uint16_t vb = v[((size_t)seq * Hkv + h) * D + c];
+      (reinterpret_cast<uint16_t *>(sd.k) + h * stride_rows(sd, D))[(size_t)count * D + c] = kb;
+      (reinterpret_cast<uint16_t *>(sd.v) + h * stride_rows(sd, D))[(size_t)count * D + c] = vb;
+      (reinterpret_cast<uint16_t *>(sd.kcm) + h * stride_kcm(sd, D))[(size_t)c * sd.cstride + count] = kb;
+      if (c == 0) (reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd))[count] = st[ST_NEXT_POS];
+    }
+  }
+  score_part<D, G>(sd, seq, h, Hkv, room ? count + 1 : count, part, room, q, L.c);
+}
+
+template <int D>
+__global__ __launch_bounds__(kTopkThreads) void k_rocket_select(const SeqDesc *__restrict__ seqs, int32_t *state,
+                                                                const int2 *__restrict__ pairs, int Hkv) {
+  __shared__ SelLds L;
+  const int2 pr = pairs[blockIdx.x];
+  const int seq = pr.x, h = pr.y, tid = threadIdx.x;
+  const SeqDesc &sd = seqs[seq];
+  int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
+  const int count = st[ST_COUNT], pos = st[ST_NEXT_POS];
+  const bool room = count < sd.cap;
+  const int n = room ? count + 1 : count, k = sd.topk;
+  int32_t *sel = reinterpret_cast<int32_t *>(sd.sel) + h * stride_sel(sd);
+  if (k >= n) {
+    for (int j = tid; j < n; j += kTopkThreads) sel[j] = j;
+  } else {
+    const uint32_t *akeys = reinterpret_cast<const uint32_t *>(sd.akeys) + h * stride_slots(sd);
+    select_keys<kTopkThreads>(n, k, [&](int j) { return gld(akeys + j); }, sel, L);
+  }
+  __syncthreads();  // every thread has read the state
+  if (tid == 0) {
+    st[ST_SEL_COUNT] = min(k, n);
+    if (room) {
+      st[ST_COUNT] = count + 1;
+      st[ST_NEXT_POS] = pos + 1;
+    }
+  }
 }
 
 // ---- prefill -----------------------------------------------------------------------------------
@@ -386,7 +481,7 @@ __global__ __launch_bounds__(128) void k_prefill_uq_values(const SeqDesc *__rest
     or_uq_code(s_blk, c, j, code, D);
   }
   __syncthreads();
-  store_block(reinterpret_cast<uint8_t *>(sd.vc), (int)stride_codes(sd), h, 4 * q, sd.rowbytes, s_blk, D / 2);
+  store_block<D>(reinterpret_cast<uint8_t *>(sd.vc), (int)stride_codes(sd), h, 4 * q, sd.rowbytes, s_blk, D / 2);
 }
 
 template <int D>
@@ -536,6 +631,16 @@ hipError_t append_decode_impl(const Dev &dv, const Shape &sh, const uint16_t *k,
   return hipGetLastError();
 }
 
+template <int D, int G>
+hipError_t append_select_impl(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
+                              const uint16_t *q, hipStream_t st, LaunchEv ev_score, LaunchEv ev_select) {
+  hipExtLaunchKernelGGL((k_append_score<D, G>), dim3(dv.n_prep), dim3(kScoreThreads), 0, st, ev_score.start,
+                        ev_score.stop, 0, dv.seqs, dv.state, dv.prep, k, v, q, dv.cbtab, sh.Hkv);
+  hipExtLaunchKernelGGL(k_rocket_select<D>, dim3(dv.n_rk_pairs), dim3(kTopkThreads), 0, st, ev_select.start,
+                        ev_select.stop, 0, dv.seqs, dv.state, dv.rk_pairs, sh.Hkv);
+  return hipGetLastError();
+}
+
 template <int D>
 hipError_t prefill_impl(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq, const uint16_t *k,
                         const uint16_t *v, hipStream_t st) {
@@ -577,6 +682,21 @@ hipError_t prefill_impl(const Dev &dv, const Shape &sh, const SeqDesc &hs, int s
 hipError_t launch_append_decode(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
                                 hipStream_t st, LaunchEv ev) {
   return sh.D == 64 ? append_decode_impl<64>(dv, sh, k, v, st, ev) : append_decode_impl<128>(dv, sh, k, v, st, ev);
+}
+
+hipError_t launch_append_select(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
+                                const uint16_t *q, hipStream_t st, LaunchEv ev_score, LaunchEv ev_select) {
+  switch (sh.D * 16 + sh.G) {
+    case 64 * 16 + 1: return append_select_impl<64, 1>(dv, sh, k, v, q, st, ev_score, ev_select);
+    case 64 * 16 + 2: return append_select_impl<64, 2>(dv, sh, k, v, q, st, ev_score, ev_select);
+    case 64 * 16 + 4: return append_select_impl<64, 4>(dv, sh, k, v, q, st, ev_score, ev_select);
+    case 64 * 16 + 8: return append_select_impl<64, 8>(dv, sh, k, v, q, st, ev_score, ev_select);
+    case 128 * 16 + 1: return append_select_impl<128, 1>(dv, sh, k, v, q, st, ev_score, ev_select);
+    case 128 * 16 + 2: return append_select_impl<128, 2>(dv, sh, k, v, q, st, ev_score, ev_select);
+    case 128 * 16 + 4: return append_select_impl<128, 4>(dv, sh, k, v, q, st, ev_score, ev_select);
+    case 128 * 16 + 8: return append_select_impl<128, 8>(dv, sh, k, v, q, st, ev_score, ev_select);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq, const uint16_t *k,

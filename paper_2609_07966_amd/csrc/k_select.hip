@@ -5,14 +5,13 @@
 // observation window votes for (SnapKV), then attends to a top-k subset per decode step.
 // Selections are block-wide radix selects on order-preserving 32-bit keys followed by an
 // ascending-position compaction, so ties resolve by position exactly as specified.
-#include "kernels_common.h"
+#include "select_dev.h"
 
 namespace mkv {
 
 namespace {
 
 constexpr int NT = 256;
-constexpr int kTopkLdsKeys = 10240;  // score keys of up to this many retained tokens stay in LDS
 
 // Compact positions [0, n) whose flag is set into ascending slots; calls emit(j, slot) for each.
 // flag(j, eq_before) may use eq_before = number of keys equal to the threshold at indices < j.
@@ -36,265 +35,18 @@ MKV_DEV int compact_ascending(int n, Flag flag, IsEq is_eq, Emit emit, int *s_tm
 }
 
 // ---- RocketKV decode top-k ---------------------------------------------------------------------
-// Radix select of the k-th largest of n keys (4 passes of 8 bits) for a workgroup of NT threads:
-// one histogram per wave, two sets used in turn so that the set of the next pass is cleared
-// while wave 0 searches the digit of this one (2 barriers per pass).  hist[0] must be zero and
-// visible on entry.  Returns the k-th key, how many keys equal it and how many of those are needed.
-template <int NTH, typename Get>
-MKV_DEV void topk_radix(int n, int k, Get get, int (*hist)[NTH / 64][256], int *s3, uint32_t *kth, int *n_equal,
-                        int *need) {
-  constexpr int NWV = NTH / 64;
-  const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  uint32_t prefix = 0, mask = 0;
-  int remaining = k, eq = 0;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int buf = pass & 1, shift = 24 - 8 * pass;
-    for (int i = threadIdx.x; i < n; i += NTH) {
-      const uint32_t key = get(i);
-      if ((key & mask) == prefix) atomicAdd(&hist[buf][wid][(key >> shift) & 255u], 1);
-    }
-    __syncthreads();
-    if (wid == 0) {
-      // lane l owns digits 255 - 4l .. 252 - 4l (descending), so the exclusive scan over lanes
-      // gives the count of larger digits
-      int cnt[4], tot = 0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int d = 255 - (4 * lane + i);
-        int c = 0;
-#pragma unroll
-        for (int w = 0; w < NWV; ++w) c += hist[buf][w][d];
-        cnt[i] = c;
-        tot += c;
-      }
-      int inc = tot;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(inc, o);
-        if (lane >= o) inc += y;
-      }
-      int above = inc - tot;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (above < remaining && remaining <= above + cnt[i]) {
-          s3[0] = 255 - (4 * lane + i);
-          s3[1] = remaining - above;
-          s3[2] = cnt[i];
-        }
-        above += cnt[i];
-      }
-    } else {
-      for (int e = threadIdx.x - 64; e < NWV * 256; e += NTH - 64) (&hist[buf ^ 1][0][0])[e] = 0;
-    }
-    __syncthreads();
-    prefix |= (uint32_t)s3[0] << shift;
-    mask |= 255u << shift;
-    remaining = s3[1];
-    eq = s3[2];
-  }
-  *kth = prefix;
-  *n_equal = eq;
-  *need = remaining;
-}
-
-
-// Approximate scores of the T consecutive tokens [j0, j0 + T) (T = 4 or 8) from the channel-major
-// key copy: one 2T-byte load per selected channel, R channels' loads issued before any is used,
-// channels ascending, every product and sum rounded to fp32 separately (no fused multiply-add).
-// Rows are padded to 8 tokens and j0 is a multiple of T, so no load leaves its row.
-template <int T, int R>
-MKV_DEV void score_tokens(const uint16_t *kcm, int cstride, int j0, int nch, const int *sel_ch, const float *sel_qb,
-                          float (&acc)[T]) {
-#pragma unroll
-  for (int t = 0; t < T; ++t) acc[t] = 0.f;
-  for (int i0 = 0; i0 < nch; i0 += R) {
-    uint32_t w[R][T / 2];
-#pragma unroll
-    for (int ii = 0; ii < R; ++ii) {
-      const int i = min(i0 + ii, nch - 1);
-      const uint32_t *p = reinterpret_cast<const uint32_t *>(kcm + (size_t)sel_ch[i] * cstride + j0);
-#pragma unroll
-      for (int u = 0; u < T / 2; ++u) w[ii][u] = gld(p + u);
-    }
-#pragma unroll
-    for (int ii = 0; ii < R; ++ii) {
-      if (i0 + ii < nch) {
-        const float qb = sel_qb[i0 + ii];
-#pragma unroll
-        for (int u = 0; u < T / 2; ++u) {
-          acc[2 * u] = __fadd_rn(acc[2 * u], __fmul_rn(qb, h2f(w[ii][u])));
-          acc[2 * u + 1] = __fadd_rn(acc[2 * u + 1], __fmul_rn(qb, h2f(w[ii][u] >> 16)));
-        }
-      }
-    }
-  }
-}
-
-
-// One workgroup of 1024 threads per (sequence, kv head): a kept set of up to a few thousand
-// tokens is scored with ~4 tokens per thread and selected by radix passes over LDS keys.
-constexpr int kTopkThreads = 1024;
+// One workgroup of kTopkThreads threads per (sequence, kv head) over the tokens already appended
+// (a decode step instead spreads the scores over several workgroups, in k_append.hip).
 template <int D, int G>
-__global__ __launch_bounds__(kTopkThreads) void k_topk(const SeqDesc *__restrict__ seqs, int32_t *state,
-                                             const uint16_t *__restrict__ q, int32_t *pos_out, int topk_max,
-                                             int Hkv) {
-  __shared__ float s_a[D];
-  __shared__ float s_qb[D];
-  __shared__ int s_ch[D];
-  __shared__ int s_beats[kTopkThreads];
-  __shared__ int whist[2][kTopkThreads / 64][256];
-  __shared__ int s3[3];
-  __shared__ int s_tmp[kTopkThreads / 64];
-  __shared__ uint32_t s_keys[kTopkLdsKeys];
+__global__ __launch_bounds__(kTopkThreads, 8) void k_topk(const SeqDesc *__restrict__ seqs, int32_t *state,
+                                                       const uint16_t *__restrict__ q, int32_t *pos_out,
+                                                       int topk_max, int Hkv) {
+  __shared__ TopkLds<D> L;
   const int seq = blockIdx.x / Hkv, h = blockIdx.x % Hkv;
   const SeqDesc &sd = seqs[seq];
   if (sd.method != ROCKET) return;
   int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
-  const int n = st[ST_COUNT];
-  const int k = sd.topk;
-  int32_t *sel = reinterpret_cast<int32_t *>(sd.sel) + h * stride_sel(sd);
-  const int32_t *pos = reinterpret_cast<const int32_t *>(sd.pos) + h * stride_slots(sd);
-  int32_t *chan_out = reinterpret_cast<int32_t *>(sd.aux1) + (size_t)h * D;
-  const int Hq = Hkv * G;
-  const uint16_t *qh = q + ((size_t)seq * Hq + h * G) * D;
-
-  // channel magnitudes and head sums, float32 in ascending head order
-  for (int c = threadIdx.x; c < D; c += kTopkThreads) {
-    float a = 0.f, qb = 0.f;
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const float x = h2f(qh[(size_t)g * D + c]);
-      a = __fadd_rn(a, fabsf(x));
-      qb = __fadd_rn(qb, x);
-    }
-    s_a[c] = a;
-    s_qb[c] = qb;
-  }
-  __syncthreads();
-  const int nch = min(sd.nch, D);
-  // channel c is selected iff fewer than nch channels beat it (larger a, or equal a and lower
-  // index); the kTopkThreads / D threads of channel c each count a slice of the others
-  {
-    static_assert(kTopkThreads % D == 0, "whole slices per channel");
-    constexpr int P = kTopkThreads / D, W = D / P;
-    const int c = threadIdx.x % D, part = threadIdx.x / D;
-    const float a = s_a[c];
-    int beats = 0;
-#pragma unroll
-    for (int i = 0; i < W; ++i) {
-      const int c2 = part * W + i;
-      const float b = s_a[c2];
-      beats += (b > a || (b == a && c2 < c)) ? 1 : 0;
-    }
-    s_beats[threadIdx.x] = beats;
-  }
-  __syncthreads();
-  if (threadIdx.x < D) {
-    int t = 0;
-#pragma unroll
-    for (int p = 0; p < kTopkThreads / D; ++p) t += s_beats[p * D + threadIdx.x];
-    s_ch[threadIdx.x] = t < nch ? 1 : 0;
-  }
-  __syncthreads();
-  __shared__ int s_sel_ch[D];
-  __shared__ float s_sel_qb[D];
-  __shared__ int s_wcnt[(D + 63) / 64];
-  // ascending compaction of the selected channels: rank = selected channels below c
-  {
-    const int c = threadIdx.x;
-    const bool f = c < D && s_ch[c] != 0;
-    const uint64_t m = __ballot(f);
-    const int lane = c & 63, w = c >> 6;
-    if (c < D && lane == 0) s_wcnt[w] = __popcll(m);
-    __syncthreads();
-    if (f) {
-      int r = __popcll(m & ((lane == 0) ? 0ull : (~0ull >> (64 - lane))));
-      for (int i = 0; i < w; ++i) r += s_wcnt[i];
-      s_sel_ch[r] = c;
-      s_sel_qb[r] = s_qb[c];
-    }
-  }
-  __syncthreads();
-  for (int i = threadIdx.x; i < nch; i += kTopkThreads) chan_out[i] = s_sel_ch[i];
-
-  if (k >= n) {
-    for (int j = threadIdx.x; j < n; j += kTopkThreads) sel[j] = j;
-    if (pos_out != nullptr)
-      for (int i = threadIdx.x; i < topk_max; i += kTopkThreads)
-        pos_out[((size_t)seq * Hkv + h) * topk_max + i] = i < n ? pos[i] : -1;
-    if (threadIdx.x == 0) st[ST_SEL_COUNT] = n;
-    return;
-  }
-
-  // approximate scores from the channel-major key copy, channels ascending,
-  // acc = fl32(acc + fl32(qbar_c * k_jc)); the keys stay in LDS when they fit.  A lane scores 4
-  // consecutive tokens (8 for sets of more than 4 kTopkThreads tokens, so that one pass covers up
-  // to 8 kTopkThreads)
-  const uint16_t *kcm = reinterpret_cast<const uint16_t *>(sd.kcm) + h * stride_kcm(sd, D);
-  uint32_t *akeys = reinterpret_cast<uint32_t *>(sd.akeys) + h * stride_slots(sd);
-  const bool in_lds = n <= kTopkLdsKeys;
-  const int cstride = sd.cstride;
-  auto put = [&](int j, float a) {
-    if (j < n) {
-      if (in_lds) s_keys[j] = float_key(a);
-      else gst(akeys + j, float_key(a));
-    }
-  };
-  if (n <= 4 * kTopkThreads) {
-    const int j0 = 4 * (int)threadIdx.x;
-    if (j0 < n) {
-      float acc[4];
-      score_tokens<4, 32>(kcm, cstride, j0, nch, s_sel_ch, s_sel_qb, acc);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) put(j0 + r, acc[r]);
-    }
-  } else {
-    for (int j0 = 8 * (int)threadIdx.x; j0 < n; j0 += 8 * kTopkThreads) {
-      float acc[8];
-      score_tokens<8, 16>(kcm, cstride, j0, nch, s_sel_ch, s_sel_qb, acc);
-#pragma unroll
-      for (int r = 0; r < 8; ++r) put(j0 + r, acc[r]);
-    }
-  }
-  for (int e = threadIdx.x; e < (kTopkThreads / 64) * 256; e += kTopkThreads) (&whist[0][0][0])[e] = 0;
-  __syncthreads();
-  auto getk = [&](int i) { return in_lds ? s_keys[i] : gld(akeys + i); };
-  uint32_t kth;
-  int n_eq, need;
-  topk_radix<kTopkThreads>(n, k, getk, whist, s3, &kth, &n_eq, &need);
-  // each thread takes a contiguous run of tokens; counts of keys above and equal to the
-  // threshold before its run place its selected tokens in ascending order
-  const int per = (n + kTopkThreads - 1) / kTopkThreads;
-  const int ja = min(n, (int)threadIdx.x * per), jb = min(n, ja + per);
-  int gt = 0, eq = 0;
-  for (int j = ja; j < jb; ++j) {
-    const uint32_t kk = getk(j);
-    gt += kk > kth ? 1 : 0;
-    eq += kk == kth ? 1 : 0;
-  }
-  // one scan of both counts when n < 2^15 keeps them apart in the two halves of a word
-  int tot, gt_before, eq_run;
-  if (n < 32768) {
-    const int both = block_exclusive_scan<kTopkThreads>((gt << 16) | eq, s_tmp, &tot);
-    gt_before = both >> 16;
-    eq_run = both & 0xFFFF;
-  } else {
-    gt_before = block_exclusive_scan<kTopkThreads>(gt, s_tmp, &tot);
-    eq_run = block_exclusive_scan<kTopkThreads>(eq, s_tmp, &tot);
-  }
-  int slot = gt_before + min(eq_run, need);
-  for (int j = ja; j < jb; ++j) {
-    const uint32_t kk = getk(j);
-    const bool take = kk > kth || (kk == kth && eq_run < need);
-    eq_run += kk == kth ? 1 : 0;
-    if (take && slot < k) gst(sel + slot, j);
-    slot += take ? 1 : 0;
-  }
-  __syncthreads();
-  if (pos_out != nullptr)
-    for (int i = threadIdx.x; i < topk_max; i += kTopkThreads)
-      pos_out[((size_t)seq * Hkv + h) * topk_max + i] = i < k ? gld(pos + gld(sel + i)) : -1;
-  if (threadIdx.x == 0) st[ST_SEL_COUNT] = k;
+  topk_pair<D, G>(sd, st, seq, h, Hkv, st[ST_COUNT], q, pos_out, topk_max, L);
 }
 
 // ---- causal prefill attention statistics for H2O scoring, on the matrix cores ------------------

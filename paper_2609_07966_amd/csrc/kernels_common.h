@@ -143,16 +143,25 @@ MKV_DEV uint32_t float_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Inclusive prefix sum over the wave (all lanes active) by DPP: four row shifts give every row of
+// 16 lanes its own prefix sums (lanes whose source lies before the row add 0), then row_bcast:15
+// adds row 0's and row 2's totals to rows 1 and 3, and row_bcast:31 the total of rows 0-1 to
+// rows 2 and 3.
+MKV_DEV int wave_incl_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, true);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, true);   // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return x;
+}
+
 // Exclusive prefix sum over a block of NT threads (NT multiple of 64).  `tmp` is NT/64 ints of LDS.
 template <int NT>
 MKV_DEV int block_exclusive_scan(int x, int *tmp, int *total) {
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  int inc = x;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    int y = __shfl_up(inc, o);
-    if (lane >= o) inc += y;
-  }
+  const int inc = wave_incl_scan(x);
   if (lane == 63) tmp[wid] = inc;
   __syncthreads();
   int base = 0, tot = 0;
@@ -204,49 +213,6 @@ MKV_DEV void radix_select_kth(int n, int k, Get get, int *hist, int *shared3, ui
   }
   *kth = prefix;
   *n_equal = eq;
-  *need = remaining;
-}
-
-// Radix select as above with one histogram per wave (less atomic contention on popular digits)
-// and a parallel digit search.  `whist` is NT/64 x 256 ints, `s_tmp` NT/64 ints, `shared3` 3 ints.
-template <int NT, typename Get>
-MKV_DEV void radix_select_kth_waves(int n, int k, Get get, int (*whist)[256], int *shared3, int *s_tmp,
-                                    uint32_t *kth, int *n_equal, int *need) {
-  static_assert(NT >= 256 && NT % 64 == 0, "threads 0..255 own one digit each");
-  const int wid = threadIdx.x >> 6;
-  uint32_t prefix = 0, mask = 0;
-  int remaining = k;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    for (int e = threadIdx.x; e < (NT / 64) * 256; e += NT) (&whist[0][0])[e] = 0;
-    __syncthreads();
-    for (int i = threadIdx.x; i < n; i += NT) {
-      const uint32_t key = get(i);
-      if ((key & mask) == prefix) atomicAdd(&whist[wid][(key >> shift) & 255u], 1);
-    }
-    __syncthreads();
-    // thread b < 256 owns digit 255 - b, so the exclusive scan gives the count of larger digits
-    const int dgt = 255 - (int)threadIdx.x;
-    int cnt = 0;
-    if (threadIdx.x < 256) {
-#pragma unroll
-      for (int w = 0; w < NT / 64; ++w) cnt += whist[w][dgt];
-    }
-    int tot;
-    const int above = block_exclusive_scan<NT>(cnt, s_tmp, &tot);
-    if (threadIdx.x < 256 && above < remaining && remaining <= above + cnt) {
-      shared3[0] = dgt;
-      shared3[1] = remaining - above;
-      shared3[2] = cnt;
-    }
-    __syncthreads();
-    prefix |= (uint32_t)shared3[0] << shift;
-    mask |= 255u << shift;
-    remaining = shared3[1];
-    *n_equal = shared3[2];
-    __syncthreads();
-  }
-  *kth = prefix;
   *need = remaining;
 }
 

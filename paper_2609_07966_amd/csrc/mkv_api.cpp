@@ -43,13 +43,16 @@ mkv_status hip_fail(hipError_t e, const char *what) {
 
 enum Phase { PH_CREATED, PH_PROMPT, PH_READY, PH_APPENDED, PH_SELECTED, PH_ATTENDED };
 
-constexpr int kProfKinds = 4;
+constexpr int kProfKinds = 5;
 
 struct Layout {
   std::vector<SeqDesc> seqs;  // offsets (relative to the arena) in the pointer fields
   size_t off_seqs = 0, off_state = 0, off_tiles = 0, off_cbtab = 0, off_partials = 0, total = 0;
+  size_t off_prep = 0, off_rk_pairs = 0;
   int n_tiles = 0, n_tiles_uq = 0, n_tiles_rk = 0;
   std::vector<int4> tiles;
+  std::vector<int4> prep;      // decode-step append / scoring work list
+  std::vector<int2> rk_pairs;  // RocketKV (seq, kv head) pairs
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -268,6 +271,24 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
   }
   L->n_tiles = (int)L->tiles.size();
   L->off_tiles = take(sizeof(int4) * L->n_tiles);
+  // a decode step's append and scoring work: RocketKV scoring parts (one per kScoreTokens tokens
+  // of the largest retained set) first, then the plain appends
+  L->prep.clear();
+  L->rk_pairs.clear();
+  for (int s = 0; s < S; ++s) {
+    const SeqDesc &d = L->seqs[s];
+    if (d.method != ROCKET) continue;
+    const int parts = (d.cap + kScoreTokensPerPart - 1) / kScoreTokensPerPart;
+    for (int h = 0; h < Hkv; ++h) {
+      L->rk_pairs.push_back(make_int2(s, h));
+      for (int p = 0; p < parts; ++p) L->prep.push_back(make_int4(s, h, p, parts));
+    }
+  }
+  for (int s = 0; s < S; ++s)
+    if (L->seqs[s].method != ROCKET)
+      for (int h = 0; h < Hkv; ++h) L->prep.push_back(make_int4(s, h, -1, 0));
+  L->off_prep = take(sizeof(int4) * L->prep.size());
+  L->off_rk_pairs = take(sizeof(int2) * std::max<size_t>(1, L->rk_pairs.size()));
   L->off_partials = take(sizeof(float) * (size_t)L->n_tiles * G * (D + 2));
   L->total = off;
   return MKV_OK;
@@ -287,8 +308,6 @@ struct mkv_cache {
   bool any_h2o = false, any_rocket = false, h2o_done = false, snap_done = false;
   int topk_max = 0;
   int h2o_rows = 0, rocket_rows = 0;
-  // independent kernels overlap on two library streams (default priority), forked from and joined
-  // into the caller's stream: [0] top-k and RocketKV attention, [1] uniform 4-bit attention
   // profiling
   bool evict_pending = false;  // H2O: the last eviction call's victims await the next decode append
   int prof_mask = 0;  // bit k: launches of kind k are timed
@@ -428,6 +447,10 @@ mkv_status mkv_cache_create(const mkv_shape *shape, const mkv_config *cfg, const
   c->dv.partials = reinterpret_cast<float *>(c->arena + L.off_partials);
   c->dv.cbtab = reinterpret_cast<const float *>(c->arena + L.off_cbtab);
   c->dv.n_tiles = L.n_tiles;
+  c->dv.prep = reinterpret_cast<const int4 *>(c->arena + L.off_prep);
+  c->dv.rk_pairs = reinterpret_cast<const int2 *>(c->arena + L.off_rk_pairs);
+  c->dv.n_prep = (int)L.prep.size();
+  c->dv.n_rk_pairs = (int)L.rk_pairs.size();
   c->dv.n_tiles_uq = L.n_tiles_uq;
   c->dv.n_tiles_rk = L.n_tiles_rk;
   hipStream_t hst = static_cast<hipStream_t>(stream);
@@ -435,6 +458,11 @@ mkv_status mkv_cache_create(const mkv_shape *shape, const mkv_config *cfg, const
                                 hipMemcpyHostToDevice, hst);
   if (e == hipSuccess)
     e = hipMemcpyAsync(c->arena + L.off_tiles, L.tiles.data(), sizeof(int4) * L.tiles.size(),
+                       hipMemcpyHostToDevice, hst);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(c->arena + L.off_prep, L.prep.data(), sizeof(int4) * L.prep.size(), hipMemcpyHostToDevice, hst);
+  if (e == hipSuccess && !L.rk_pairs.empty())
+    e = hipMemcpyAsync(c->arena + L.off_rk_pairs, L.rk_pairs.data(), sizeof(int2) * L.rk_pairs.size(),
                        hipMemcpyHostToDevice, hst);
   if (e == hipSuccess)
     e = hipMemcpyAsync(c->arena + L.off_cbtab, table, sizeof table, hipMemcpyHostToDevice, hst);
@@ -470,6 +498,18 @@ mkv_status decode_append(mkv_cache *c, const uint16_t *k, const uint16_t *v, hip
   c->evict_pending = false;
   c->steps++;
   c->phase = PH_APPENDED;
+  return MKV_OK;
+}
+
+// A decode step's append and top-k selection: the appends with the RocketKV scores, then the
+// selection (the caller has made every check of decode_append and mkv_topk_select).
+mkv_status decode_append_select(mkv_cache *c, const uint16_t *k, const uint16_t *v, const uint16_t *q,
+                                hipStream_t hst) {
+  hipError_t e = launch_append_select(c->dv, c->sh, k, v, q, hst, prof_ev(c, 4), prof_ev(c, 3));
+  if (e != hipSuccess) return hip_fail(e, "decode append and top-k select");
+  c->evict_pending = false;
+  c->steps++;
+  c->phase = PH_SELECTED;
   return MKV_OK;
 }
 
@@ -607,9 +647,10 @@ mkv_status mkv_decode_step(mkv_cache *c, const uint16_t *k, const uint16_t *v, c
     return fail(MKV_ESTATE, "decode step must follow prefill or a completed decode step");
   if (c->steps >= c->sh.max_new)
     return fail(MKV_ECAPACITY, "cache holds %d decode steps (max_new_tokens)", c->sh.max_new);
-  mkv_status st = decode_append(c, k, v, static_cast<hipStream_t>(stream));
+  // with RocketKV sequences present the append and the top-k share one launch
+  mkv_status st = c->any_rocket ? decode_append_select(c, k, v, q, static_cast<hipStream_t>(stream))
+                                : decode_append(c, k, v, static_cast<hipStream_t>(stream));
   if (st != MKV_OK) return st;
-  if ((st = mkv_topk_select(c, q, nullptr, stream)) != MKV_OK) return st;
   if ((st = mkv_decode_attention(c, q, out, stream)) != MKV_OK) return st;
   return mkv_h2o_update_evict(c, nullptr, stream);
 }

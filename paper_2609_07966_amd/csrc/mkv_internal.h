@@ -130,6 +130,9 @@ inline float round_to_half(double x) {
   return (float)(nearbyint(ldexp(x, -qexp)) * ldexp(1.0, qexp));
 }
 
+// Tokens one RocketKV scoring workgroup of a decode step covers.
+constexpr int kScoreTokensPerPart = 1024;
+
 // Kernel launchers (defined in the .hip files).  All enqueue on `st`.
 struct Dev {
   const SeqDesc *seqs;   // device [S]
@@ -140,6 +143,10 @@ struct Dev {
   int n_tiles;
   int n_tiles_uq;        // tiles of uniform 4-bit sequences (reported, not used by the launches)
   int n_tiles_rk;        // the last n_tiles_rk tiles belong to RocketKV sequences
+  const int4 *prep;      // device [n_prep]: a decode step's append / scoring work (seq, kv head,
+                         // part or -1 for a plain append, parts)
+  const int2 *rk_pairs;  // device [n_rk_pairs]: the RocketKV (seq, kv head) pairs
+  int n_prep, n_rk_pairs;
 };
 
 // Optional timing events of one launch: when set, they record the kernel's own start and end
@@ -163,6 +170,11 @@ hipError_t launch_attention_combine(const Dev &dv, const Shape &sh, float *out, 
                                     LaunchEv ev = {});
 hipError_t launch_topk(const Dev &dv, const Shape &sh, const uint16_t *q, int32_t *pos_out, int topk_max,
                        hipStream_t st, LaunchEv ev = {});
+// The decode append of every sequence and the RocketKV top-k in two launches (the appends and the
+// scores, spread over several workgroups per kv head; then the selection), with the effect of
+// launch_append_decode followed by launch_topk without positions.
+hipError_t launch_append_select(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
+                                const uint16_t *q, hipStream_t st, LaunchEv ev_score = {}, LaunchEv ev_select = {});
 hipError_t launch_h2o_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
                                   const uint16_t *q_rows, hipStream_t st);
 hipError_t launch_snap_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,

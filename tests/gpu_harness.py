@@ -72,12 +72,13 @@ def _keep_set_tie_ok(scores, gpu_keep, ora_keep, protected):
 class Run:
     """One GPU cache and its oracle twins for a workload."""
 
-    def __init__(self, wl, steps, tile_tokens=None, device="cuda"):
+    def __init__(self, wl, steps, tile_tokens=None, device="cuda", fused=False):
         import torch
         from paper_2609_07966_amd.cache import KVCache
         self.torch = torch
         self.wl = wl
         self.steps = steps
+        self.fused = fused  # one mkv_decode_step per step instead of the four separate calls
         S = wl.n_seqs
         self.cfgs = [wl.cfg(s) for s in range(S)]
         self.need_cb = any(c["method"] == "kvq" for c in self.cfgs)
@@ -202,10 +203,13 @@ class Run:
         kn, vn, q = step_inputs(wl, t)
         kd, vd, qd = self.h(kn), self.h(vn), self.h(q)
         out = torch.empty((wl.n_seqs, wl.n_q_heads, wl.head_dim), dtype=torch.float32, device=self.dev)
-        cache.append(kd, vd)
-        cache.topk(qd)
-        cache.attention(qd, out)
-        cache.evict()
+        if self.fused:
+            cache.step(kd, vd, qd, out)
+        else:
+            cache.append(kd, vd)
+            cache.topk(qd)
+            cache.attention(qd, out)
+            cache.evict()
         gout = out.cpu().numpy()
         G = wl.group
         for s, seq in enumerate(self.oracle):

@@ -18,6 +18,7 @@ hipError_t launch_prefill_seq(const Dev &, const Shape &, const SeqDesc &, int, 
 hipError_t launch_attention_partial(const Dev &, const Shape &, const uint16_t *, hipStream_t, LaunchEv) { return hipErrorNotSupported; }
 hipError_t launch_attention_combine(const Dev &, const Shape &, float *, hipStream_t, LaunchEv) { return hipErrorNotSupported; }
 hipError_t launch_topk(const Dev &, const Shape &, const uint16_t *, int32_t *, int, hipStream_t, LaunchEv) { return hipErrorNotSupported; }
+hipError_t launch_append_select(const Dev &, const Shape &, const uint16_t *, const uint16_t *, const uint16_t *, hipStream_t, LaunchEv, LaunchEv) { return hipErrorNotSupported; }
 hipError_t launch_h2o_prefill_seq(const Dev &, const Shape &, const SeqDesc &, int, const uint16_t *, hipStream_t) { return hipErrorNotSupported; }
 hipError_t launch_snap_prefill_seq(const Dev &, const Shape &, const SeqDesc &, int, const uint16_t *, hipStream_t) { return hipErrorNotSupported; }
 hipError_t launch_init_state(const Dev &, const Shape &, hipStream_t) { return hipErrorNotSupported; }

@@ -10,11 +10,13 @@ from workloads import make_workload
 pytestmark = pytest.mark.gpu
 
 
-def _run(wl, steps, check_codes=True):
+def _run(wl, steps, check_codes=True, fused=False):
+    """fused: drive the cache by mkv_decode_step (append and top-k in one launch) instead of the
+    separate calls."""
     from gpu_harness import Run, log
     log(f"[parity] {wl.name} S={wl.n_seqs} Hq={wl.n_q_heads} Hkv={wl.n_kv_heads} d={wl.head_dim} "
-        f"prompts={wl.prompt_lens} cfgs={wl.config_ids} steps={steps}")
-    r = Run(wl, steps).run(check_codes=check_codes)
+        f"prompts={wl.prompt_lens} cfgs={wl.config_ids} steps={steps} fused={fused}")
+    r = Run(wl, steps, fused=fused).run(check_codes=check_codes)
     log(f"[parity]   max normalised error {r.max_err:.2e}, near-ties adopted {r.near_ties}")
     return r
 
@@ -62,10 +64,25 @@ def test_h2o_evictions():
     _run(wl, 40)
 
 
-def test_rocket_prefill_and_topk():
+@pytest.mark.parametrize("fused", [False, True])
+def test_rocket_prefill_and_topk(fused):
     wl = make_workload("custom", seed=7, n_seqs=2, n_q_heads=32, n_kv_heads=8, head_dim=128,
                        prompt_lens=[3000, 2100], steps=10, config_ids=["Rocket-1024", "Rocket-2048"])
-    _run(wl, 10)
+    _run(wl, 10, fused=fused)
+
+
+def test_rocket_large_retained_sets():
+    # retained sets past 4 x 1024 tokens (a lane scores 8 tokens) and past the 10240 score keys
+    # the top-k holds in LDS (keys in the global scratch), through the fused append and top-k
+    wl = make_workload("custom", seed=18, n_seqs=2, n_q_heads=4, n_kv_heads=1, head_dim=64,
+                       prompt_lens=[12000, 6000], steps=4, config_ids=[0, 0])
+    wl.config_ids = [8, 8]
+    cfgs = [{"id": 8, "name": "Rocket-11000", "method": "rocket", "keep_tokens": 11000, "window": 32, "pool": 7,
+             "topk": 0, "n_channels": 16},
+            {"id": 8, "name": "Rocket-5000", "method": "rocket", "keep_tokens": 5000, "window": 32, "pool": 7,
+             "topk": 0, "n_channels": 32}]
+    wl.cfg = lambda s: dict(cfgs[s])
+    _run(wl, 4, fused=True)
 
 
 def test_mixed_batch_every_config():
@@ -73,7 +90,7 @@ def test_mixed_batch_every_config():
     lens = [int(x) for x in np.rint(np.exp(r.uniform(np.log(200), np.log(3000), 11)))]
     wl = make_workload("custom", seed=8, n_seqs=11, n_q_heads=32, n_kv_heads=8, head_dim=128,
                        prompt_lens=lens, steps=6, config_ids=list(range(11)))
-    _run(wl, 6)
+    _run(wl, 6, fused=True)
 
 
 @pytest.mark.parametrize("hq,hkv,d", [(32, 4, 64), (8, 8, 128), (16, 8, 64)])
@@ -81,7 +98,7 @@ def test_mixed_other_head_shapes(hq, hkv, d):
     wl = make_workload("custom", seed=9, n_seqs=6, n_q_heads=hq, n_kv_heads=hkv, head_dim=d,
                        prompt_lens=[700, 1300, 257, 900, 2050, 600], steps=5,
                        config_ids=["FP16", "KVQ3", "UQ4-g64", "H2O-20", "Rocket-1024", "KVQ2"])
-    _run(wl, 5)
+    _run(wl, 5, fused=True)
 
 
 def test_edge_cases():
@@ -97,7 +114,7 @@ def test_edge_cases():
              "topk": 4096, "n_channels": 32},
             {"id": 5, "name": "H2O-dense", "method": "h2o", "budget_pct": 1000}]
     wl.cfg = lambda s: dict(cfgs[s])
-    _run(wl, 12)
+    _run(wl, 12, fused=True)
 
 
 def test_kvquant_without_outliers():
@@ -137,7 +154,7 @@ def test_small_budgets_and_selections():
             {"id": 8, "name": "Rocket-top8", "method": "rocket", "keep_tokens": 64, "window": 32, "pool": 7,
              "topk": 8, "n_channels": 32}]
     wl.cfg = lambda s: dict(cfgs[s])
-    _run(wl, 12)
+    _run(wl, 12, fused=True)
 
 
 def test_tiny_prompts_quantized():
@@ -157,7 +174,7 @@ def test_paper_grid_settings():
                        prompt_lens=[900, 1300, 3000, 2500, 4100], steps=6,
                        config_ids=["H2O-40", "H2O-60", "Rocket-8x", "Rocket-16x", "Rocket-32x"],
                        boost_frac=0.05, boost=3.0)
-    _run(wl, 6)
+    _run(wl, 6, fused=True)
 
 
 @pytest.mark.parametrize("hq,n0", [(4, 13001), (8, 7001)])
