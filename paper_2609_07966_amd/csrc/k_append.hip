@@ -241,7 +241,38 @@ struct AppendLds {
   int tmp[4];
   uint32_t blk[D / 2];
   float cbt[kCbTableFloats];  // codebooks and midpoints, read many times below
+  unsigned long long vkey[D / 64];
+  int vslot;
 };
+
+// H2O: the slot the last attention pass chose for eviction (-1: none), the lowest (score,
+// position) key among its per-part candidates; threads 0..D-1, every one gets the result.
+template <int D>
+MKV_DEV int h2o_victim(const SeqDesc &sd, int h, AppendLds<D> &L) {
+  const int c = threadIdx.x, lane = c & 63, w = c >> 6;
+  const uint32_t *vb = reinterpret_cast<const uint32_t *>(sd.vbest) + (size_t)h * sd.vparts * 4;
+  unsigned long long best = ~0ull;
+  int bslot = -1;
+  for (int p = c; p < sd.vparts; p += D) {
+    const uint4 e = gld16(vb + 4 * p);
+    const unsigned long long key = (unsigned long long)e.x | ((unsigned long long)e.y << 32);
+    if (key < best) {
+      best = key;
+      bslot = (int)e.z;
+    }
+  }
+  const unsigned long long wm = wave_min_u64(best);
+  if (lane == 0) L.vkey[w] = wm;
+  __syncthreads();
+  unsigned long long all = L.vkey[0];
+#pragma unroll
+  for (int i = 1; i < D / 64; ++i) all = L.vkey[i] < all ? L.vkey[i] : all;
+  // keys carry the position, so at most one thread holds the lowest
+  if (all != ~0ull && best == all) L.vslot = bslot;
+  if (c == 0 && all == ~0ull) L.vslot = -1;
+  __syncthreads();
+  return L.vslot;
+}
 
 // Append the new token of (seq, h) by threads 0..D-1 of the workgroup (every barrier below is
 // reached by exactly those threads).
@@ -256,7 +287,7 @@ MKV_DEV void append_pair(const SeqDesc &sd, int32_t *st, int seq, int h, int Hkv
   for (int i = c; i < kCbTableFloats; i += D) s_cbt[i] = cbtab[i];
   const int count = st[ST_COUNT], pos = st[ST_NEXT_POS];
   // H2O: an eviction decided by the last attention pass frees its slot for this token (-1: none)
-  const int victim = sd.method == H2O ? st[ST_VICTIM] : -1;
+  const int victim = sd.method == H2O ? h2o_victim<D>(sd, h, L) : -1;
   const int slot = sd.method == H2O ? (victim >= 0 ? victim : st[ST_FREE_SLOT]) : count;
   // a full region (reachable only by replaying a captured decode step past max_new_tokens) drops
   // the token instead of writing past the region; the decision is the same for every thread
@@ -282,7 +313,6 @@ MKV_DEV void append_pair(const SeqDesc &sd, int32_t *st, int seq, int h, int Hkv
         (reinterpret_cast<float *>(sd.score) + h * stride_slots(sd))[slot] = 0.f;
         st[ST_COUNT] = new_count;
         st[ST_FREE_SLOT] = new_count;
-        st[ST_VICTIM] = -1;
       }
       break;
     }
@@ -615,7 +645,6 @@ __global__ void k_prefill_state(const SeqDesc *__restrict__ seqs, int seq, int32
   st[ST_NEXT_POS] = sd.n0;
   st[ST_FREE_SLOT] = 0;
   st[ST_KEPT] = sd.n0;
-  st[ST_VICTIM] = -1;
 }
 
 __global__ void k_init_state(int32_t *state, int n) {

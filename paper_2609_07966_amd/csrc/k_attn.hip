@@ -1002,39 +1002,47 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   merge_waves<D, G, NW>(&s_wave[0][0], kWaveFloats, partials + (size_t)tid * G * (D + 2));
 }
 
-// Log-sum-exp merge of one (sequence, kv head)'s tiles; H2O also adds every query head's
-// probability to each retained token's accumulated score and picks the eviction victim.  One
-// workgroup of 512 threads per pair: a wave per query head reduces the tile maxima and sums while
-// every thread's output values of all tiles and an H2O pair's slot data (logits, score, position)
-// are already in flight, so the merge waits for one round of loads.
+// Log-sum-exp merge of one (sequence, kv head)'s tiles, and for H2O the score accumulation and the
+// eviction candidates, over a work list (int4: seq, kv head, part, parts).  Part 0 merges the
+// output.  An H2O kv head has one part per kCombineSlots slots: each adds every query head's
+// probability to the accumulated score of its slots and writes its own eviction candidate, the
+// lowest (score, position) key among the positions older than the R most recent (none while the
+// head is within its budget); the next decode append takes the lowest candidate's slot.  512
+// threads: a wave per query head reduces the tile maxima and sums while every thread's output
+// values and slot data are already in flight, so a part waits for one round of loads.
 constexpr int kMaxTilesPerPair = 64;
 constexpr int kCombineThreads = 512;
 
 template <int D, int G>
 __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc *__restrict__ seqs,
-                                                                  int32_t *__restrict__ state,
+                                                                  const int32_t *__restrict__ state,
+                                                                  const int4 *__restrict__ items,
                                                                   const float *__restrict__ partials,
                                                                   float *__restrict__ out, int Hkv) {
   constexpr int NWC = kCombineThreads / 64;
   static_assert(G <= NWC, "a wave per query head");
   constexpr int kChunk = 32;  // tiles whose output loads a thread issues together
-  constexpr int kU = G >= 8 ? 6 : 12;  // H2O slots per thread and round (G <= 4: 6144 slots per round)
+  constexpr int kU = kCombineSlots / kCombineThreads;  // H2O slots per thread
+  static_assert(kU * kCombineThreads == kCombineSlots, "whole slots per thread");
   __shared__ float sW[kMaxTilesPerPair][G];  // tile weights 2^(m_t - M) / L
   __shared__ float sM[G], sL[G];
   __shared__ unsigned long long s_best[NWC];
-  const int seq = blockIdx.x / Hkv, h = blockIdx.x % Hkv;
+  __shared__ int s_bslot[NWC];
+  const int4 it = items[blockIdx.x];
+  const int seq = it.x, h = it.y, part = it.z;
   const SeqDesc &sd = seqs[seq];
   const int first = sd.tile_first + h * sd.tile_count, nt = sd.tile_count;
   const float *P = partials + (size_t)first * G * (D + 2);
   const int wv = threadIdx.x >> 6, ln = threadIdx.x & 63;
+  const bool merge = part == 0;
   const bool h2o = sd.method == H2O;
-  int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
+  const int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
   const float *lg = reinterpret_cast<const float *>(sd.logits) + h * stride_logits(sd, G);
   float *score = reinterpret_cast<float *>(sd.score) + h * stride_slots(sd);
   const int32_t *pos = reinterpret_cast<const int32_t *>(sd.pos) + h * stride_slots(sd);
   // loads in the order they are needed: tile maxima and sums (wave g, lane t: tile t, nt <= 64),
-  // the output values of the first kChunk tiles, then an H2O pair's first round of slot data
-  // (every slot below the capacity is allocated, so these need not wait for the count)
+  // part 0's output values of the first kChunk tiles, then an H2O part's slot data (every slot
+  // below the capacity is allocated, so these need not wait for the count)
   float tm = -INFINITY, tl = 0.f;
   if (wv < G && ln < nt) {
     tm = P[((size_t)ln * G + wv) * (D + 2)];
@@ -1042,14 +1050,17 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
   }
   constexpr int kE = (G * D + kCombineThreads - 1) / kCombineThreads;  // output elements per thread
   float o0[kE][kChunk];
+  if (merge) {
 #pragma unroll
-  for (int i = 0; i < kE; ++i) {
-    const int e = min((int)threadIdx.x + i * kCombineThreads, G * D - 1);
-    const float *po = P + (size_t)(e / D) * (D + 2) + 2 + e % D;
+    for (int i = 0; i < kE; ++i) {
+      const int e = min((int)threadIdx.x + i * kCombineThreads, G * D - 1);
+      const float *po = P + (size_t)(e / D) * (D + 2) + 2 + e % D;
 #pragma unroll
-    for (int u = 0; u < kChunk; ++u) o0[i][u] = po[(size_t)min(u, nt - 1) * G * (D + 2)];
+      for (int u = 0; u < kChunk; ++u) o0[i][u] = po[(size_t)min(u, nt - 1) * G * (D + 2)];
+    }
   }
   int count = 0, limit = 0;
+  const int j0 = part * kCombineSlots + (int)threadIdx.x;
   float lgv[kU][G], scv[kU];
   int pv[kU];
   if (h2o) {
@@ -1057,7 +1068,7 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
     limit = st[ST_NEXT_POS] - 1 - sd.R + 1;
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
-      const int j = min((int)threadIdx.x + u * kCombineThreads, sd.cap - 1);
+      const int j = min(j0 + u * kCombineThreads, sd.cap - 1);
 #pragma unroll
       for (int g = 0; g < G; ++g) lgv[u][g] = gld(lg + (size_t)j * G + g);
       scv[u] = gld(score + j);
@@ -1074,33 +1085,31 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
     }
   }
   __syncthreads();
-  const int Hq = Hkv * G;
+  if (merge) {
+    const int Hq = Hkv * G;
 #pragma unroll
-  for (int i = 0; i < kE; ++i) {
-    const int e = (int)threadIdx.x + i * kCombineThreads;
-    if (e < G * D) {
-      const int g = e / D, c = e % D;
-      float acc = 0.f;
-#pragma unroll
-      for (int u = 0; u < kChunk; ++u)
-        if (u < nt) acc = fmaf(o0[i][u], sW[u][g], acc);
-      const float *po = P + (size_t)g * (D + 2) + 2 + c;
-      for (int t0 = kChunk; t0 < nt; t0 += kChunk) {  // more than kChunk tiles
-        float o[kChunk];
-#pragma unroll
-        for (int u = 0; u < kChunk; ++u) o[u] = po[(size_t)min(t0 + u, nt - 1) * G * (D + 2)];
+    for (int i = 0; i < kE; ++i) {
+      const int e = (int)threadIdx.x + i * kCombineThreads;
+      if (e < G * D) {
+        const int g = e / D, c = e % D;
+        float acc = 0.f;
 #pragma unroll
         for (int u = 0; u < kChunk; ++u)
-          if (t0 + u < nt) acc = fmaf(o[u], sW[t0 + u][g], acc);
+          if (u < nt) acc = fmaf(o0[i][u], sW[u][g], acc);
+        const float *po = P + (size_t)g * (D + 2) + 2 + c;
+        for (int t0 = kChunk; t0 < nt; t0 += kChunk) {  // more than kChunk tiles
+          float o[kChunk];
+#pragma unroll
+          for (int u = 0; u < kChunk; ++u) o[u] = po[(size_t)min(t0 + u, nt - 1) * G * (D + 2)];
+#pragma unroll
+          for (int u = 0; u < kChunk; ++u)
+            if (t0 + u < nt) acc = fmaf(o[u], sW[t0 + u][g], acc);
+        }
+        out[((size_t)seq * Hq + h * G + g) * D + c] = acc;
       }
-      out[((size_t)seq * Hq + h * G + g) * D + c] = acc;
     }
   }
   if (h2o) {
-    // accumulate, and find the eviction candidate (lowest score among positions older than the
-    // R most recent, lower position on a tie); the next decode append writes its token there
-    // (no victim unless one is found below: the barrier of the search orders this write first)
-    if (threadIdx.x == 0) st[ST_VICTIM] = -1;
     float invL[G], M[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -1109,40 +1118,39 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(const SeqDesc 
     }
     unsigned long long best = ~0ull;
     int best_slot = -1;
-    for (int j0 = threadIdx.x; j0 < count; j0 += kU * kCombineThreads) {
-      if (j0 != (int)threadIdx.x) {  // rounds after the first (more than 6144 slots)
 #pragma unroll
-        for (int u = 0; u < kU; ++u) {
-          const int j = min(j0 + u * kCombineThreads, count - 1);
+    for (int u = 0; u < kU; ++u) {
+      const int j = j0 + u * kCombineThreads;
+      float acc = 0.f;
 #pragma unroll
-          for (int g = 0; g < G; ++g) lgv[u][g] = gld(lg + (size_t)j * G + g);
-          scv[u] = gld(score + j);
-          pv[u] = gld(pos + j);
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kU; ++u) {
-        const int j = j0 + u * kCombineThreads;
-        float acc = 0.f;
-#pragma unroll
-        for (int g = 0; g < G; ++g) acc += fexp2(lgv[u][g] - M[g]) * invL[g];  // arguments <= 0
-        const float sc = scv[u] + acc;
-        if (j < count) gst(score + j, sc);
-        const unsigned long long key =
-            ((unsigned long long)__builtin_bit_cast(uint32_t, sc) << 32) | (unsigned long long)(uint32_t)pv[u];
-        if (j < count && pv[u] < limit && key < best) {
-          best = key;
-          best_slot = j;
-        }
+      for (int g = 0; g < G; ++g) acc += fexp2(lgv[u][g] - M[g]) * invL[g];  // arguments <= 0
+      const float sc = scv[u] + acc;
+      if (j < count) gst(score + j, sc);
+      const unsigned long long key =
+          ((unsigned long long)__builtin_bit_cast(uint32_t, sc) << 32) | (unsigned long long)(uint32_t)pv[u];
+      if (j < count && pv[u] < limit && key < best) {
+        best = key;
+        best_slot = j;
       }
     }
-    if (count > sd.B) {
-      const unsigned long long wb = wave_min_u64(best);
-      if (ln == 0) s_best[wv] = wb;
-      __syncthreads();
-      unsigned long long all = s_best[0];
-      for (int w = 1; w < NWC; ++w) all = s_best[w] < all ? s_best[w] : all;
-      if (best_slot >= 0 && best == all) st[ST_VICTIM] = best_slot;
+    if (count <= sd.B) best = ~0ull;  // within the budget: no eviction
+    const unsigned long long wb = wave_min_u64(best);
+    if (ln == 0) s_best[wv] = wb;
+    if (wb != ~0ull && best == wb) s_bslot[wv] = best_slot;  // keys carry the position: one lane
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      unsigned long long all = ~0ull;
+      int slot = -1;
+      for (int w = 0; w < NWC; ++w)
+        if (s_best[w] < all) {
+          all = s_best[w];
+          slot = s_bslot[w];
+        }
+      uint32_t *vb = reinterpret_cast<uint32_t *>(sd.vbest) + ((size_t)h * sd.vparts + part) * 4;
+      gst(vb, (uint32_t)all);
+      gst(vb + 1, (uint32_t)(all >> 32));
+      gst(vb + 2, (uint32_t)slot);
+      gst(vb + 3, 0u);
     }
   }
 }
@@ -1158,8 +1166,8 @@ hipError_t partial_impl(const Dev &dv, const Shape &sh, const uint16_t *q, hipSt
 
 template <int D, int G>
 hipError_t combine_impl(const Dev &dv, const Shape &sh, float *out, hipStream_t st, LaunchEv ev) {
-  hipExtLaunchKernelGGL((k_attn_combine<D, G>), dim3(sh.S * sh.Hkv), dim3(kCombineThreads), 0, st, ev.start,
-                        ev.stop, 0, dv.seqs, dv.state, dv.partials, out, sh.Hkv);
+  hipExtLaunchKernelGGL((k_attn_combine<D, G>), dim3(dv.n_comb), dim3(kCombineThreads), 0, st, ev.start,
+                        ev.stop, 0, dv.seqs, dv.state, dv.comb, dv.partials, out, sh.Hkv);
   return hipGetLastError();
 }
 

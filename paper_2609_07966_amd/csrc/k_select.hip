@@ -292,6 +292,14 @@ __global__ __launch_bounds__(NT) void k_h2o_keep(const SeqDesc *__restrict__ seq
         }
       },
       s_tmp);
+  // no eviction candidates before the first attention pass
+  uint32_t *vb = reinterpret_cast<uint32_t *>(sd.vbest) + (size_t)h * sd.vparts * 4;
+  for (int p = threadIdx.x; p < sd.vparts; p += NT) {
+    vb[4 * p] = 0xFFFFFFFFu;
+    vb[4 * p + 1] = 0xFFFFFFFFu;
+    vb[4 * p + 2] = 0xFFFFFFFFu;
+    vb[4 * p + 3] = 0u;
+  }
   if (threadIdx.x == 0) {
     int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
     st[ST_COUNT] = kept;

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstddef>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -48,14 +49,26 @@ constexpr int kProfKinds = 5;
 struct Layout {
   std::vector<SeqDesc> seqs;  // offsets (relative to the arena) in the pointer fields
   size_t off_seqs = 0, off_state = 0, off_tiles = 0, off_cbtab = 0, off_partials = 0, total = 0;
-  size_t off_prep = 0, off_rk_pairs = 0;
+  size_t off_prep = 0, off_rk_pairs = 0, off_comb = 0;
   int n_tiles = 0, n_tiles_uq = 0, n_tiles_rk = 0;
   std::vector<int4> tiles;
   std::vector<int4> prep;      // decode-step append / scoring work list
   std::vector<int2> rk_pairs;  // RocketKV (seq, kv head) pairs
+  std::vector<int4> comb;      // combine work list
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Every region pointer of a descriptor (arena offsets in the layout, device addresses once the
+// arena is known); the descriptor is its integer fields followed by exactly these.
+constexpr uint64_t SeqDesc::*kRegionFields[] = {
+    &SeqDesc::k,      &SeqDesc::v,      &SeqDesc::kc,      &SeqDesc::vc,      &SeqDesc::kmeta, &SeqDesc::vmeta,
+    &SeqDesc::kres,   &SeqDesc::krow,   &SeqDesc::kout,    &SeqDesc::vout,    &SeqDesc::vdel,  &SeqDesc::pos,
+    &SeqDesc::score,  &SeqDesc::logits, &SeqDesc::vbest,   &SeqDesc::stage_k, &SeqDesc::stage_v,
+    &SeqDesc::kcm,    &SeqDesc::sel,    &SeqDesc::akeys,   &SeqDesc::aux0,    &SeqDesc::aux1};
+static_assert(offsetof(SeqDesc, k) + sizeof(kRegionFields) / sizeof(kRegionFields[0]) * sizeof(uint64_t) ==
+                  sizeof(SeqDesc),
+              "every region pointer of SeqDesc is relocated");
 
 constexpr int kMaxTiles = 32;  // per (sequence, kv head); the combine kernel holds up to 64
 
@@ -204,6 +217,8 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
         d.pos = take(H * d.cap * 4);
         d.score = take(H * d.cap * 4);
         d.logits = take(H * d.cap * G * 4);
+        d.vparts = (d.cap + kCombineSlots - 1) / kCombineSlots;
+        d.vbest = take(H * d.vparts * 16);
         d.stage_k = take(H * n0 * D * 2);
         d.stage_v = take(H * n0 * D * 2);
         d.aux0 = take(H * n0 * 4);
@@ -288,6 +303,17 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
     if (L->seqs[s].method != ROCKET)
       for (int h = 0; h < Hkv; ++h) L->prep.push_back(make_int4(s, h, -1, 0));
   L->off_prep = take(sizeof(int4) * L->prep.size());
+  // the combine: H2O kv heads' parts (one per kCombineSlots slots) first, then one item per pair
+  L->comb.clear();
+  for (int pass = 0; pass < 2; ++pass)
+    for (int s = 0; s < S; ++s) {
+      const SeqDesc &d = L->seqs[s];
+      if ((d.method == H2O) != (pass == 0)) continue;
+      const int parts = d.method == H2O ? d.vparts : 1;
+      for (int h = 0; h < Hkv; ++h)
+        for (int p = 0; p < parts; ++p) L->comb.push_back(make_int4(s, h, p, parts));
+    }
+  L->off_comb = take(sizeof(int4) * L->comb.size());
   L->off_rk_pairs = take(sizeof(int2) * std::max<size_t>(1, L->rk_pairs.size()));
   L->off_partials = take(sizeof(float) * (size_t)L->n_tiles * G * (D + 2));
   L->total = off;
@@ -425,12 +451,9 @@ mkv_status mkv_cache_create(const mkv_shape *shape, const mkv_config *cfg, const
   const uint64_t base = (uint64_t)(uintptr_t)arena;
   c->hs = L.seqs;
   for (auto &d : c->hs) {
-    uint64_t *ptrs[] = {&d.k, &d.v, &d.kc, &d.vc, &d.kmeta, &d.vmeta, &d.kres, &d.krow, &d.kout, &d.vout, &d.vdel,
-                        &d.pos, &d.score, &d.logits, &d.stage_k, &d.stage_v, &d.kcm, &d.sel, &d.akeys,
-                        &d.aux0, &d.aux1};
     // offset 0 holds the descriptor table, so a zero offset marks a region the method lacks
-    for (uint64_t *p : ptrs)
-      if (*p) *p += base;
+    for (uint64_t SeqDesc::*f : kRegionFields)
+      if (d.*f) d.*f += base;
     if (d.method == H2O) {
       c->any_h2o = true;
       c->h2o_rows += d.n0;
@@ -450,6 +473,8 @@ mkv_status mkv_cache_create(const mkv_shape *shape, const mkv_config *cfg, const
   c->dv.prep = reinterpret_cast<const int4 *>(c->arena + L.off_prep);
   c->dv.rk_pairs = reinterpret_cast<const int2 *>(c->arena + L.off_rk_pairs);
   c->dv.n_prep = (int)L.prep.size();
+  c->dv.comb = reinterpret_cast<const int4 *>(c->arena + L.off_comb);
+  c->dv.n_comb = (int)L.comb.size();
   c->dv.n_rk_pairs = (int)L.rk_pairs.size();
   c->dv.n_tiles_uq = L.n_tiles_uq;
   c->dv.n_tiles_rk = L.n_tiles_rk;
@@ -461,6 +486,8 @@ mkv_status mkv_cache_create(const mkv_shape *shape, const mkv_config *cfg, const
                        hipMemcpyHostToDevice, hst);
   if (e == hipSuccess)
     e = hipMemcpyAsync(c->arena + L.off_prep, L.prep.data(), sizeof(int4) * L.prep.size(), hipMemcpyHostToDevice, hst);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(c->arena + L.off_comb, L.comb.data(), sizeof(int4) * L.comb.size(), hipMemcpyHostToDevice, hst);
   if (e == hipSuccess && !L.rk_pairs.empty())
     e = hipMemcpyAsync(c->arena + L.off_rk_pairs, L.rk_pairs.data(), sizeof(int2) * L.rk_pairs.size(),
                        hipMemcpyHostToDevice, hst);
@@ -822,8 +849,21 @@ extern "C" mkv_status mkv_export(mkv_cache *c, int32_t seq, int32_t h, int32_t w
   mkv_status st = dget(stv, (uint64_t)(uintptr_t)(c->dv.state + ((size_t)seq * c->sh.Hkv + h) * ST_WORDS), ST_WORDS);
   if (st != MKV_OK) return st;
   const int count = stv[ST_COUNT];
-  // H2O: a victim whose eviction is pending is no longer part of the retained set
-  const int gone = (d.method == H2O && c->evict_pending) ? stv[ST_VICTIM] : -1;
+  // H2O: a victim whose eviction is pending is no longer part of the retained set (the lowest key
+  // among the last attention pass's per-part candidates)
+  int gone = -1;
+  if (d.method == H2O && c->evict_pending) {
+    std::vector<uint32_t> vb;
+    if ((st = dget(vb, d.vbest + (uint64_t)h * d.vparts * 16, (size_t)d.vparts * 4)) != MKV_OK) return st;
+    unsigned long long best = ~0ull;
+    for (int p = 0; p < d.vparts; ++p) {
+      const unsigned long long key = (unsigned long long)vb[4 * p] | ((unsigned long long)vb[4 * p + 1] << 32);
+      if (key < best) {
+        best = key;
+        gone = (int)vb[4 * p + 2];
+      }
+    }
+  }
   std::vector<uint8_t> out;
   auto put = [&](const void *p, size_t bytes) {
     const uint8_t *b = static_cast<const uint8_t *>(p);

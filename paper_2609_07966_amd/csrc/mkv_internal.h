@@ -24,8 +24,6 @@ enum StateWord : int32_t {
   ST_KOUT_FILL = 3,  // KVQ: entries used in the key-outlier pool
   ST_SEL_COUNT = 4,  // ROCKET: tokens selected by the last top-k
   ST_KEPT = 5,       // tokens kept after prefill (H2O / ROCKET), prompt length otherwise
-  ST_VICTIM = 6,     // H2O: slot chosen for eviction by the last attention pass (-1: none); the
-                     // eviction takes effect when the next decode append reuses the slot
   ST_WORDS = 8
 };
 
@@ -52,6 +50,7 @@ struct SeqDesc {
   int32_t pool_cap, nblk, w_eff, chunk;   // KVQ outlier pool; UQ blocks; window rows; tile tokens
   int32_t tile_first, tile_count, q_off, cstride;  // partial tiles (per kv head); prompt-q row offset;
                                                    // ROCKET channel-major row stride (cap rounded to 8)
+  int32_t vparts, spare0, spare1, spare2;  // H2O: eviction candidates per kv head (one per combine part)
   uint64_t k, v;            // fp16 [cap][d] rows (FP16 / H2O / ROCKET)
   uint64_t kc, vc;          // packed codes [cap][rowbytes] (UQ / KVQ)
   uint64_t kmeta, vmeta;    // UQ: float2 [nblk][d], float2 [cap][d/64]; KVQ: float2 tau/inv [d], float [cap]
@@ -60,6 +59,8 @@ struct SeqDesc {
   uint64_t vdel;            // KVQ: u32 [nov_slots][cap] value-outlier differences for the attention
   uint64_t pos, score;      // H2O / ROCKET: int32 [cap], float [cap]
   uint64_t logits;          // H2O: float [cap][G] log2-domain logits of the last attention
+  uint64_t vbest;           // H2O: [vparts] eviction candidates of the last attention pass, 16 bytes
+                            // each: u64 key (score bits << 32 | position; ~0 = none), int32 slot
   uint64_t stage_k, stage_v;// H2O / ROCKET: fp16 [n0][d] prompt staging
   uint64_t kcm;             // ROCKET: fp16 [d][cap] channel-major keys
   uint64_t sel, akeys;      // ROCKET: int32 [topk] selected slots; u32 [cap] score keys
@@ -132,6 +133,8 @@ inline float round_to_half(double x) {
 
 // Tokens one RocketKV scoring workgroup of a decode step covers.
 constexpr int kScoreTokensPerPart = 1024;
+// H2O slots one combine workgroup scores (an H2O kv head has ceil(cap / kCombineSlots) parts).
+constexpr int kCombineSlots = 2048;
 
 // Kernel launchers (defined in the .hip files).  All enqueue on `st`.
 struct Dev {
@@ -146,7 +149,8 @@ struct Dev {
   const int4 *prep;      // device [n_prep]: a decode step's append / scoring work (seq, kv head,
                          // part or -1 for a plain append, parts)
   const int2 *rk_pairs;  // device [n_rk_pairs]: the RocketKV (seq, kv head) pairs
-  int n_prep, n_rk_pairs;
+  const int4 *comb;      // device [n_comb]: combine work (seq, kv head, part, parts)
+  int n_prep, n_rk_pairs, n_comb;
 };
 
 // Optional timing events of one launch: when set, they record the kernel's own start and end
@@ -155,7 +159,7 @@ struct LaunchEv {
   hipEvent_t start = nullptr, stop = nullptr;
 };
 
-// H2O pairs whose last attention pass chose a victim (ST_VICTIM >= 0) write the token into its slot.
+// H2O pairs whose last attention pass chose a victim write the token into its slot.
 hipError_t launch_append_decode(const Dev &dv, const Shape &sh, const uint16_t *k, const uint16_t *v,
                                 hipStream_t st, LaunchEv ev = {});
 hipError_t launch_prefill_seq(const Dev &dv, const Shape &sh, const SeqDesc &hs, int seq,
