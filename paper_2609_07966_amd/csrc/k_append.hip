@@ -528,38 +528,72 @@ __global__ __launch_bounds__(128) void k_prefill_uq_keys(const SeqDesc *__restri
   }
 }
 
-// KVQ key thresholds: thread c finds the n_o-th largest |k| (0-based) of channel c over the prompt
-// by a two-pass radix select on the 15-bit fp16 magnitude, with a private 256-bin histogram.
+// KVQ key thresholds: the n_o-th largest |k| (0-based) of every channel over the prompt, by a
+// two-pass radix select on the 15-bit fp16 magnitude.  A workgroup takes 64 channels of one kv
+// head: lane l of every wave owns channel c0 + l (one coalesced 128-byte load per token), the 8
+// waves take every eighth token, kCalibBatch tokens' loads in flight at a time, and count into
+// one 256-bin histogram per channel by LDS atomics (rows padded so that the lanes' bins spread
+// over the banks); thread c < 64 then finds its channel's digit.
+constexpr int kCalibThreads = 512;
+constexpr int kCalibBatch = 16;
 template <int D>
-__global__ __launch_bounds__(128) void k_kvq_calibrate(const SeqDesc *__restrict__ seqs, int seq,
-                                                      const uint16_t *__restrict__ k, int Hkv, int n0) {
-  __shared__ uint16_t hist[D][256];
+__global__ __launch_bounds__(kCalibThreads) void k_kvq_calibrate(const SeqDesc *__restrict__ seqs, int seq,
+                                                                 const uint16_t *__restrict__ k, int Hkv, int n0) {
+  __shared__ uint32_t hist[64][257];
+  __shared__ uint32_t s_sel[64], s_rem[64];
   const SeqDesc &sd = seqs[seq];
-  const int h = blockIdx.x, c = threadIdx.x;
-  const int want = sd.bp > 0 ? sd.n_o : 0;   // 0-based rank from the top
-  float tau = 0.f;
-  if (want < n0) {
-    uint32_t hi_sel = 0;
-    int remaining = want + 1;   // 1-based rank
-    for (int pass = 0; pass < 2; ++pass) {
-      for (int b = 0; b < 256; ++b) hist[c][b] = 0;
-      for (int t = 0; t < n0; ++t) {
-        const uint32_t key = k[((size_t)t * Hkv + h) * D + c] & 0x7FFFu;
-        if (pass == 0) hist[c][key >> 8]++;
-        else if ((key >> 8) == hi_sel) hist[c][key & 255u]++;
-      }
-      int cum = 0, dg = 0;
-      for (int b = 255; b >= 0; --b) {
-        if (cum + hist[c][b] >= remaining) { dg = b; break; }
-        cum += hist[c][b];
-      }
-      remaining -= cum;
-      if (pass == 0) hi_sel = (uint32_t)dg;
-      else tau = h2f((hi_sel << 8) | (uint32_t)dg);
-    }
+  const int h = blockIdx.x, c0 = 64 * blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int NW = kCalibThreads / 64;
+  const int want = sd.bp > 0 ? sd.n_o : 0;  // 0-based rank from the top
+  if (want >= n0) {  // fewer prompt tokens than the rank: no threshold (every key is an inlier)
+    if (threadIdx.x < 64)
+      (reinterpret_cast<float2 *>(sd.kmeta) + (size_t)h * D)[c0 + threadIdx.x] = make_float2(0.f, 0.f);
+    return;
   }
-  const float inv = tau > 0.f ? __fdiv_rn(1.0f, tau) : 0.f;
-  (reinterpret_cast<float2 *>(sd.kmeta) + (size_t)h * D)[c] = make_float2(tau, inv);
+  if (threadIdx.x < 64) s_rem[threadIdx.x] = (uint32_t)want + 1;  // 1-based rank
+  const uint16_t *kc = k + (size_t)h * D + c0 + lane;
+  const size_t tstride = (size_t)Hkv * D;
+  for (int pass = 0; pass < 2; ++pass) {
+    for (int e = threadIdx.x; e < 64 * 257; e += kCalibThreads) (&hist[0][0])[e] = 0u;
+    __syncthreads();
+    const uint32_t sel = pass == 0 ? 0u : s_sel[lane];
+    for (int t0 = wave; t0 < n0; t0 += NW * kCalibBatch) {
+      uint32_t key[kCalibBatch];
+#pragma unroll
+      for (int b = 0; b < kCalibBatch; ++b)
+        key[b] = (uint32_t)gld(kc + (size_t)min(t0 + b * NW, n0 - 1) * tstride) & 0x7FFFu;
+#pragma unroll
+      for (int b = 0; b < kCalibBatch; ++b) {
+        if (t0 + b * NW >= n0) break;
+        if (pass == 0) atomicAdd(&hist[lane][key[b] >> 8], 1u);
+        else if ((key[b] >> 8) == sel) atomicAdd(&hist[lane][key[b] & 255u], 1u);
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x < 64) {
+      const int c = threadIdx.x;
+      const uint32_t remaining = s_rem[c];
+      uint32_t cum = 0;
+      int dg = 0;
+      for (int bb = 255; bb >= 0; --bb) {
+        if (cum + hist[c][bb] >= remaining) {
+          dg = bb;
+          break;
+        }
+        cum += hist[c][bb];
+      }
+      s_rem[c] = remaining - cum;
+      if (pass == 0) {
+        s_sel[c] = (uint32_t)dg;
+      } else {
+        const float tau = h2f((s_sel[c] << 8) | (uint32_t)dg);
+        const float inv = tau > 0.f ? __fdiv_rn(1.0f, tau) : 0.f;
+        (reinterpret_cast<float2 *>(sd.kmeta) + (size_t)h * D)[c0 + c] = make_float2(tau, inv);
+      }
+    }
+    __syncthreads();
+  }
 }
 
 // KVQ prompt keys, pass 1 (write codes, count outliers per token into krow[t+1]) or pass 2
@@ -693,7 +727,7 @@ hipError_t prefill_impl(const Dev &dv, const Shape &sh, const SeqDesc &hs, int s
       hipLaunchKernelGGL(k_prefill_uq_keys<D>, dim3(n0 / 64 + 1, Hkv), dim3(D), 0, st, dv.seqs, seq, k, Hkv, n0);
       break;
     case KVQ:
-      hipLaunchKernelGGL(k_kvq_calibrate<D>, dim3(Hkv), dim3(D), 0, st, dv.seqs, seq, k, Hkv, n0);
+      hipLaunchKernelGGL(k_kvq_calibrate<D>, dim3(Hkv, D / 64), dim3(kCalibThreads), 0, st, dv.seqs, seq, k, Hkv, n0);
       hipLaunchKernelGGL(k_kvq_keys<D>, dim3(n0, Hkv), dim3(D), 0, st, dv.seqs, seq, k, dv.cbtab, Hkv, 0);
       hipLaunchKernelGGL(k_kvq_scan, dim3(Hkv), dim3(256), 0, st, dv.seqs, seq, dv.state, Hkv, n0);
       hipLaunchKernelGGL(k_kvq_keys<D>, dim3(n0, Hkv), dim3(D), 0, st, dv.seqs, seq, k, dv.cbtab, Hkv, 1);

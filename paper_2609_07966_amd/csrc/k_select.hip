@@ -13,27 +13,6 @@ namespace {
 
 constexpr int NT = 256;
 
-// Compact positions [0, n) whose flag is set into ascending slots; calls emit(j, slot) for each.
-// flag(j, eq_before) may use eq_before = number of keys equal to the threshold at indices < j.
-template <typename Flag, typename IsEq, typename Emit>
-MKV_DEV int compact_ascending(int n, Flag flag, IsEq is_eq, Emit emit, int *s_tmp) {
-  int run = 0, eq_run = 0;
-  for (int a = 0; a < n; a += NT) {
-    const int j = a + (int)threadIdx.x;
-    const bool in = j < n;
-    const int e = (in && is_eq(j)) ? 1 : 0;
-    int eq_tot;
-    const int eq_before = eq_run + block_exclusive_scan<NT>(e, s_tmp, &eq_tot);
-    const int f = (in && flag(j, eq_before)) ? 1 : 0;
-    int tot;
-    const int ex = block_exclusive_scan<NT>(f, s_tmp, &tot);
-    if (f) emit(j, run + ex);
-    run += tot;
-    eq_run += eq_tot;
-  }
-  return run;
-}
-
 // ---- RocketKV decode top-k ---------------------------------------------------------------------
 // One workgroup of kTopkThreads threads per (sequence, kv head) over the tokens already appended
 // (a decode step instead spreads the scores over several workgroups, in k_append.hip).
@@ -250,13 +229,13 @@ __global__ __launch_bounds__(NT) void k_h2o_colsums(const SeqDesc *__restrict__ 
 }
 
 // Keep the R most recent prompt tokens plus the top B - R scores of the rest (newer on ties),
-// compact them into slots 0..kept-1 in ascending position order.
+// gathered into slots 0..kept-1 in ascending position order.  The selection runs over the
+// candidates in reverse order (index ncand - 1 - j), so that its lower-index tie rule prefers
+// newer tokens; its ascending output, reversed, is ascending in position.
 template <int D>
-__global__ __launch_bounds__(NT) void k_h2o_keep(const SeqDesc *__restrict__ seqs, int seq, int32_t *state,
-                                                 int Hkv) {
-  __shared__ int hist[256];
-  __shared__ int s3[3];
-  __shared__ int s_tmp[NT / 64];
+__global__ __launch_bounds__(kTopkThreads) void k_h2o_keep(const SeqDesc *__restrict__ seqs, int seq, int32_t *state,
+                                                           int Hkv) {
+  __shared__ SelLds L;
   const SeqDesc &sd = seqs[seq];
   const int h = blockIdx.x, n0 = sd.n0;
   const float *S = reinterpret_cast<const float *>(sd.aux0) + (size_t)h * n0;
@@ -264,37 +243,36 @@ __global__ __launch_bounds__(NT) void k_h2o_keep(const SeqDesc *__restrict__ seq
   const bool all = B >= n0;
   const int ncand = all ? 0 : n0 - R;
   const int H = all ? 0 : B - R;
-  uint32_t kth = 0xFFFFFFFFu;
-  int n_eq = 0, need = 0;
-  if (H > 0) radix_select_kth<NT>(ncand, H, [&](int i) { return float_key(S[i]); }, hist, s3, &kth, &n_eq, &need);
+  const int kept = all ? n0 : min(B, sd.cap);
+  int32_t *pos = reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd);
+  if (all) {
+    for (int j = threadIdx.x; j < n0; j += kTopkThreads) pos[j] = j;
+  } else {
+    if (H > 0) {
+      // the scratch of the row statistics (no longer needed) takes the reversed selection
+      int32_t *rsel = reinterpret_cast<int32_t *>(sd.aux1) + (size_t)h * n0;
+      select_keys<kTopkThreads, 32>(ncand, H, [&](int i) { return float_key(gld(S + (ncand - 1 - i))); }, rsel, L);
+      __syncthreads();
+      for (int i = threadIdx.x; i < H; i += kTopkThreads) pos[H - 1 - i] = ncand - 1 - gld(rsel + i);
+    }
+    for (int i = threadIdx.x; i < R; i += kTopkThreads) pos[H + i] = ncand + i;
+  }
+  __syncthreads();
   const uint16_t *sk = reinterpret_cast<const uint16_t *>(sd.stage_k) + h * stride_stage(sd, D);
   const uint16_t *sv = reinterpret_cast<const uint16_t *>(sd.stage_v) + h * stride_stage(sd, D);
   uint16_t *dk = reinterpret_cast<uint16_t *>(sd.k) + h * stride_rows(sd, D);
   uint16_t *dvv = reinterpret_cast<uint16_t *>(sd.v) + h * stride_rows(sd, D);
-  int32_t *pos = reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd);
   float *score = reinterpret_cast<float *>(sd.score) + h * stride_slots(sd);
-  const int kept = compact_ascending(
-      n0,
-      [&](int j, int eq_before) {
-        if (all || j >= ncand) return true;
-        if (H == 0) return false;
-        const uint32_t kk = float_key(S[j]);
-        return kk > kth || (kk == kth && eq_before >= n_eq - need);
-      },
-      [&](int j) { return !all && H > 0 && j < ncand && float_key(S[j]) == kth; },
-      [&](int j, int slot) {
-        if (slot >= sd.cap) return;
-        pos[slot] = j;
-        score[slot] = S[j];
-        for (int c = 0; c < D; c += 8) {
-          *reinterpret_cast<uint4 *>(dk + (size_t)slot * D + c) = *reinterpret_cast<const uint4 *>(sk + (size_t)j * D + c);
-          *reinterpret_cast<uint4 *>(dvv + (size_t)slot * D + c) = *reinterpret_cast<const uint4 *>(sv + (size_t)j * D + c);
-        }
-      },
-      s_tmp);
+  for (int it = threadIdx.x; it < kept * (D / 8); it += kTopkThreads) {
+    const int slot = it / (D / 8), u = it % (D / 8);
+    const int j = gld(pos + slot);
+    *reinterpret_cast<uint4 *>(dk + (size_t)slot * D + 8 * u) = gld16(sk + (size_t)j * D + 8 * u);
+    *reinterpret_cast<uint4 *>(dvv + (size_t)slot * D + 8 * u) = gld16(sv + (size_t)j * D + 8 * u);
+    if (u == 0) score[slot] = gld(S + j);
+  }
   // no eviction candidates before the first attention pass
   uint32_t *vb = reinterpret_cast<uint32_t *>(sd.vbest) + (size_t)h * sd.vparts * 4;
-  for (int p = threadIdx.x; p < sd.vparts; p += NT) {
+  for (int p = threadIdx.x; p < sd.vparts; p += kTopkThreads) {
     vb[4 * p] = 0xFFFFFFFFu;
     vb[4 * p + 1] = 0xFFFFFFFFu;
     vb[4 * p + 2] = 0xFFFFFFFFu;
@@ -309,167 +287,243 @@ __global__ __launch_bounds__(NT) void k_h2o_keep(const SeqDesc *__restrict__ seq
 }
 
 // ---- SnapKV prefill -------------------------------------------------------------------------------
-// Window row r = i * G + g (query head h*G + g at position n0 - w + i).  Pass 1: per 256-key chunk
-// and wave, the partial (max, sum of exp2) of every row.  Pass 2: merge, then votes of the
-// chunk's keys.  Pass 3: pool, select, compact.
-constexpr int SNAP_CHUNK = 256;
+// Window row r = i * G + g (query head h*G + g at position n0 - w + i; it attends to keys
+// 0 .. n0 - w + i).  Pass 1: per 256-key chunk and wave, the partial (max, sum of exp2) of every
+// row, from v_mfma_f32_16x16x32_f16 logit tiles.  Pass 2: each row's partials merged.  Pass 3: the
+// votes of a chunk's keys, the logits recomputed on the matrix cores.  Pass 4: max pooling into
+// order-preserving keys.  Pass 5: select, gather the kept rows.
+constexpr int SNAP_CHUNK = 256;  // keys per workgroup: 64 per wave, 4 key tiles of 16
+constexpr int SNAP_ROWS = 64;    // window rows staged in LDS at a time (4 row tiles of 16)
 
+// The window rows [r0, r0 + 64) (clamped to the last row) as fp16 operands in LDS.
 template <int D>
-MKV_DEV void load_key_row(const uint16_t *ks, int j, int n0, float *kr) {
-  if (j < n0) {
-#pragma unroll
-    for (int c = 0; c < D; c += 8) {
-      const uint4 u = *reinterpret_cast<const uint4 *>(ks + (size_t)j * D + c);
-      unpack8(u, kr + c);
-    }
-  } else {
-#pragma unroll
-    for (int c = 0; c < D; ++c) kr[c] = 0.f;
-  }
-}
-
-template <int D>
-MKV_DEV void load_window(float (*sq)[D], const uint16_t *qw, int h, int G, int Hq, int w, int wfull,
-                         int r0, int nr) {
-  for (int e = threadIdx.x; e < nr * D; e += NT) {
-    const int rr = e / D, c = e % D;
-    const int r = r0 + rr, i = r / G, g = r % G;
+MKV_DEV void stage_window(uint4 (*sq)[D / 8 + 1], const uint16_t *qw, int h, int G, int Hq, int w, int wfull,
+                          int rows, int r0) {
+  constexpr int U = D / 8;
+  for (int e = threadIdx.x; e < SNAP_ROWS * U; e += NT) {
+    const int rr = e / U, u = e % U;
+    const int r = min(r0 + rr, rows - 1), i = r / G, g = r % G;
     // the last w of the `wfull` window rows
-    sq[rr][c] = h2f(qw[((size_t)(wfull - w + i) * Hq + h * G + g) * D + c]);
+    sq[rr][u] = gld16(reinterpret_cast<const uint4 *>(qw + ((size_t)(wfull - w + i) * Hq + h * G + g) * D) + u);
   }
 }
 
-constexpr int SNAP_ROWS = 64;   // window rows staged in LDS at a time
+// A wave's 4 key tiles (16 keys each) of the chunk as matrix operands: key 16 n + lr, channels
+// 8 lq .. 8 lq + 7 of k-step s.
+template <int D>
+MKV_DEV void snap_key_operands(const uint16_t *ks, int key0, int n0, uint4 (&kop)[4][D / 32]) {
+  constexpr int U = D / 8;
+  const int lane = threadIdx.x & 63, lr = lane & 15, lq = lane >> 4;
+#pragma unroll
+  for (int n = 0; n < 4; ++n)
+#pragma unroll
+    for (int s = 0; s < D / 32; ++s)
+      kop[n][s] = gld16(reinterpret_cast<const uint4 *>(ks) + (size_t)min(key0 + 16 * n + lr, n0 - 1) * U + 4 * s + lq);
+}
 
 template <int D>
 __global__ __launch_bounds__(NT) void k_snap_rowstats(const SeqDesc *__restrict__ seqs, int seq,
                                                       const uint16_t *__restrict__ qw, int Hq, int G,
                                                       float scale2) {
-  __shared__ float sq[SNAP_ROWS][D];
+  constexpr int KS = D / 32;
+  __shared__ uint4 sq[SNAP_ROWS][D / 8 + 1];
   const SeqDesc &sd = seqs[seq];
   const int n0 = sd.n0, w = sd.w_eff, wfull = sd.window;
   const int chunk = blockIdx.x, h = blockIdx.y;
   const int nchunk = (n0 + SNAP_CHUNK - 1) / SNAP_CHUNK;
-  const int j = chunk * SNAP_CHUNK + (int)threadIdx.x;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const uint16_t *ks = reinterpret_cast<const uint16_t *>(sd.stage_k) + h * stride_stage(sd, D);
-  float kr[D];
-  load_key_row<D>(ks, j, n0, kr);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, lr = lane & 15, lq = lane >> 4;
+  const int key0 = chunk * SNAP_CHUNK + 64 * wave;
+  uint4 kop[4][KS];
+  snap_key_operands<D>(reinterpret_cast<const uint16_t *>(sd.stage_k) + h * stride_stage(sd, D), key0, n0, kop);
   const int rows = w * G;
   float2 *part = reinterpret_cast<float2 *>(sd.aux1) + (size_t)h * rows * nchunk * 4;
   for (int r0 = 0; r0 < rows; r0 += SNAP_ROWS) {
-    const int nr = min(SNAP_ROWS, rows - r0);
     __syncthreads();
-    load_window<D>(sq, qw, h, G, Hq, w, wfull, r0, nr);
+    stage_window<D>(sq, qw, h, G, Hq, w, wfull, rows, r0);
     __syncthreads();
-    for (int rr = 0; rr < nr; ++rr) {
-      const int r = r0 + rr, i = r / G;
-      const int posr = n0 - w + i;
-      float acc = 0.f;
+#pragma unroll 1
+    for (int t = 0; t < SNAP_ROWS / 16 && r0 + 16 * t < rows; ++t) {
+      float v[4][4];
 #pragma unroll
-      for (int c = 0; c < D; ++c) acc = fmaf(sq[rr][c], kr[c], acc);
-      const float s = (j <= posr && j < n0) ? acc * scale2 : -INFINITY;
-      const float M = wave_max(s);
-      const float L = wave_sum(M == -INFINITY ? 0.f : exp2f(s - M));
-      if (lane == 0) part[((size_t)r * nchunk + chunk) * 4 + wave] = make_float2(M, L);
+      for (int n = 0; n < 4; ++n) {
+        f4v S = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) S = mfma_k32(sq[16 * t + lr][4 * s + lq], kop[n][s], S);
+        const int key = key0 + 16 * n + lr;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = r0 + 16 * t + 4 * lq + j, posr = n0 - w + r / G;
+          v[n][j] = (key <= posr && key < n0) ? S[j] * scale2 : -INFINITY;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float M = row16_max(fmaxf(fmaxf(v[0][j], v[1][j]), fmaxf(v[2][j], v[3][j])));
+        float e = 0.f;
+        if (M != -INFINITY) {
+#pragma unroll
+          for (int n = 0; n < 4; ++n) e += fexp2(v[n][j] - M);  // arguments <= 0
+        }
+        const float L = row16_sum(e);
+        const int r = r0 + 16 * t + 4 * lq + j;
+        if (lr == 0 && r < rows) part[((size_t)r * nchunk + chunk) * 4 + wave] = make_float2(M, L);
+      }
     }
   }
 }
 
+// Merge each window row's 4 nchunk partials (one wave per row); entry 0 of the row then holds
+// (max, sum of exp2) over all its keys.
+template <int D>
+__global__ __launch_bounds__(NT) void k_snap_merge(const SeqDesc *__restrict__ seqs, int seq, int G) {
+  const SeqDesc &sd = seqs[seq];
+  const int n0 = sd.n0, rows = sd.w_eff * G, h = blockIdx.y;
+  const int nchunk = (n0 + SNAP_CHUNK - 1) / SNAP_CHUNK, np = 4 * nchunk;
+  const int lane = threadIdx.x & 63, r = blockIdx.x * (NT / 64) + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  float2 *pr = reinterpret_cast<float2 *>(sd.aux1) + ((size_t)h * rows + r) * np;
+  float m = -INFINITY, l = 0.f;
+  for (int e = lane; e < np; e += 64) {
+    const float xm = gld(reinterpret_cast<const float *>(pr + e)), xl = gld(reinterpret_cast<const float *>(pr + e) + 1);
+    if (xm == -INFINITY) continue;
+    const float mx = fmaxf(m, xm);
+    l = l * fexp2(m - mx) + xl * fexp2(xm - mx);  // arguments <= 0 (m = -inf gives 0)
+    m = mx;
+  }
+  const float M = wave_max(m);
+  const float L = wave_sum(m == -INFINITY ? 0.f : l * fexp2(m - M));
+  if (lane == 0) pr[0] = make_float2(M, L);
+}
+
+// Votes of a chunk's keys: sum over the window rows of exp2(s - M_r) / L_r.
 template <int D>
 __global__ __launch_bounds__(NT) void k_snap_votes(const SeqDesc *__restrict__ seqs, int seq,
                                                    const uint16_t *__restrict__ qw, int Hq, int G,
                                                    float scale2) {
-  __shared__ float sq[SNAP_ROWS][D];
-  __shared__ float2 sml[SNAP_ROWS];
+  constexpr int KS = D / 32;
+  __shared__ uint4 sq[SNAP_ROWS][D / 8 + 1];
+  __shared__ float2 sml[SNAP_ROWS];  // (M, 1 / L) of the staged rows
   const SeqDesc &sd = seqs[seq];
   const int n0 = sd.n0, w = sd.w_eff, wfull = sd.window;
   const int chunk = blockIdx.x, h = blockIdx.y;
   const int nchunk = (n0 + SNAP_CHUNK - 1) / SNAP_CHUNK;
-  const int j = chunk * SNAP_CHUNK + (int)threadIdx.x;
-  const uint16_t *ks = reinterpret_cast<const uint16_t *>(sd.stage_k) + h * stride_stage(sd, D);
-  float kr[D];
-  load_key_row<D>(ks, j, n0, kr);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, lr = lane & 15, lq = lane >> 4;
+  const int key0 = chunk * SNAP_CHUNK + 64 * wave;
+  uint4 kop[4][KS];
+  snap_key_operands<D>(reinterpret_cast<const uint16_t *>(sd.stage_k) + h * stride_stage(sd, D), key0, n0, kop);
   const int rows = w * G;
   const float2 *part = reinterpret_cast<const float2 *>(sd.aux1) + (size_t)h * rows * nchunk * 4;
-  float vote = 0.f;
+  float col[4] = {0.f, 0.f, 0.f, 0.f};
   for (int r0 = 0; r0 < rows; r0 += SNAP_ROWS) {
-    const int nr = min(SNAP_ROWS, rows - r0);
     __syncthreads();
-    load_window<D>(sq, qw, h, G, Hq, w, wfull, r0, nr);
-    for (int rr = threadIdx.x; rr < nr; rr += NT) {
-      const float2 *pp = part + (size_t)(r0 + rr) * nchunk * 4;
-      float M = -INFINITY;
-      for (int e = 0; e < nchunk * 4; ++e) M = fmaxf(M, pp[e].x);
-      float L = 0.f;
-      for (int e = 0; e < nchunk * 4; ++e)
-        if (pp[e].x != -INFINITY) L += pp[e].y * exp2f(pp[e].x - M);
-      sml[rr] = make_float2(M, L);
+    stage_window<D>(sq, qw, h, G, Hq, w, wfull, rows, r0);
+    if (threadIdx.x < SNAP_ROWS) {
+      const float *ml = reinterpret_cast<const float *>(part + (size_t)min(r0 + (int)threadIdx.x, rows - 1) * nchunk * 4);
+      sml[threadIdx.x] = make_float2(gld(ml), 1.f / gld(ml + 1));
     }
     __syncthreads();
-    for (int rr = 0; rr < nr; ++rr) {
-      const int r = r0 + rr, i = r / G;
-      const int posr = n0 - w + i;
-      float acc = 0.f;
+#pragma unroll 1
+    for (int t = 0; t < SNAP_ROWS / 16 && r0 + 16 * t < rows; ++t) {
 #pragma unroll
-      for (int c = 0; c < D; ++c) acc = fmaf(sq[rr][c], kr[c], acc);
-      if (j <= posr && j < n0) vote += exp2f(acc * scale2 - sml[rr].x) / sml[rr].y;
+      for (int n = 0; n < 4; ++n) {
+        f4v S = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) S = mfma_k32(sq[16 * t + lr][4 * s + lq], kop[n][s], S);
+        const int key = key0 + 16 * n + lr;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int rr = 16 * t + 4 * lq + j, r = r0 + rr, posr = n0 - w + r / G;
+          // arguments <= 0 wherever the row statistics hold this logit
+          if (r < rows && key <= posr && key < n0) col[n] += fexp2(S[j] * scale2 - sml[rr].x) * sml[rr].y;
+        }
+      }
     }
   }
-  if (j < n0 - w) (reinterpret_cast<float *>(sd.aux0) + (size_t)h * n0)[j] = vote;
+  float *votes = reinterpret_cast<float *>(sd.aux0) + (size_t)h * n0;
+#pragma unroll
+  for (int n = 0; n < 4; ++n) {
+    float x = col[n];
+    x += __shfl_xor(x, 16);
+    x += __shfl_xor(x, 32);
+    const int key = key0 + 16 * n + lr;
+    if (lq == 0 && key < n0 - w) votes[key] = x;
+  }
 }
 
+// Max pooling of the candidates' votes (odd kernel `pool`, clipped to [0, n0 - w)) into
+// order-preserving keys, one thread per candidate.
+__global__ __launch_bounds__(NT) void k_snap_pool(const SeqDesc *__restrict__ seqs, int seq) {
+  const SeqDesc &sd = seqs[seq];
+  const int n0 = sd.n0, ncand = n0 - sd.w_eff, h = blockIdx.y, half = sd.pool / 2;
+  const int j = blockIdx.x * NT + (int)threadIdx.x;
+  if (j >= ncand) return;
+  const float *votes = reinterpret_cast<const float *>(sd.aux0) + (size_t)h * n0;
+  float m = gld(votes + j);
+  const int lo = max(0, j - half), hi = min(ncand - 1, j + half);
+  for (int x = lo; x <= hi; ++x) m = fmaxf(m, gld(votes + x));
+  gst(reinterpret_cast<uint32_t *>(sd.aux1) + (size_t)h * n0 + j, float_key(m));
+}
+
+// Keep the T - w highest pooled votes among the candidates (lower position on a tie) and the w
+// window tokens; gather their rows (and the channel-major key copy) into slots 0..kept-1 in
+// ascending position order.
 template <int D>
-__global__ __launch_bounds__(NT) void k_snap_keep(const SeqDesc *__restrict__ seqs, int seq, int32_t *state,
-                                                  int Hkv) {
-  __shared__ int hist[256];
-  __shared__ int s3[3];
-  __shared__ int s_tmp[NT / 64];
+__global__ __launch_bounds__(kTopkThreads) void k_snap_keep(const SeqDesc *__restrict__ seqs, int seq,
+                                                            int32_t *state, int Hkv) {
+  __shared__ SelLds L;
   const SeqDesc &sd = seqs[seq];
   const int h = blockIdx.x, n0 = sd.n0, w = sd.w_eff;
   const bool all = sd.T >= n0;
-  const int ncand = all ? 0 : n0 - w;
-  const int want = all ? 0 : sd.T - w;
-  const float *votes = reinterpret_cast<const float *>(sd.aux0) + (size_t)h * n0;
-  const int half = sd.pool / 2;
-  auto pooled = [&](int j) {
-    float m = votes[j];
-    const int lo = max(0, j - half), hi = min(ncand - 1, j + half);
-    for (int x = lo; x <= hi; ++x) m = fmaxf(m, votes[x]);
-    return float_key(m);
-  };
-  uint32_t kth = 0xFFFFFFFFu;
-  int n_eq = 0, need = 0;
-  if (want > 0) radix_select_kth<NT>(ncand, want, pooled, hist, s3, &kth, &n_eq, &need);
+  const int ncand = n0 - w, want = sd.T - w;
+  const int kept = all ? n0 : sd.T;
+  int32_t *pos = reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd);
+  if (all) {
+    for (int j = threadIdx.x; j < n0; j += kTopkThreads) pos[j] = j;
+  } else {
+    if (want > 0) {
+      const uint32_t *keys = reinterpret_cast<const uint32_t *>(sd.aux1) + (size_t)h * n0;
+      select_keys<kTopkThreads, 32>(ncand, want, [&](int j) { return gld(keys + j); }, pos, L);
+    }
+    for (int i = threadIdx.x; i < w; i += kTopkThreads) pos[want + i] = ncand + i;
+  }
+  __syncthreads();
+  // gather: item (16-byte chunk u, slot) with slots consecutive across lanes, so the 2-byte
+  // stores into the channel-major copy are coalesced
   const uint16_t *sk = reinterpret_cast<const uint16_t *>(sd.stage_k) + h * stride_stage(sd, D);
   const uint16_t *sv = reinterpret_cast<const uint16_t *>(sd.stage_v) + h * stride_stage(sd, D);
   uint16_t *dk = reinterpret_cast<uint16_t *>(sd.k) + h * stride_rows(sd, D);
   uint16_t *dvv = reinterpret_cast<uint16_t *>(sd.v) + h * stride_rows(sd, D);
   uint16_t *kcm = reinterpret_cast<uint16_t *>(sd.kcm) + h * stride_kcm(sd, D);
-  int32_t *pos = reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd);
-  const int cap = sd.cap, cstride = sd.cstride;
-  const int kept = compact_ascending(
-      n0,
-      [&](int j, int eq_before) {
-        if (all || j >= ncand) return true;
-        if (want == 0) return false;
-        const uint32_t kk = pooled(j);
-        return kk > kth || (kk == kth && eq_before < need);
-      },
-      [&](int j) { return !all && want > 0 && j < ncand && pooled(j) == kth; },
-      [&](int j, int slot) {
-        if (slot >= cap) return;
-        pos[slot] = j;
-        for (int c = 0; c < D; c += 8) {
-          const uint4 a = *reinterpret_cast<const uint4 *>(sk + (size_t)j * D + c);
-          *reinterpret_cast<uint4 *>(dk + (size_t)slot * D + c) = a;
-          *reinterpret_cast<uint4 *>(dvv + (size_t)slot * D + c) = *reinterpret_cast<const uint4 *>(sv + (size_t)j * D + c);
-          const uint32_t wv[4] = {a.x, a.y, a.z, a.w};
+  const int cstride = sd.cstride, total = kept * (D / 8);
+  // batches of kGather items per thread: every position and row load in flight before the stores
+  constexpr int kGather = 8;
+  for (int base = threadIdx.x; base < total; base += kGather * kTopkThreads) {
+    int jj[kGather];
+    uint4 a[kGather], b[kGather];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) kcm[(size_t)(c + e) * cstride + slot] = (uint16_t)(wv[e / 2] >> (16 * (e & 1)));
-        }
-      },
-      s_tmp);
+    for (int q = 0; q < kGather; ++q) {
+      const int it = min(base + q * kTopkThreads, total - 1);
+      jj[q] = gld(pos + it % kept);
+    }
+#pragma unroll
+    for (int q = 0; q < kGather; ++q) {
+      const int u = min(base + q * kTopkThreads, total - 1) / kept;
+      a[q] = gld16(sk + (size_t)jj[q] * D + 8 * u);
+      b[q] = gld16(sv + (size_t)jj[q] * D + 8 * u);
+    }
+#pragma unroll
+    for (int q = 0; q < kGather; ++q) {
+      const int it = base + q * kTopkThreads;
+      if (it >= total) break;
+      const int u = it / kept, slot = it % kept;
+      *reinterpret_cast<uint4 *>(dk + (size_t)slot * D + 8 * u) = a[q];
+      *reinterpret_cast<uint4 *>(dvv + (size_t)slot * D + 8 * u) = b[q];
+      const uint32_t wv[4] = {a[q].x, a[q].y, a[q].z, a[q].w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        kcm[(size_t)(8 * u + e) * cstride + slot] = (uint16_t)(wv[e / 2] >> (16 * (e & 1)));
+    }
+  }
   if (threadIdx.x == 0) {
     int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
     st[ST_COUNT] = kept;
@@ -490,9 +544,11 @@ hipError_t h2o_prefill_impl(const Dev &dv, const Shape &sh, const SeqDesc &hs, i
                             hipStream_t st) {
   const float scale2 = kLog2e / sqrtf((float)D);
   const int nb = (hs.n0 + TB - 1) / TB;
+  // one query head per workgroup: sharing a staged key tile among several heads of a kv head was
+  // measured slower (fewer, longer workgroups at lower occupancy)
   hipLaunchKernelGGL(k_h2o_rowstats<D>, dim3(nb, sh.Hq), dim3(NT), 0, st, dv.seqs, seq, q, sh.Hq, sh.G, scale2);
   hipLaunchKernelGGL(k_h2o_colsums<D>, dim3(nb, sh.Hkv), dim3(NT), 0, st, dv.seqs, seq, q, sh.Hq, sh.G, scale2);
-  hipLaunchKernelGGL(k_h2o_keep<D>, dim3(sh.Hkv), dim3(NT), 0, st, dv.seqs, seq, dv.state, sh.Hkv);
+  hipLaunchKernelGGL(k_h2o_keep<D>, dim3(sh.Hkv), dim3(kTopkThreads), 0, st, dv.seqs, seq, dv.state, sh.Hkv);
   return hipGetLastError();
 }
 
@@ -501,13 +557,16 @@ hipError_t snap_prefill_impl(const Dev &dv, const Shape &sh, const SeqDesc &hs, 
                              hipStream_t st) {
   const float scale2 = kLog2e / sqrtf((float)D);
   if (hs.T < hs.n0) {
-    const int nchunk = (hs.n0 + SNAP_CHUNK - 1) / SNAP_CHUNK;
+    const int nchunk = (hs.n0 + SNAP_CHUNK - 1) / SNAP_CHUNK, rows = hs.w_eff * sh.G;
     hipLaunchKernelGGL(k_snap_rowstats<D>, dim3(nchunk, sh.Hkv), dim3(NT), 0, st, dv.seqs, seq, qw, sh.Hq, sh.G,
                        scale2);
+    hipLaunchKernelGGL(k_snap_merge<D>, dim3((rows + NT / 64 - 1) / (NT / 64), sh.Hkv), dim3(NT), 0, st, dv.seqs,
+                       seq, sh.G);
     hipLaunchKernelGGL(k_snap_votes<D>, dim3(nchunk, sh.Hkv), dim3(NT), 0, st, dv.seqs, seq, qw, sh.Hq, sh.G,
                        scale2);
+    hipLaunchKernelGGL(k_snap_pool, dim3((hs.n0 - hs.w_eff + NT - 1) / NT, sh.Hkv), dim3(NT), 0, st, dv.seqs, seq);
   }
-  hipLaunchKernelGGL(k_snap_keep<D>, dim3(sh.Hkv), dim3(NT), 0, st, dv.seqs, seq, dv.state, sh.Hkv);
+  hipLaunchKernelGGL(k_snap_keep<D>, dim3(sh.Hkv), dim3(kTopkThreads), 0, st, dv.seqs, seq, dv.state, sh.Hkv);
   return hipGetLastError();
 }
 

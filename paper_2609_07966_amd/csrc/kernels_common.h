@@ -176,44 +176,4 @@ MKV_DEV int block_exclusive_scan(int x, int *tmp, int *total) {
   return base + inc - x;
 }
 
-// Block-wide radix select over n 32-bit keys read through `get(i)`: returns the k-th largest key
-// (1 <= k <= n), the number of keys equal to it, and how many of those equal keys are needed
-// to make k.  `hist` is 256 ints of LDS, `shared3` 3 ints of LDS.
-template <int NT, typename Get>
-MKV_DEV void radix_select_kth(int n, int k, Get get, int *hist, int *shared3, uint32_t *kth,
-                              int *n_equal, int *need) {
-  uint32_t prefix = 0, mask = 0;
-  int remaining = k;
-  int eq = 0;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    for (int i = threadIdx.x; i < 256; i += NT) hist[i] = 0;
-    __syncthreads();
-    for (int i = threadIdx.x; i < n; i += NT) {
-      uint32_t key = get(i);
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      int cum = 0, dg = 0;
-      for (int d = 255; d >= 0; --d) {
-        if (cum + hist[d] >= remaining) { dg = d; break; }
-        cum += hist[d];
-      }
-      shared3[0] = dg;
-      shared3[1] = remaining - cum;
-      shared3[2] = hist[dg];
-    }
-    __syncthreads();
-    prefix |= (uint32_t)shared3[0] << shift;
-    mask |= 255u << shift;
-    remaining = shared3[1];
-    eq = shared3[2];
-    __syncthreads();
-  }
-  *kth = prefix;
-  *n_equal = eq;
-  *need = remaining;
-}
-
 }  // namespace mkv

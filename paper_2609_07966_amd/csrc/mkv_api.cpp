@@ -247,7 +247,7 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
         d.stage_k = take(H * n0 * D * 2);
         d.stage_v = take(H * n0 * D * 2);
         d.aux0 = take(H * n0 * 4);
-        d.aux1 = take(std::max(H * d.w_eff * G * nchunk * 4 * 8, H * D * 4));
+        d.aux1 = take(std::max({H * d.w_eff * G * nchunk * 4 * 8, H * D * 4, H * n0 * 4}));
         d.q_off = q_rk;
         q_rk += c.window;
         break;

@@ -22,7 +22,7 @@ constexpr int kScoreTokens = kScoreTokensPerPart;  // tokens per scoring workgro
 static_assert(kScoreTokens == 4 * kScoreThreads, "a scoring thread takes 4 tokens");
 constexpr int kTopkLdsKeys = 10240;  // stand-alone top-k: score keys of up to this many tokens in LDS
 constexpr int kTopkHists = 4;        // digit histograms; waves w, w + 4, w + 8, ... share one
-constexpr int kRegKeys = 8;          // keys a selecting thread holds in registers
+constexpr int kRegKeys = 8;          // keys a decode-step selecting thread holds in registers
 
 // The channel pick of a workgroup of NTH threads.
 template <int D, int NTH>
@@ -155,26 +155,27 @@ MKV_DEV void score_tokens(const uint16_t *kcm, int cstride, int j0, int nch, con
 // The k largest of the n keys src(j) (1 <= k < n; order-preserving keys, ties to the lower
 // index) by a workgroup of NTH threads: their indices go to sel[0..k) in ascending order.
 // Thread t owns the run [t per, t per + per) (per = ceil(n / NTH)) and holds its keys in
-// registers when per <= kRegKeys (else re-reads src in every pass).  The k-th key comes from 4
-// radix passes of 8 bits: digit counts go to kTopkHists LDS histograms by atomics, and wave 0
+// registers when per <= KR (else re-reads src in every pass).  The k-th key comes from 4
+// radix passes of 8 bits: digit counts go to kTopkHists LDS histograms by atomics (one per run of
+// equal digits in a thread's keys), and wave 0
 // finds the digit by a scan over lanes while the other waves clear the next pass's histogram set
 // (2 barriers per pass).  Then counts of keys above and equal to the threshold before each run,
 // by one block scan, place every thread's selected indices.  Keys written by other threads of the
 // workgroup must be visible on entry.
-template <int NTH, typename Src>
+template <int NTH, int KR = kRegKeys, typename Src>
 MKV_DEV void select_keys(int n, int k, Src src, int32_t *sel, SelLds &L) {
   const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
   const int per = (n + NTH - 1) / NTH;
   const int ja = min(n, tid * per), m = min(n, ja + per) - ja;
-  const bool regs = per <= kRegKeys;  // block-uniform
-  uint32_t kr[kRegKeys];
+  const bool regs = per <= KR;  // block-uniform
+  uint32_t kr[KR];
 #pragma unroll
-  for (int u = 0; u < kRegKeys; ++u) kr[u] = (regs && u < m) ? src(ja + u) : 0u;
+  for (int u = 0; u < KR; ++u) kr[u] = (regs && u < m) ? src(ja + u) : 0u;
   // f(u, key) over this thread's keys in index order
   auto each = [&](auto f) {
     if (regs) {
 #pragma unroll
-      for (int u = 0; u < kRegKeys; ++u)
+      for (int u = 0; u < KR; ++u)
         if (u < m) f(u, kr[u]);
     } else {
       for (int u = 0; u < m; ++u) f(u, src(ja + u));
@@ -187,9 +188,21 @@ MKV_DEV void select_keys(int n, int k, Src src, int32_t *sel, SelLds &L) {
   for (int pass = 0; pass < 4; ++pass) {
     const int buf = pass & 1, shift = 24 - 8 * pass;
     int *hw = L.hist[buf][wid % kTopkHists];
+    // a thread's consecutive keys often share the digit (the leading digits of similar scores
+    // coincide): one atomic per run of equal digits
+    int run_d = 0, run_c = 0;
     each([&](int, uint32_t key) {
-      if ((key & mask) == prefix) atomicAdd(&hw[(key >> shift) & 255u], 1);
+      if ((key & mask) == prefix) {
+        const int d = (int)((key >> shift) & 255u);
+        if (run_c > 0 && d != run_d) {
+          atomicAdd(&hw[run_d], run_c);
+          run_c = 0;
+        }
+        run_d = d;
+        ++run_c;
+      }
     });
+    if (run_c > 0) atomicAdd(&hw[run_d], run_c);
     __syncthreads();
     if (wid == 0) {
       // lane l owns digits 255 - 4l .. 252 - 4l (descending), so the exclusive scan over lanes
