@@ -89,10 +89,12 @@ int tile_tokens(const SeqDesc &s, int D, double tile_bytes) {
 
 // Tile size: large tiles amortise each workgroup's set-up, but a launch needs several
 // workgroups per slot (256 CUs x 3 resident workgroups) to balance: about 4 rounds, within
-// 64 to 192 KiB (measured best for batches of ~40 MB and ~600 MB per step).
+// 64 to 192 KiB (measured best for batches of ~40 MB and ~600 MB per step); then adjusted to
+// whole rounds (below).
+constexpr int kTileSlots = 256 * 3;  // resident attention workgroups (3 per CU)
 double tile_bytes_for(double total_bytes) {
-  constexpr double kSlots = 256 * 3, kRounds = 4;
-  return std::min(196608.0, std::max(65536.0, total_bytes / (kSlots * kRounds)));
+  constexpr double kRounds = 4;
+  return std::min(196608.0, std::max(65536.0, total_bytes / (kTileSlots * kRounds)));
 }
 
 mkv_status check_shape(const mkv_shape *sh) {
@@ -264,19 +266,43 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
     const SeqDesc &d = L->seqs[s];
     total += (double)Hkv * (d.method == ROCKET ? d.topk : d.cap) * token_bytes(d, D);
   }
-  const double tile_bytes = tile_bytes_for(total);
+  // a sequence's tokens per tile and tile count at a given tile size
+  auto split = [&](const SeqDesc &d, double tb, int *chunk) {
+    const int amax = d.method == ROCKET ? d.topk : d.cap;
+    int c = tile_tokens(d, D, tb), n = std::max(1, (amax + c - 1) / c);
+    if (n > kMaxTiles) {  // long sequences: fewer, larger tiles keep the combine short
+      c = (((amax + kMaxTiles - 1) / kMaxTiles) + 63) & ~63;
+      n = (amax + c - 1) / c;
+    }
+    *chunk = c;
+    return n;
+  };
+  auto count_at = [&](double tb) {
+    long long n = 0;
+    int c;
+    for (int s = 0; s < S; ++s) n += (long long)Hkv * split(L->seqs[s], tb, &c);
+    return n;
+  };
+  // whole rounds of resident workgroups: when the size rule leaves the last round partly idle,
+  // smaller tiles (down to 16 KiB) fill it, the smallest size whose count still fits in the
+  // rounds begun.  (Fewer, larger tiles to drop a nearly empty last round were measured worse:
+  // H2O-40 alone 32.3 against 29.5 us.)
+  double tile_bytes = tile_bytes_for(total);
+  {
+    const long long cap = (count_at(tile_bytes) + kTileSlots - 1) / kTileSlots * kTileSlots;
+    for (double tb = 16384.0; tb < tile_bytes; tb *= 1.02)
+      if (count_at(tb) <= cap) {
+        tile_bytes = tb;
+        break;
+      }
+  }
   for (int pass = 0; pass < 2; ++pass)
   for (int s = 0; s < S; ++s) {
     SeqDesc &d = L->seqs[s];
     const int grp = d.method == ROCKET ? 1 : 0;
     if (grp != pass) continue;
     const int amax = d.method == ROCKET ? d.topk : d.cap;
-    d.chunk = tile_tokens(d, D, tile_bytes);
-    d.tile_count = std::max(1, (amax + d.chunk - 1) / d.chunk);
-    if (d.tile_count > kMaxTiles) {  // long sequences: fewer, larger tiles keep the combine short
-      d.chunk = (((amax + kMaxTiles - 1) / kMaxTiles) + 63) & ~63;
-      d.tile_count = (amax + d.chunk - 1) / d.chunk;
-    }
+    d.tile_count = split(d, tile_bytes, &d.chunk);
     d.tile_first = (int)L->tiles.size();
     for (int h = 0; h < Hkv; ++h)
       for (int t = 0; t < d.tile_count; ++t)
