@@ -81,7 +81,9 @@ double token_bytes(const SeqDesc &s, int D) {
   }
 }
 
-// Tokens per attention tile for a tile of about `tile_bytes`.
+// Tokens per attention tile for a tile of about `tile_bytes` (a multiple of 64: tiles of 32-token
+// granularity, which filled the slots of small launches more finely, were measured slower on the
+// FP16, uniform 4-bit, H2O and RocketKV per-configuration launches).
 int tile_tokens(const SeqDesc &s, int D, double tile_bytes) {
   const int t = (int)(tile_bytes / token_bytes(s, D)) & ~63;
   return std::max(64, std::min(t, 4096));

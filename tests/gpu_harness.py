@@ -72,7 +72,7 @@ def _keep_set_tie_ok(scores, gpu_keep, ora_keep, protected):
 class Run:
     """One GPU cache and its oracle twins for a workload."""
 
-    def __init__(self, wl, steps, tile_tokens=None, device="cuda", fused=False):
+    def __init__(self, wl, steps, device="cuda", fused=False):
         import torch
         from paper_2609_07966_amd.cache import KVCache
         self.torch = torch
