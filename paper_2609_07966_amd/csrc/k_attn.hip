@@ -14,10 +14,11 @@
 // two codes (codebook entries are fp16 values); its key thresholds are folded into q and its
 // value scales into p, both of which are fp32: their fp16 rounding residual rides in the spare
 // columns G..2G-1 of the same product and is added back after it.  Outliers are sparse
-// corrections, applied without LDS atomics (measured slower here than plain read-modify-write):
-// the terms of a batch's key outliers are computed by the whole wave at once, one entry per
-// lane, and summed per token from LDS; value outliers accumulate in LDS rows private to each
-// lane and are folded into the output at the end.
+// corrections: the logit terms of a batch's key outliers are computed by the whole wave at once,
+// one entry per lane, into LDS and summed per token by the token's lane (LDS atomics measured
+// slower there); value outliers add p (x - s cb[code]) to the wave's per-head LDS rows by LDS
+// atomics (private rows per lane with read-modify-write measured slower there), folded into the
+// output at the end.
 //
 // Uniform 4-bit tiles run the same matrix loop: 4-bit codes become exact fp16 integers, each
 // 64-token block's key steps are folded into q, each token's value steps into p, and the minima
