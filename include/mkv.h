@@ -223,7 +223,8 @@ mkv_status mkv_decode_attention_noalloc(mkv_cache *cache, const uint16_t *q, flo
  * Graph capture: the step enqueues three or four kernels on `stream` (the
  * append, with the scores when RocketKV sequences are present; their
  * selection; attention partial; combine) and nothing else (no allocation,
- * copy, memset or synchronization; profiling events only when enabled), and every per-step quantity (counts, positions, H2O victims,
+ * copy, memset or synchronization; profiling events only when enabled), and
+ * every per-step quantity (counts, positions, H2O eviction candidates,
  * outlier fills) lives in device state, so a captured step may be replayed
  * any number of times with new k, v, q written into the captured buffers.
  * The host-side step count then no longer follows the device: capacity is
