@@ -816,7 +816,9 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   const SeqDesc &sd = seqs[seq];
   const int method = sd.method;
   const int32_t *st = state + ((size_t)seq * Hkv + h) * ST_WORDS;
-  const int n_act = (method == ROCKET) ? st[ST_SEL_COUNT] : st[ST_COUNT];
+  // both counts are read alongside the descriptor (not after it), then chosen by method
+  const int n_cnt = st[ST_COUNT], n_sel = st[ST_SEL_COUNT];
+  const int n_act = (method == ROCKET) ? n_sel : n_cnt;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int Hq = Hkv * G;
   const uint16_t *qh = q + ((size_t)seq * Hq + h * G) * D;
@@ -824,56 +826,82 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   const int lr = lane & 15, lq = lane >> 4;
   const bool kvq = method == KVQ;
   const bool uq = method == UQ;
-  if (uq) {
-    for (int e = threadIdx.x; e < G * D; e += kTileThreads) {
-      const int g = e / D, c = e % D;
-      s_q[c][g] = h2f(qh[(size_t)g * D + c]) * qscale;
+  // Set-up: every global read of the tile's set-up is issued before any of it is used (the
+  // reads are independent, so the tile waits for one round trip, not one per read).
+  constexpr int kQI = (G * D + kTileThreads - 1) / kTileThreads;  // q elements per thread
+  // both lookup tables of a codebook take at most 256 uint4 (the 2-bit quad tables)
+  static_assert(kTileThreads >= 256, "one uint4 of the lookup tables per thread");
+  if (uq || kvq) {
+    uint16_t qv[kQI];
+    float tv[kQI];
+#pragma unroll
+    for (int i = 0; i < kQI; ++i) {
+      const int e = min((int)threadIdx.x + i * kTileThreads, G * D - 1);
+      qv[i] = qh[(size_t)(e / D) * D + e % D];
     }
-  }
-  if (kvq) {
-    // the codebook's lookup tables (copied as built on the host), the key codebook, and q,
-    // q * tau for this kv head
-    const int bits = sd.bits, nc = 1 << bits;
-    const uint32_t *lut = reinterpret_cast<const uint32_t *>(cbtab + kLutBase) + lut_offset(bits);
-    for (int e = threadIdx.x; e < lut_half_words(bits) / 2; e += kTileThreads)
-      reinterpret_cast<uint4 *>(s_lut)[e] = gld16(lut + 4 * e);
-    if (threadIdx.x < 16) s_cbk[threadIdx.x] = threadIdx.x < nc ? cbtab[cb_offset(bits) + threadIdx.x] : 0.f;
-    const float *tau = reinterpret_cast<const float *>(sd.kmeta) + (size_t)h * D * 2;
-    for (int e = threadIdx.x; e < G * D; e += kTileThreads) {
-      const int g = e / D, c = e % D;
-      const float qx = h2f(qh[(size_t)g * D + c]) * qscale;
-      s_q[c][g] = qx;
-      s_q[c][G + g] = qx * gld(tau + 2 * c);
+    uint4 lv = make_uint4(0u, 0u, 0u, 0u);
+    int nlut = 0;
+    float cbv = 0.f;
+    if (kvq) {
+      // tau per channel, the codebook's lookup tables (copied as built on the host) and the key
+      // codebook
+      const float *tau = reinterpret_cast<const float *>(sd.kmeta) + (size_t)h * D * 2;
+#pragma unroll
+      for (int i = 0; i < kQI; ++i) tv[i] = gld(tau + 2 * ((threadIdx.x + i * kTileThreads) % D));
+      const int bits = sd.bits, nc = 1 << bits;
+      const uint32_t *lut = reinterpret_cast<const uint32_t *>(cbtab + kLutBase) + lut_offset(bits);
+      nlut = lut_half_words(bits) / 2;
+      if ((int)threadIdx.x < nlut) lv = gld16(lut + 4 * threadIdx.x);
+      if (threadIdx.x < 16 && (int)threadIdx.x < nc) cbv = cbtab[cb_offset(bits) + threadIdx.x];
+      // cleared per-wave outlier rows
+      float4 *vz = reinterpret_cast<float4 *>(&s_wave[wave][0]);
+      for (int e = lane; e < kWaveFloats / 4; e += 64) vz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+      float4 *kz = reinterpret_cast<float4 *>(&s_kc[wave][0][0]);
+      for (int e = lane; e < (G + 1) * 36 / 4; e += 64) kz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if ((int)threadIdx.x < nlut) reinterpret_cast<uint4 *>(s_lut)[threadIdx.x] = lv;
+      if (threadIdx.x < 16) s_cbk[threadIdx.x] = cbv;
     }
-    float4 *vz = reinterpret_cast<float4 *>(&s_wave[wave][0]);
-    for (int e = lane; e < kWaveFloats / 4; e += 64) vz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
-    float4 *kz = reinterpret_cast<float4 *>(&s_kc[wave][0][0]);
-    for (int e = lane; e < (G + 1) * 36 / 4; e += 64) kz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+    // q of each head (scaled), and for KVQuant q * tau
+#pragma unroll
+    for (int i = 0; i < kQI; ++i) {
+      const int e = threadIdx.x + i * kTileThreads;
+      if (e < G * D) {
+        const int g = e / D, c = e % D;
+        const float qx = h2f(qv[i]) * qscale;
+        s_q[c][g] = qx;
+        if (kvq) s_q[c][G + g] = qx * tv[i];
+      }
+    }
   }
   __syncthreads();
   // q.k operand B: query head lr, channels CPL*lq + 4m .. +3 (KVQuant: fp16 part of the scaled
   // q' in columns g < G, its residual in columns 2G-1-g)
   QB<D> qb;
+  if (kvq) {
+    const int g = lr < G ? lr : lr < 2 * G ? 2 * G - 1 - lr : 0;
 #pragma unroll
-  for (int m = 0; m < NM; ++m) {
-    uint32_t w[2] = {0u, 0u};
-    const int c = kvq ? CPL * lq + 4 * m : 32 * (m / 2) + 8 * lq + 4 * (m % 2);
-    if (kvq) {
-      if (lr < 2 * G) {
-        const int g = lr < G ? lr : 2 * G - 1 - lr;
+    for (int m = 0; m < NM; ++m) {
+      const int c = CPL * lq + 4 * m;
+      uint32_t w[2];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const float x0 = s_q[c + 2 * j][G + g], x1 = s_q[c + 2 * j + 1][G + g];
-          const float h0 = (float)(_Float16)x0, h1 = (float)(_Float16)x1;
-          w[j] = lr < G ? pk_f16(h0, h1) : pk_f16(x0 - h0, x1 - h1);
-        }
+      for (int j = 0; j < 2; ++j) {
+        const float x0 = s_q[c + 2 * j][G + g], x1 = s_q[c + 2 * j + 1][G + g];
+        const float h0 = (float)(_Float16)x0, h1 = (float)(_Float16)x1;
+        w[j] = lr < G ? pk_f16(h0, h1) : lr < 2 * G ? pk_f16(x0 - h0, x1 - h1) : 0u;
       }
-    } else if (lr < G) {
-      const uint32_t *qp = reinterpret_cast<const uint32_t *>(qh + (size_t)lr * D + c);
-      w[0] = gld(qp);
-      w[1] = gld(qp + 1);
+      qb.b[m] = mk_h4(w[0], w[1]);
     }
-    qb.b[m] = mk_h4(w[0], w[1]);
+  } else {
+    uint32_t w[NM][2];
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      const int c = 32 * (m / 2) + 8 * lq + 4 * (m % 2);
+      const uint32_t *qp = reinterpret_cast<const uint32_t *>(qh + (size_t)min(lr, G - 1) * D + c);
+      w[m][0] = gld(qp);  // lanes lr >= G read head G - 1 and drop it
+      w[m][1] = gld(qp + 1);
+    }
+#pragma unroll
+    for (int m = 0; m < NM; ++m) qb.b[m] = lr < G ? mk_h4(w[m][0], w[m][1]) : mk_h4(0u, 0u);
   }
   float m_run = -INFINITY, l_part = 0.f;
   float uq_om[D / 64];  // uniform 4-bit: sum p mn per value group (summed over the lane quads)
