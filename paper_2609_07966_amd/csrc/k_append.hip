@@ -165,10 +165,14 @@ MKV_DEV void store_quad(const SeqDesc &sd, int h, int t0, const uint32_t *s_blk,
   for (int w = threadIdx.x; w < words; w += D) gst(dst + w, s_blk[w]);
 }
 
-// KVQ key of one token: code under the frozen per-channel threshold, and the outlier flag.
-MKV_DEV int kvq_key_code(const SeqDesc &sd, int h, int c, uint32_t kbits, const float *cbtab, int D,
-                         bool *outl) {
-  const float2 ti = (reinterpret_cast<const float2 *>(sd.kmeta) + (size_t)h * D)[c];
+// The frozen (threshold, 1 / threshold) pair of KVQ key channel c of kv head h.
+MKV_DEV float2 kvq_key_tau(const SeqDesc &sd, int h, int c, int D) {
+  return (reinterpret_cast<const float2 *>(sd.kmeta) + (size_t)h * D)[c];
+}
+
+// KVQ key of one token: code under the frozen per-channel threshold ti (kvq_key_tau), and the
+// outlier flag.
+MKV_DEV int kvq_key_code(const SeqDesc &sd, float2 ti, uint32_t kbits, const float *cbtab, bool *outl) {
   const float x = h2f(kbits);
   const float xhat = __fmul_rn(x, ti.y);
   const int nc = 1 << sd.bits;
@@ -284,16 +288,18 @@ MKV_DEV void append_pair(const SeqDesc &sd, int32_t *st, int seq, int h, int Hkv
   int *s_tmp = L.tmp;
   uint32_t *s_blk = L.blk;
   const int c = threadIdx.x;
+  // reads that need only the work item or the descriptor are issued first
+  const uint32_t kb = k[((size_t)seq * Hkv + h) * D + c];
+  const uint32_t vb = v[((size_t)seq * Hkv + h) * D + c];
+  const float2 ti = sd.method == KVQ ? kvq_key_tau(sd, h, c, D) : make_float2(0.f, 0.f);
+  const int count = st[ST_COUNT], pos = st[ST_NEXT_POS], kfill = st[ST_KOUT_FILL];
   for (int i = c; i < kCbTableFloats; i += D) s_cbt[i] = cbtab[i];
-  const int count = st[ST_COUNT], pos = st[ST_NEXT_POS];
   // H2O: an eviction decided by the last attention pass frees its slot for this token (-1: none)
   const int victim = sd.method == H2O ? h2o_victim<D>(sd, h, L) : -1;
   const int slot = sd.method == H2O ? (victim >= 0 ? victim : st[ST_FREE_SLOT]) : count;
   // a full region (reachable only by replaying a captured decode step past max_new_tokens) drops
   // the token instead of writing past the region; the decision is the same for every thread
-  if (slot >= sd.cap || (sd.method == KVQ && sd.bp > 0 && st[ST_KOUT_FILL] + D > sd.pool_cap)) return;
-  const uint32_t kb = k[((size_t)seq * Hkv + h) * D + c];
-  const uint32_t vb = v[((size_t)seq * Hkv + h) * D + c];
+  if (slot >= sd.cap || (sd.method == KVQ && sd.bp > 0 && kfill + D > sd.pool_cap)) return;
   __syncthreads();  // every thread has read the state before thread 0 updates it
   switch (sd.method) {
     case FP16: {
@@ -350,12 +356,12 @@ MKV_DEV void append_pair(const SeqDesc &sd, int32_t *st, int seq, int h, int Hkv
     }
     case KVQ: {
       bool outl;
-      const int code = kvq_key_code(sd, h, c, kb, s_cbt, D, &outl);
+      const int code = kvq_key_code(sd, ti, kb, s_cbt, &outl);
       uint8_t *row = reinterpret_cast<uint8_t *>(sd.kc) + h * stride_codes(sd) + (size_t)count * sd.rowbytes;
       pack_row<D>(code, sd.bits, s_code, row);
       int total;
       const int r = flag_rank<D>(outl, s_tmp, &total);
-      const int fill = st[ST_KOUT_FILL];
+      const int fill = kfill;
       uint32_t *ko = reinterpret_cast<uint32_t *>(sd.kout) + h * stride_kout(sd);
       if (outl) ko[fill + r] = outlier_entry(kb, count, code, c);
       const int vcode = kvq_value_token<D>(sd, h, count, vb, s_cbt, s_abs, &L.scale, s_tmp);
@@ -432,6 +438,9 @@ __global__ __launch_bounds__(kScoreThreads) void k_append_score(const SeqDesc *_
     append_pair<D>(sd, st, seq, h, Hkv, k, v, cbtab, L.a);
     return;
   }
+  // the query channels first: their address needs only the work item
+  uint16_t qr[G];
+  load_qcol<D, G>(q + ((size_t)seq * Hkv * G + h * G) * D, qr);
   const int count = st[ST_COUNT];
   // a full region (reachable only by replaying a captured decode step past max_new_tokens) drops
   // the token, as the separate append does
@@ -447,7 +456,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_append_score(const SeqDesc *_
       if (c == 0) (reinterpret_cast<int32_t *>(sd.pos) + h * stride_slots(sd))[count] = st[ST_NEXT_POS];
     }
   }
-  score_part<D, G>(sd, seq, h, Hkv, room ? count + 1 : count, part, room, q, L.c);
+  score_part<D, G>(sd, h, room ? count + 1 : count, part, room, qr, L.c);
 }
 
 template <int D>
@@ -608,7 +617,7 @@ __global__ __launch_bounds__(128) void k_kvq_keys(const SeqDesc *__restrict__ se
   const int t = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
   const uint32_t kb = k[((size_t)t * Hkv + h) * D + c];
   bool outl;
-  const int code = kvq_key_code(sd, h, c, kb, cbtab, D, &outl);
+  const int code = kvq_key_code(sd, kvq_key_tau(sd, h, c, D), kb, cbtab, &outl);
   uint32_t *krow = reinterpret_cast<uint32_t *>(sd.krow) + h * stride_krow(sd);
   if (pass == 0) {
     uint8_t *row = reinterpret_cast<uint8_t *>(sd.kc) + h * stride_codes(sd) + (size_t)t * sd.rowbytes;

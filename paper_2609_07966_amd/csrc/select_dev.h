@@ -49,23 +49,33 @@ struct TopkLds {
   uint32_t keys[kTopkLdsKeys];
 };
 
-// The nch channels of kv head h's query group qh (G rows of D fp16) into L.sel_ch / L.sel_qb in
-// ascending channel order; returns nch.  Ends with a barrier.
+// Query channel tid (tid < D; other threads read channel D - 1 and ignore it) of each of the G
+// rows of the kv head's query group qh; loaded by the caller before anything it waits on.
+template <int D, int G>
+MKV_DEV void load_qcol(const uint16_t *qh, uint16_t (&qr)[G]) {
+  const int c = min((int)threadIdx.x, D - 1);
+#pragma unroll
+  for (int g = 0; g < G; ++g) qr[g] = gld(qh + (size_t)g * D + c);
+}
+
+// The nch channels of a kv head's query group (thread c < D holds channel c of its G rows, from
+// load_qcol) into L.sel_ch / L.sel_qb in ascending channel order; returns nch.  Ends with a
+// barrier.
 template <int D, int G, int NTH>
-MKV_DEV int channel_pick(const SeqDesc &sd, const uint16_t *qh, ChanLds<D, NTH> &L) {
+MKV_DEV int channel_pick(const SeqDesc &sd, const uint16_t (&qr)[G], ChanLds<D, NTH> &L) {
   static_assert(NTH % D == 0, "whole slices per channel");
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   // channel magnitudes and head sums, float32 in ascending head order
-  for (int c = tid; c < D; c += NTH) {
+  if (tid < D) {
     float a = 0.f, qb = 0.f;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const float x = h2f(gld(qh + (size_t)g * D + c));
+      const float x = h2f(qr[g]);
       a = __fadd_rn(a, fabsf(x));
       qb = __fadd_rn(qb, x);
     }
-    L.a[c] = a;
-    L.qb[c] = qb;
+    L.a[tid] = a;
+    L.qb[tid] = qb;
   }
   __syncthreads();
   const int nch = min(sd.nch, D);
@@ -262,15 +272,15 @@ MKV_DEV void select_keys(int n, int k, Src src, int32_t *sel, SelLds &L) {
 
 // ---- a decode step's scoring workgroups -----------------------------------------------------------
 // Part `part` of a RocketKV (sequence, kv head) with n retained tokens (the new one included):
-// the channel pick (every part makes it; part 0 also writes it out) and the scores of tokens
-// [part kScoreTokens, (part + 1) kScoreTokens), as keys into the head's global key array.
+// the channel pick (every part makes it, from the query channels qr; part 0 also writes it out)
+// and the scores of tokens [part kScoreTokens, (part + 1) kScoreTokens), as keys into the
+// head's global key array.
 // L.knew must hold the new token's key (token n - 1) when `has_new`; the pick's barriers publish it.
 template <int D, int G>
-MKV_DEV void score_part(const SeqDesc &sd, int seq, int h, int Hkv, int n, int part, bool has_new, const uint16_t *q,
+MKV_DEV void score_part(const SeqDesc &sd, int h, int n, int part, bool has_new, const uint16_t (&qr)[G],
                         ChanLds<D, kScoreThreads> &L) {
   const int tid = threadIdx.x;
-  const uint16_t *qh = q + ((size_t)seq * Hkv * G + h * G) * D;
-  const int nch = channel_pick<D, G, kScoreThreads>(sd, qh, L);
+  const int nch = channel_pick<D, G, kScoreThreads>(sd, qr, L);
   if (part == 0)
     for (int i = tid; i < nch; i += kScoreThreads) (reinterpret_cast<int32_t *>(sd.aux1) + (size_t)h * D)[i] = L.sel_ch[i];
   if (sd.topk >= n) return;  // every token is selected; no scores needed
@@ -296,8 +306,9 @@ MKV_DEV void topk_pair(const SeqDesc &sd, int32_t *st, int seq, int h, int Hkv, 
   const int k = sd.topk;
   int32_t *sel = reinterpret_cast<int32_t *>(sd.sel) + h * stride_sel(sd);
   const int32_t *pos = reinterpret_cast<const int32_t *>(sd.pos) + h * stride_slots(sd);
-  const uint16_t *qh = q + ((size_t)seq * Hkv * G + h * G) * D;
-  const int nch = channel_pick<D, G, NTH>(sd, qh, L.c);
+  uint16_t qr[G];
+  load_qcol<D, G>(q + ((size_t)seq * Hkv * G + h * G) * D, qr);
+  const int nch = channel_pick<D, G, NTH>(sd, qr, L.c);
   for (int i = tid; i < nch; i += NTH) (reinterpret_cast<int32_t *>(sd.aux1) + (size_t)h * D)[i] = L.c.sel_ch[i];
   if (k >= n) {
     for (int j = tid; j < n; j += NTH) sel[j] = j;
