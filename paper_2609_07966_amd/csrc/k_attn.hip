@@ -416,12 +416,24 @@ struct MKVQ {
   }
 };
 
-// the 4-bit nibbles k and k + 4 of w as a packed pair of fp16 integers: each becomes the fp16
-// value 1024 + n by an and-or, then n by one packed fp16 subtraction (both exact)
+// (x & mask) | bits in one instruction (the compiler splits it in two when both are literals)
+MKV_DEV uint32_t and_or(uint32_t x, uint32_t mask, uint32_t bits) {
+  uint32_t r;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "s"(mask), "v"(bits));
+  return r;
+}
+
+// the 4-bit nibbles k and k + 4 of w as a packed pair of fp16 integers: one and-or sets each
+// nibble into the mantissa of an fp16 base (1024 for a nibble at the foot of its 16-bit half, 64
+// for one 4 bits up; nibbles 2, 3, 6 and 7 after a shift by 8), then one packed fp16 subtraction
+// removes the base (both exact)
 MKV_DEV uint32_t nib_pair(uint32_t w, int k) {
-  const h2v x = __builtin_bit_cast(h2v, ((w >> (4 * k)) & 0x000F000Fu) | 0x64006400u);
-  const h2v off = {(_Float16)1024.0f, (_Float16)1024.0f};
-  return __builtin_bit_cast(uint32_t, x - off);
+  const uint32_t x = k >= 2 ? w >> 8 : w;
+  const bool up = k & 1;
+  const h2v v = __builtin_bit_cast(h2v, and_or(x, up ? 0x00F000F0u : 0x000F000Fu, up ? 0x54005400u : 0x64006400u));
+  const _Float16 base = up ? (_Float16)64.0f : (_Float16)1024.0f;
+  const h2v off = {base, base};
+  return __builtin_bit_cast(uint32_t, v - off);
 }
 
 // Uniform 4-bit (64-token key blocks with per-channel min and step; per-token value groups of
