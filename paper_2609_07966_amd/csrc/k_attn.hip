@@ -457,7 +457,11 @@ struct MUQ {
   const float *qs;                        // LDS [D][2G]: scaled q in columns 0..G-1
   float2 *vm;                             // LDS [32 * NGRP]: this wave's batch of value (min, step)
   float *km;                              // LDS [D][2]: this wave's key block (min, step) pairs
+  static constexpr int SROW = D + 4;      // staging row stride (halves): rows start 2 banks apart
+  _Float16 *stg;                          // LDS [2G][SROW]: this wave's q'' staging rows
   int lr, lq, prole, cur_blk;
+  int next_blk;                           // the block whose (min, step) pairs `next_km` holds
+  U4 next_km;                             // lanes l < D / 2: channels 2l, 2l + 1 of that block
   float kbias;                            // sum q mn of head lr for the current block
   float om[NGRP];                         // sum p mn of head lr per value group
   struct Raw {
@@ -494,20 +498,59 @@ struct MUQ {
     if (blk == cur_blk) return;
     cur_blk = blk;
     if (!RES) {
-      // stage the block's (min, step) pairs: lane l takes channels 2l and 2l + 1
+      // stage the block's (min, step) pairs, lane l taking channels 2l and 2l + 1 (loaded one
+      // block ahead, the first on demand), then load the next block's (the last complete block
+      // of the range at most)
       const int l = threadIdx.x & 63;
       if (l < D / 2) {
-        const U4 u = gld16u(kmeta + ((size_t)blk * D + 2 * l) * 2);
+        const U4 u = next_blk == blk ? next_km : gld16u(kmeta + ((size_t)blk * D + 2 * l) * 2);
+        next_blk = min(blk + 1, (bend - 1) >> 6);
+        next_km = gld16u(kmeta + ((size_t)next_blk * D + 2 * l) * 2);
         float4 *dst = reinterpret_cast<float4 *>(km + 4 * l);
         *dst = make_float4(__builtin_bit_cast(float, u.x), __builtin_bit_cast(float, u.y),
                            __builtin_bit_cast(float, u.z), __builtin_bit_cast(float, u.w));
       }
     }
-    // the head whose part this column carries (columns >= 2G: any head, the operand is zero)
+    if (!RES) {
+      // q'' = q st of every (channel, head) computed once: lane l takes head l % G and channels
+      // l / G + (64 / G) i, writes the fp16 part and the residual of each into the wave's
+      // staging rows (row g: head g's parts, row 2G-1-g: its residuals; each row in operand
+      // order, so that lane quad lq reads operand m as 4 halves at CPL lq + 4m), and sums
+      // q mn over its channels; the sums of a head meet by xor shuffles among the lanes of the
+      // same l % G, which include lane lr = g of every quad
+      constexpr int LPH = 64 / G, NCH = D / LPH;  // lanes per head, channels per lane
+      const int l = threadIdx.x & 63, g = l % G, k0 = l / G;
+      float bias = 0.f;
+#pragma unroll
+      for (int i = 0; i < NCH; ++i) {
+        const int c = k0 + LPH * i;
+        const float q = qs[c * 2 * G + g];
+        const float2 ms = *reinterpret_cast<const float2 *>(km + 2 * c);
+        const float x = q * ms.y;
+        bias += q * ms.x;
+        const float hv = (float)(_Float16)x;
+        const _Float16 rv = (_Float16)(x - hv);
+        // operand position of channel c: quad c / CPL, then (m, j) with kofs(m, j) = c % CPL
+        const int d = c % CPL;
+        const int pos = (c / CPL) * CPL + 4 * (2 * (d >> 3) + ((d >> 1) & 1)) + 2 * (d & 1) + ((d >> 2) & 1);
+        stg[g * SROW + pos] = (_Float16)hv;
+        stg[(2 * G - 1 - g) * SROW + pos] = rv;
+      }
+#pragma unroll
+      for (int o = G; o < 64; o *= 2) bias += __shfl_xor(bias, o);
+      kbias = lr < G ? bias : 0.f;
+      const _Float16 *row = stg + min(lr, 2 * G - 1) * SROW + CPL * lq;
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        const h4v v = *reinterpret_cast<const h4v *>(row + 4 * m);
+        qb.b[m] = lr < 2 * G ? v : mk_h4(0u, 0u);
+      }
+      return;
+    }
+    // the fp16 block (prepared once per range): q'' = q, in the lane's own column (the head
+    // whose part it carries; columns >= 2G: any head, the operand is zero)
     const int g = lr < G ? lr : lr < 2 * G ? 2 * G - 1 - lr : 0;
     const float *qrow = qs + CPL * lq * 2 * G + g;  // q of channel CPL*lq + d at qrow[d * 2G]
-    const float *krw = km + 2 * CPL * lq;           // (min, step) of that channel at krw[2d]
-    float bias = 0.f;
 #pragma unroll
     for (int m = 0; m < NM; ++m) {
       uint32_t w[2];
@@ -516,13 +559,7 @@ struct MUQ {
         float hv[2], rv[2];
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
-          const int d = kofs(m, 2 * h2 + e);
-          const float q = qrow[d * 2 * G];
-          float x = q;
-          if (!RES) {
-            x = q * krw[2 * d + 1];
-            bias += q * krw[2 * d];
-          }
+          const float x = qrow[kofs(m, 2 * h2 + e) * 2 * G];
           hv[e] = (float)(_Float16)x;
           rv[e] = (float)(_Float16)(x - hv[e]);
         }
@@ -531,9 +568,7 @@ struct MUQ {
       }
       qb.b[m] = mk_h4(w[0], w[1]);
     }
-    bias += __shfl_xor(bias, 16);
-    bias += __shfl_xor(bias, 32);
-    kbias = lr < G ? bias : 0.f;
+    kbias = 0.f;
   }
   template <bool FULL>
   MKV_DEV void fetch(int base, int b, int, const Carry &, Raw &r) const {
@@ -813,6 +848,7 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
   // per wave: KVQuant value-outlier terms [G][D] while the wave runs; then the wave's (max,
   // sum, o) for the merge
   constexpr int kWaveFloats = G * (D + 4);  // holds [G][D + 2] for the merge
+  static_assert(2 * G * (D + 4) * 2 <= kWaveFloats * 4, "uniform 4-bit q'' staging fits the wave region");
   __shared__ __attribute__((aligned(16))) float s_wave[NW][kWaveFloats];
   __shared__ float s_q[D][2 * G];            // KVQuant: scaled q of each head, then scaled q * tau
   __shared__ __attribute__((aligned(16))) uint32_t s_lut[1024];  // KVQuant: key, then value table
@@ -933,10 +969,12 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
       ld.qs = &s_q[0][0];
       ld.vm = s_vm[wave];
       ld.km = s_km[wave];
+      ld.stg = reinterpret_cast<_Float16 *>(&s_wave[wave][0]);
       ld.lr = lr;
       ld.lq = lq;
       ld.prole = lr < G ? 0 : lr < 2 * G ? 1 : 2;
       ld.cur_blk = -1;
+      ld.next_blk = -1;
       ld.kbias = 0.f;
     };
     MUQ<D, G, false> lq_;
