@@ -1078,7 +1078,9 @@ __global__ __launch_bounds__(kTileThreads) void k_attn_partial_mx(
     }
   }
   __syncthreads();
-  merge_waves<D, G, NW>(&s_wave[0][0], kWaveFloats, partials + (size_t)tid * G * (D + 2));
+  // the tile's partial slot (tiles launch in an order of their own)
+  const int slot = sd.tile_first + h * sd.tile_count + tile.z / sd.chunk;
+  merge_waves<D, G, NW>(&s_wave[0][0], kWaveFloats, partials + (size_t)slot * G * (D + 2));
 }
 
 // Log-sum-exp merge of one (sequence, kv head)'s tiles, and for H2O the score accumulation and the
