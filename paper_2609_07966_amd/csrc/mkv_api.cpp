@@ -269,8 +269,16 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
     total += (double)Hkv * (d.method == ROCKET ? d.topk : d.cap) * token_bytes(d, D);
   }
   // a sequence's tokens per tile and tile count at a given tile size
+  // In launches of three or more rounds of workgroups, fp16-row tiles (FP16, H2O) take twice the
+  // bytes: they are bandwidth-bound, and each tile a CU starts costs a dispatch gap (a median
+  // 2 us from one tile's end to the next one's start on that CU, measured with clock stamps), so
+  // fewer, longer row tiles leave the slots busier (mixed batch: 134.0-135.1 against 135.8-136.3
+  // us per partial launch; 1.5x and 2.5-3x no better, 0.75x 6 us slower).  Shorter launches keep
+  // them (H2O-40 alone: 32.7 against 30.3 us with doubled row tiles, half a round left over).
+  bool long_rows = false;
   auto split = [&](const SeqDesc &d, double tb, int *chunk) {
     const int amax = d.method == ROCKET ? d.topk : d.cap;
+    if (long_rows && (d.method == FP16 || d.method == H2O)) tb *= 2;
     int c = tile_tokens(d, D, tb), n = std::max(1, (amax + c - 1) / c);
     if (n > kMaxTiles) {  // long sequences: fewer, larger tiles keep the combine short
       c = (((amax + kMaxTiles - 1) / kMaxTiles) + 63) & ~63;
@@ -290,6 +298,7 @@ mkv_status make_layout(const mkv_shape *shp, const mkv_config *cfg, const int32_
   // rounds begun.  (Fewer, larger tiles to drop a nearly empty last round were measured worse:
   // H2O-40 alone 32.3 against 29.5 us.)
   double tile_bytes = tile_bytes_for(total);
+  long_rows = count_at(tile_bytes) >= 3 * kTileSlots;
   {
     const long long cap = (count_at(tile_bytes) + kTileSlots - 1) / kTileSlots * kTileSlots;
     for (double tb = 16384.0; tb < tile_bytes; tb *= 1.02)
