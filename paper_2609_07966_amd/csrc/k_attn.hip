@@ -4,7 +4,9 @@
 // (MetaKV Section 2.1): all tokens with dequantized values (uniform / KVQuant), the retained
 // set (H2O) or the selected set (RocketKV).  One launch covers all sequences: each workgroup
 // takes one tile = (sequence, kv head, token range) and runs the loop for that sequence's method;
-// the 4 waves of a workgroup split the tile's tokens into contiguous ranges.
+// the 4 waves of a workgroup split the tile's tokens into contiguous ranges.  Tiles launch in an
+// order chosen on the host (quantized tiles early, RocketKV's last), so a tile writes its partial
+// to the slot its sequence, kv head and range give, not to its launch index.
 //
 // Matrix path (fp16 rows, gathered rows, KVQuant): a wave handles 16 tokens per step with
 // v_mfma_f32_16x16x16_f16.  q.k is S^T = K Q^T (tokens x query heads; channels permuted so a
@@ -20,9 +22,10 @@
 // atomics (private rows per lane with read-modify-write measured slower there), folded into the
 // output at the end.
 //
-// Uniform 4-bit tiles run the same matrix loop: 4-bit codes become exact fp16 integers, each
-// 64-token block's key steps are folded into q, each token's value steps into p, and the minima
-// enter as per-head bias terms.
+// Uniform 4-bit tiles run the same matrix loop: 4-bit codes become exact fp16 integers (one
+// and-or and one packed subtraction per pair), each 64-token block's key steps are folded into q
+// (computed once per channel and head across the wave and staged in LDS), each token's value
+// steps into p, and the minima enter as per-head bias terms.
 //
 // Logits use the base-2 exponent (scaled by log2(e)/sqrt(d)).  fp16-row tiles keep the loads of
 // the next 16 tokens in flight while computing the current 16; the other paths issue the loads
