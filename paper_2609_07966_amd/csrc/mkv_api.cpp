@@ -426,6 +426,18 @@ mkv_status check_hip(hipError_t e, const char *what) {
 
 }  // namespace
 
+namespace mkv {
+mkv_status layout_tiles(const mkv_shape *shape, const mkv_config *cfg, const int32_t *prompt_len,
+                        std::vector<int4> *tiles, std::vector<SeqDesc> *seqs) {
+  Layout L;
+  const mkv_status st = make_layout(shape, cfg, prompt_len, &L);
+  if (st != MKV_OK) return st;
+  *tiles = L.tiles;
+  *seqs = L.seqs;
+  return MKV_OK;
+}
+}  // namespace mkv
+
 extern "C" {
 
 const char *mkv_status_str(mkv_status s) {

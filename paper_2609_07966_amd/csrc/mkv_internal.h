@@ -1,6 +1,8 @@
 // Internal layout shared by the host library and the HIP kernels.
 #pragma once
 
+#include <vector>
+
 #include <math.h>
 #include <stdint.h>
 
@@ -170,6 +172,10 @@ hipError_t launch_attention_partial(const Dev &dv, const Shape &sh, const uint16
 // on the first call per device.
 constexpr size_t kStaticScratchBytes = size_t(8) << 20;
 hipError_t static_scratch(float **ptr, size_t *bytes);
+// The attention tiles of a cache layout in launch order, and the sequences' descriptors (tile
+// bookkeeping: tile_first, tile_count, chunk); host only, for checks of the layout rules.
+mkv_status layout_tiles(const mkv_shape *shape, const mkv_config *cfg, const int32_t *prompt_len,
+                        std::vector<int4> *tiles, std::vector<SeqDesc> *seqs);
 hipError_t launch_attention_combine(const Dev &dv, const Shape &sh, float *out, hipStream_t st,
                                     LaunchEv ev = {});
 hipError_t launch_topk(const Dev &dv, const Shape &sh, const uint16_t *q, int32_t *pos_out, int topk_max,

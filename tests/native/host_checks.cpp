@@ -3,6 +3,7 @@
 // reaches a device).  Exercises arena sizing for every configuration, argument validation, the
 // KV-memory accounting, the configuration choice and the host codebook fit.  Exit status 0 when
 // every check holds.
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -101,6 +102,63 @@ int main() {
     off[2] += 1e-4f;
     CHECK(mkv_cache_create(&sh, &kv, &L, off.data(), fake, b, nullptr, &h) == MKV_EINVAL);
     CHECK(mkv_cache_destroy(nullptr) == MKV_OK);
+  }
+  // attention tile layout: every (sequence, kv head)'s ranges cover its tokens once, partial
+  // slots are distinct, RocketKV tiles launch last, and the quantized tiles are spread over the
+  // first 3/4 of the others (so about a quarter of the fp16-row tiles follow the last of them);
+  // a long mixed launch (several rounds of workgroups) and a short one
+  for (int big = 0; big < 2; ++big) {
+    const int S = big ? 64 : 6, Hkv = 8, D = 128;
+    mkv_shape sh{S, 4 * Hkv, Hkv, D, 128};
+    std::vector<mkv_config> cs(S);
+    std::vector<int32_t> pl(S);
+    uint32_t r = 777u + big;
+    for (int i = 0; i < S; ++i) {
+      cs[i] = all[i % n];
+      r = r * 1664525u + 1013904223u;
+      pl[i] = 1024 + (int)((r >> 8) % (big ? 31744u : 3000u));
+    }
+    std::vector<int4> tiles;
+    std::vector<mkv::SeqDesc> sd;
+    CHECK(mkv::layout_tiles(&sh, cs.data(), pl.data(), &tiles, &sd) == MKV_OK);
+    int expect = 0;
+    for (int i = 0; i < S; ++i) expect += Hkv * sd[i].tile_count;
+    CHECK((int)tiles.size() == expect);
+    std::vector<int> seen(tiles.size(), 0);
+    std::vector<std::vector<int>> cover(S * Hkv);
+    int last_nonrocket = -1, first_rocket = (int)tiles.size(), last_quant = -1, n_rows = 0;
+    for (int i = 0; i < (int)tiles.size(); ++i) {
+      const int4 t = tiles[i];
+      CHECK(t.x >= 0 && t.x < S && t.y >= 0 && t.y < Hkv);
+      if (!(t.x >= 0 && t.x < S && t.y >= 0 && t.y < Hkv)) continue;
+      const mkv::SeqDesc &d = sd[t.x];
+      const int amax = d.method == mkv::ROCKET ? d.topk : d.cap;
+      CHECK(d.chunk > 0 && d.chunk % 64 == 0 && t.z % d.chunk == 0);
+      CHECK(t.z < t.w && t.w == std::min(amax, t.z + d.chunk));
+      const int slot = d.tile_first + t.y * d.tile_count + t.z / d.chunk;
+      CHECK(slot >= 0 && slot < (int)tiles.size());
+      if (slot >= 0 && slot < (int)tiles.size()) ++seen[slot];
+      cover[t.x * Hkv + t.y].push_back(t.z);
+      if (d.method == mkv::ROCKET) {
+        first_rocket = std::min(first_rocket, i);
+      } else {
+        last_nonrocket = i;
+        if (d.method == mkv::KVQ || d.method == mkv::UQ) last_quant = i;
+        else ++n_rows;
+      }
+    }
+    for (int v : seen) CHECK(v == 1);
+    CHECK(last_nonrocket < first_rocket);
+    int rows_after = 0;
+    for (int i = last_quant + 1; i < first_rocket; ++i) rows_after += 1;
+    CHECK(last_quant < 0 || rows_after >= n_rows / 4 - 1);
+    for (int p = 0; p < S * Hkv; ++p) {
+      std::vector<int> z = cover[p];
+      std::sort(z.begin(), z.end());
+      const mkv::SeqDesc &d = sd[p / Hkv];
+      CHECK((int)z.size() == d.tile_count);
+      for (int j = 0; j < (int)z.size(); ++j) CHECK(z[j] == j * d.chunk);
+    }
   }
   // the configuration choice
   {
